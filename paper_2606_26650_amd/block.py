@@ -1,0 +1,381 @@
+"""One CAT-Q block-wise reconstruction step driven through the C ABI.
+
+The driver owns device buffers (torch tensors used as plain HBM allocations)
+and issues the library calls in order on one stream; it computes nothing
+itself.  The seven linears of a decoder block are stored as four fused
+matrices, q|k|v, o, gate|up and down: groups never straddle rows, so
+learnable modulation and its gradients are unchanged by the fusion, while
+the GEMMs get larger and the input gradient of q, k and v (and of gate and
+up) comes out of one contraction.
+
+Step (Sec. 2.2-2.4):
+  LM+ST of every weight (Eq. 3-6) -> block forward with alpha*T ->
+  reconstruction loss against the full-precision output on the same input
+  (Eq. 7) -> backward to the block input and to the factors of every group,
+  and (finalize) hard codes (Eq. 2) + 2-bit packing with the group scales.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from . import (BF16, HARD, IDENTITY, SOFT, attn_desc, catq_aux_attention_bwd,
+               catq_aux_attention_fwd, catq_aux_moe_combine, catq_aux_moe_combine_bwd,
+               catq_aux_moe_gather, catq_aux_moe_route, catq_aux_moe_route_workspace_bytes,
+               catq_aux_moe_scatter_add, catq_aux_rmsnorm_bwd, catq_aux_rmsnorm_fwd,
+               catq_aux_swiglu_bwd, catq_aux_swiglu_fwd, catq_attn_bwd_workspace_bytes,
+               catq_attn_saved_bytes, catq_block_recon_loss, catq_fakeq_linear_bwd,
+               catq_fakeq_linear_fwd, catq_modulate_ternarize, catq_pack_ternary,
+               catq_workspace_size, lmst_params, WS_LINEAR_BWD, WS_LOSS)
+
+DEV = "cuda"
+
+
+def bf16_tensor(bits: np.ndarray, device=DEV) -> torch.Tensor:
+    """Device bf16 tensor holding exactly the given uint16 bit patterns."""
+    t = torch.from_numpy(np.ascontiguousarray(bits).view(np.int16))
+    return t.to(device).view(torch.bfloat16)
+
+
+def empty(shape, dtype=torch.bfloat16):
+    return torch.empty(shape, dtype=dtype, device=DEV)
+
+
+class QLinear:
+    """A weight under learnable modulation: W frozen, three factor arrays
+    (per group), cached group statistics, fake weight and factor gradients.
+    ``W`` is [rows][d_in] (experts stacked along rows)."""
+
+    def __init__(self, W: torch.Tensor, d_out: int, d_in: int, g: int = 128, n_experts: int = 1):
+        self.W = W
+        self.d_out, self.d_in, self.E = d_out, d_in, n_experts
+        self.g = g
+        ng = W.numel() // g
+        self.n_groups = ng
+        self.d_mu = torch.zeros(ng, dtype=torch.float32, device=DEV)
+        self.d_alpha = torch.ones(ng, dtype=torch.float32, device=DEV)
+        self.d_delta = torch.ones(ng, dtype=torch.float32, device=DEV)
+        self.stats = torch.zeros(ng, 2, dtype=torch.float32, device=DEV)
+        self.W_fake = torch.empty_like(W)
+        self.g_mu = torch.zeros_like(self.d_mu)
+        self.g_alpha = torch.zeros_like(self.d_mu)
+        self.g_delta = torch.zeros_like(self.d_mu)
+
+    def set_factors(self, dmu, dal, dde):
+        self.d_mu.copy_(torch.as_tensor(dmu, dtype=torch.float32))
+        self.d_alpha.copy_(torch.as_tensor(dal, dtype=torch.float32))
+        self.d_delta.copy_(torch.as_tensor(dde, dtype=torch.float32))
+
+    def modulate(self, p, stats_mode, codes=None, alpha_out=None, W_fake="self"):
+        wf = self.W_fake if W_fake == "self" else W_fake
+        catq_modulate_ternarize(self.W, self.d_mu, self.d_alpha, self.d_delta, p, self.stats,
+                                stats_mode, W_fake=wf, codes=codes, alpha_out=alpha_out)
+
+
+class DenseBlock:
+    """Pre-norm decoder block (RMSNorm, fused q|k|v, QK-norm, RoPE, causal GQA
+    attention, o, residual, RMSNorm, fused gate|up, SwiGLU, down, residual)."""
+
+    def __init__(self, cfg, weights: dict, g: int = 128):
+        self.cfg = cfg
+        c = cfg
+        hd, h = c.head_dim, c.hidden
+        self.Nqkv = (c.n_q + 2 * c.n_kv) * hd
+        self.M = c.batch * c.seq
+        self.g = g
+        dev_w = {k: bf16_tensor(v) for k, v in weights.items()}
+        self.lin = {
+            "qkv": QLinear(torch.cat([dev_w["Wq"], dev_w["Wk"], dev_w["Wv"]], 0).contiguous(),
+                           self.Nqkv, h, g),
+            "o": QLinear(dev_w["Wo"], h, c.n_q * hd, g),
+            "gu": QLinear(torch.cat([dev_w["Wg"], dev_w["Wu"]], 0).contiguous(), 2 * c.ffn, h, g),
+            "d": QLinear(dev_w["Wd"], h, c.ffn, g),
+        }
+        M = self.M
+        self.desc = attn_desc(c.batch, c.seq, c.n_q, c.n_kv, hd, c.qk_norm, c.rope_theta)
+        # activations
+        self.xn1, self.rstd1 = empty((M, h)), empty((M,), torch.float32)
+        self.qkv = empty((M, self.Nqkv))
+        self.attn = empty((M, c.n_q * hd))
+        self.h1 = empty((M, h), torch.float32)      # residual stream kept in fp32
+        self.xn2, self.rstd2 = empty((M, h)), empty((M,), torch.float32)
+        self.gu = empty((M, 2 * c.ffn))
+        self.a = empty((M, c.ffn))
+        self.y = empty((M, h), torch.float32)
+        self.saved = torch.empty(catq_attn_saved_bytes(self.desc), dtype=torch.uint8, device=DEV)
+        # gradients
+        self.dy = empty((M, h))
+        self.da = empty((M, c.ffn))
+        self.dgu = empty((M, 2 * c.ffn))
+        self.dxn2 = empty((M, h))
+        self.dh1 = empty((M, h))
+        self.dattn = empty((M, c.n_q * hd))
+        self.dqkv = empty((M, self.Nqkv))
+        self.dxn1 = empty((M, h))
+        self.dx = empty((M, h))
+        self.attn_ws = torch.empty(catq_attn_bwd_workspace_bytes(self.desc), dtype=torch.uint8,
+                                   device=DEV)
+        ws = max(catq_workspace_size(WS_LINEAR_BWD, M, L.d_out, L.d_in) for L in self.lin.values())
+        self.lin_ws = torch.empty(ws, dtype=torch.uint8, device=DEV)
+        self.loss_ws = torch.empty(catq_workspace_size(WS_LOSS, M, 1, 1), dtype=torch.uint8,
+                                   device=DEV)
+        self.loss = torch.zeros(1, dtype=torch.float32, device=DEV)
+        self.stats_ready = False
+
+    # ------------------------------------------------------------------ LM+ST
+    def params(self, mode, s=15.0, s_bwd=30.0, strides=(1, 1, 1)):
+        return lmst_params(self.g, mode, 0.5, s if s else 1.0, s_bwd, strides)
+
+    def modulate_all(self, p, recompute_stats=False):
+        mode_stats = 0 if (recompute_stats or not self.stats_ready) else 1
+        for L in self.lin.values():
+            L.modulate(p, mode_stats)
+        self.stats_ready = True
+
+    # ---------------------------------------------------------------- forward
+    def forward(self, x, out=None):
+        """Block forward with the current fake weights; returns the output."""
+        c, M = self.cfg, self.M
+        h = c.hidden
+        y = self.y if out is None else out
+        catq_aux_rmsnorm_fwd(x, self.xn1, self.rstd1)
+        L = self.lin["qkv"]
+        catq_fakeq_linear_fwd(self.xn1, L.W_fake, self.qkv, M, self.Nqkv, h)
+        catq_aux_attention_fwd(self.desc, self.qkv, self.attn, self.saved)
+        L = self.lin["o"]
+        catq_fakeq_linear_fwd(self.attn, L.W_fake, self.h1, M, h, c.n_q * c.head_dim, residual=x)
+        catq_aux_rmsnorm_fwd(self.h1, self.xn2, self.rstd2)
+        L = self.lin["gu"]
+        catq_fakeq_linear_fwd(self.xn2, L.W_fake, self.gu, M, 2 * c.ffn, h)
+        catq_aux_swiglu_fwd(self.gu, self.a)
+        L = self.lin["d"]
+        catq_fakeq_linear_fwd(self.a, L.W_fake, y, M, h, c.ffn, residual=self.h1)
+        return y
+
+    def new_output(self):
+        return empty((self.M, self.cfg.hidden), torch.float32)
+
+    def target(self, x, out):
+        """Full-precision block output on the same input (IDENTITY branch)."""
+        self.modulate_all(self.params(IDENTITY))
+        return self.forward(x, out)
+
+    # --------------------------------------------------------------- backward
+    def backward(self, x, p):
+        c, M = self.cfg, self.M
+        h = c.hidden
+        ws = self.lin_ws
+
+        def lbwd(name, dY, X, dX):
+            L = self.lin[name]
+            catq_fakeq_linear_bwd(dY, X, L.W_fake, M, L.d_out, L.d_in, L.W, L.stats, L.d_mu,
+                                  L.d_alpha, L.d_delta, p, L.g_mu, L.g_alpha, L.g_delta, ws,
+                                  dX=dX)
+
+        lbwd("d", self.dy, self.a, self.da)
+        catq_aux_swiglu_bwd(self.gu, self.da, self.dgu)
+        lbwd("gu", self.dgu, self.xn2, self.dxn2)
+        catq_aux_rmsnorm_bwd(self.h1, self.rstd2, self.dxn2, self.dh1, dres=self.dy)
+        lbwd("o", self.dh1, self.attn, self.dattn)
+        catq_aux_attention_bwd(self.desc, self.qkv, self.saved, self.dattn, self.dqkv,
+                               self.attn_ws)
+        lbwd("qkv", self.dqkv, self.xn1, self.dxn1)
+        catq_aux_rmsnorm_bwd(x, self.rstd1, self.dxn1, self.dx, dres=self.dh1)
+
+    # ------------------------------------------------------------------- step
+    def step(self, x, y_fp, mode=SOFT, s=15.0, s_bwd=30.0, recompute_stats=False):
+        """LM+ST -> forward -> loss -> backward.  Loss stays on the device."""
+        p = self.params(mode, s, s_bwd)
+        self.modulate_all(p, recompute_stats)
+        self.forward(x)
+        catq_block_recon_loss(self.y, y_fp, self.loss, self.dy, self.loss_ws)
+        self.backward(x, p)
+        return self.loss
+
+    def finalize_buffers(self):
+        out = {}
+        for name, L in self.lin.items():
+            out[name] = dict(codes=torch.empty(L.W.shape, dtype=torch.int8, device=DEV),
+                             alpha=torch.empty(L.n_groups, dtype=torch.float32, device=DEV),
+                             packed=torch.empty((L.W.shape[0], L.W.shape[1] // 4),
+                                                dtype=torch.uint8, device=DEV))
+        return out
+
+    def finalize(self, bufs):
+        """Hard codes (Eq. 2), group scales and 2-bit packing of every weight."""
+        p = self.params(HARD)
+        for name, L in self.lin.items():
+            b = bufs[name]
+            L.modulate(p, 1 if self.stats_ready else 0, codes=b["codes"], alpha_out=b["alpha"],
+                       W_fake=None)
+            catq_pack_ternary(b["codes"], b["packed"])
+        self.stats_ready = True
+        return bufs
+
+    # ------------------------------------------------------------ oracle map
+    @staticmethod
+    def split_fused(cfg, name, arr):
+        """Split a fused-matrix array (rows or per-group values) into the
+        per-linear pieces, in q, k, v / gate, up order."""
+        hd = cfg.head_dim
+        if name == "qkv":
+            sizes = [cfg.n_q * hd, cfg.n_kv * hd, cfg.n_kv * hd]
+            names = ["Wq", "Wk", "Wv"]
+        elif name == "gu":
+            sizes = [cfg.ffn, cfg.ffn]
+            names = ["Wg", "Wu"]
+        elif name == "o":
+            return {"Wo": arr}
+        else:
+            return {"Wd": arr}
+        return _split_rows(arr, sizes, names)
+
+
+class MoEBlock:
+    """Decoder block whose MLP routes every token to its top-k experts (router
+    logits given, left unquantised); attention half as in DenseBlock."""
+
+    def __init__(self, cfg, weights: dict, logits: np.ndarray, g: int = 128):
+        self.cfg = c = cfg
+        hd, h = c.head_dim, c.hidden
+        self.Nqkv = (c.n_q + 2 * c.n_kv) * hd
+        self.M = c.batch * c.seq
+        self.R = self.M * c.top_k  # routed rows
+        self.g = g
+        dev_w = {k: bf16_tensor(v) for k, v in weights.items()}
+        E, F = c.n_experts, c.expert_ffn
+        self.lin = {
+            "qkv": QLinear(torch.cat([dev_w["Wq"], dev_w["Wk"], dev_w["Wv"]], 0).contiguous(),
+                           self.Nqkv, h, g),
+            "o": QLinear(dev_w["Wo"], h, c.n_q * hd, g),
+            # experts' gate|up fused per expert: [E][2F][h]
+            "gu": QLinear(torch.cat([dev_w["Wg"], dev_w["Wu"]], 1).contiguous(), 2 * F, h, g, E),
+            "d": QLinear(dev_w["Wd"].contiguous(), h, F, g, E),
+        }
+        M, R = self.M, self.R
+        self.logits = torch.from_numpy(np.ascontiguousarray(logits)).to(DEV)
+        self.desc = attn_desc(c.batch, c.seq, c.n_q, c.n_kv, hd, c.qk_norm, c.rope_theta)
+        self.ids = torch.empty((M, c.top_k), dtype=torch.int32, device=DEV)
+        self.wts = torch.empty((M, c.top_k), dtype=torch.float32, device=DEV)
+        self.perm = torch.empty((M, c.top_k), dtype=torch.int32, device=DEV)
+        self.offs = torch.empty(E + 1, dtype=torch.int64, device=DEV)
+        self.route_ws = torch.empty(catq_aux_moe_route_workspace_bytes(M, E, c.top_k),
+                                    dtype=torch.uint8, device=DEV)
+        self.xn1, self.rstd1 = empty((M, h)), empty((M,), torch.float32)
+        self.qkv = empty((M, self.Nqkv))
+        self.attn = empty((M, c.n_q * hd))
+        self.h1 = empty((M, h), torch.float32)      # residual stream kept in fp32
+        self.xn2, self.rstd2 = empty((M, h)), empty((M,), torch.float32)
+        self.xg = empty((R, h))
+        self.gu = empty((R, 2 * F))
+        self.a = empty((R, F))
+        self.yg = empty((R, h))
+        self.y = empty((M, h), torch.float32)
+        self.saved = torch.empty(catq_attn_saved_bytes(self.desc), dtype=torch.uint8, device=DEV)
+        self.dy = empty((M, h))
+        self.dyg = empty((R, h))
+        self.da = empty((R, F))
+        self.dgu = empty((R, 2 * F))
+        self.dxg = empty((R, h))
+        self.dxn2 = empty((M, h))
+        self.dh1 = empty((M, h))
+        self.dattn = empty((M, c.n_q * hd))
+        self.dqkv = empty((M, self.Nqkv))
+        self.dxn1 = empty((M, h))
+        self.dx = empty((M, h))
+        self.attn_ws = torch.empty(catq_attn_bwd_workspace_bytes(self.desc), dtype=torch.uint8,
+                                   device=DEV)
+        ws = max(catq_workspace_size(WS_LINEAR_BWD, M, self.Nqkv, h),
+                 catq_workspace_size(WS_LINEAR_BWD, M, h, c.n_q * hd),
+                 catq_workspace_size(WS_LINEAR_BWD, R, 2 * F, h, E),
+                 catq_workspace_size(WS_LINEAR_BWD, R, h, F, E))
+        self.lin_ws = torch.empty(ws, dtype=torch.uint8, device=DEV)
+        self.loss_ws = torch.empty(catq_workspace_size(WS_LOSS, M, 1, 1), dtype=torch.uint8,
+                                   device=DEV)
+        self.loss = torch.zeros(1, dtype=torch.float32, device=DEV)
+        self.stats_ready = False
+
+    params = DenseBlock.params
+    modulate_all = DenseBlock.modulate_all
+    new_output = DenseBlock.new_output
+    finalize_buffers = DenseBlock.finalize_buffers
+    finalize = DenseBlock.finalize
+
+    def route(self):
+        catq_aux_moe_route(self.logits, self.cfg.top_k, self.ids, self.wts, self.perm, self.offs,
+                           self.route_ws)
+
+    def forward(self, x, out=None):
+        c, M, R = self.cfg, self.M, self.R
+        h, E, F, k = c.hidden, c.n_experts, c.expert_ffn, c.top_k
+        y = self.y if out is None else out
+        catq_aux_rmsnorm_fwd(x, self.xn1, self.rstd1)
+        catq_fakeq_linear_fwd(self.xn1, self.lin["qkv"].W_fake, self.qkv, M, self.Nqkv, h)
+        catq_aux_attention_fwd(self.desc, self.qkv, self.attn, self.saved)
+        catq_fakeq_linear_fwd(self.attn, self.lin["o"].W_fake, self.h1, M, h, c.n_q * c.head_dim,
+                              residual=x)
+        catq_aux_rmsnorm_fwd(self.h1, self.xn2, self.rstd2)
+        self.route()
+        catq_aux_moe_gather(self.xn2, self.perm, k, self.xg)
+        catq_fakeq_linear_fwd(self.xg, self.lin["gu"].W_fake, self.gu, R, 2 * F, h, n_experts=E,
+                              row_offsets=self.offs)
+        catq_aux_swiglu_fwd(self.gu, self.a)
+        catq_fakeq_linear_fwd(self.a, self.lin["d"].W_fake, self.yg, R, h, F, n_experts=E,
+                              row_offsets=self.offs)
+        catq_aux_moe_combine(self.yg, self.perm, self.wts, self.h1, y, k)
+        return y
+
+    def target(self, x, out):
+        self.modulate_all(self.params(IDENTITY))
+        return self.forward(x, out)
+
+    def backward(self, x, p):
+        c, M, R = self.cfg, self.M, self.R
+        h, E, F, k = c.hidden, c.n_experts, c.expert_ffn, c.top_k
+        ws = self.lin_ws
+
+        def lbwd(name, dY, X, dX, rows, E_=1, offs=None):
+            L = self.lin[name]
+            catq_fakeq_linear_bwd(dY, X, L.W_fake, rows, L.d_out, L.d_in, L.W, L.stats, L.d_mu,
+                                  L.d_alpha, L.d_delta, p, L.g_mu, L.g_alpha, L.g_delta, ws,
+                                  dX=dX, n_experts=E_, row_offsets=offs)
+
+        catq_aux_moe_combine_bwd(self.dy, self.perm, self.wts, self.dyg, k)
+        lbwd("d", self.dyg, self.a, self.da, R, E, self.offs)
+        catq_aux_swiglu_bwd(self.gu, self.da, self.dgu)
+        lbwd("gu", self.dgu, self.xg, self.dxg, R, E, self.offs)
+        catq_aux_moe_scatter_add(self.dxg, self.perm, self.dxn2, k)
+        catq_aux_rmsnorm_bwd(self.h1, self.rstd2, self.dxn2, self.dh1, dres=self.dy)
+        lbwd("o", self.dh1, self.attn, self.dattn, M)
+        catq_aux_attention_bwd(self.desc, self.qkv, self.saved, self.dattn, self.dqkv,
+                               self.attn_ws)
+        lbwd("qkv", self.dqkv, self.xn1, self.dxn1, M)
+        catq_aux_rmsnorm_bwd(x, self.rstd1, self.dxn1, self.dx, dres=self.dh1)
+
+    step = DenseBlock.step
+
+    @staticmethod
+    def split_fused(cfg, name, arr):
+        """Per-linear pieces of a fused array; expert arrays are [E*rows][...]
+        (or per-group values in the same order)."""
+        hd = cfg.head_dim
+        if name == "qkv":
+            return _split_rows(arr, [cfg.n_q * hd, cfg.n_kv * hd, cfg.n_kv * hd],
+                               ["Wq", "Wk", "Wv"])
+        if name == "o":
+            return {"Wo": arr}
+        E, F = cfg.n_experts, cfg.expert_ffn
+        if name == "gu":
+            per = arr.reshape(E, 2 * F, -1)
+            return {"Wg": per[:, :F].reshape(E * F, -1), "Wu": per[:, F:].reshape(E * F, -1)}
+        return {"Wd": arr}
+
+
+def _split_rows(arr, sizes, names):
+    total = sum(sizes)
+    per_row = arr.shape[0] // total
+    out, r = {}, 0
+    for n, sz in zip(names, sizes):
+        out[n] = arr[r * per_row:(r + sz) * per_row]
+        r += sz
+    return out

@@ -1,0 +1,481 @@
+// Matrix-core GEMMs of the fake-ternary linear layers and of attention (gfx950).
+//
+// The fake-ternary linears are the only dense contractions of the step
+// (Sec. 2.4, Eq. 7: the window forward with alpha*T and its backward):
+//   forward  Y  = X . W_fake^T      both operands contiguous along K
+//   input    dX = dY . W_fake       W_fake contracted over its rows
+//   weight   G  = dY^T . X          both operands contracted over tokens
+// One kernel template covers all three: each operand is either contiguous
+// along the contraction ("row" layout, 16-byte loads straight into LDS) or
+// contiguous along the output dimension ("transposed": every thread loads an
+// 8x8 block with eight 16-byte loads and transposes it in registers with
+// v_perm before a 16-byte LDS store).  LDS holds both tiles K-contiguous, so
+// the MFMA fragment reads are always one ds_read_b128 per lane.
+//
+// Tiles: BM x BN x 64, double-buffered LDS (one barrier per K step),
+// v_mfma_f32_32x32x16_bf16, fp32 accumulation.  Block -> tile mapping puts
+// consecutive tiles of a row band on one XCD (workgroups are dealt round-robin
+// to the 8 XCDs) and walks tiles in bands of 8 rows for L2 reuse.
+#include <cmath>
+
+#include "kernels.h"
+
+namespace catq {
+
+GemmArgs gemm_args_default() {
+  GemmArgs a;
+  a.A = a.B = a.R = nullptr;
+  a.C = nullptr;
+  a.M = a.N = a.K = 0;
+  a.lda = a.ldb = a.ldc = a.ldr = 0;
+  a.a_so = a.a_si = a.b_so = a.b_si = a.c_so = a.c_si = 0;
+  a.a_div = a.b_div = a.c_div = a.inner = 1;
+  a.batch = 1;
+  a.alpha = 1.0f;
+  a.causal = 0;
+  a.group_off = nullptr;
+  a.group_mode = 0;
+  a.n_groups = 1;
+  a.b_gs = a.c_gs = 0;
+  a.max_rows_per_group = 0;
+  return a;
+}
+
+// Internal launch record: GemmArgs plus split-K (blockIdx.z = split when > 1).
+struct GemmLaunch {
+  GemmArgs g;
+  int32_t ksplit;
+  int64_t kchunk;
+  int64_t c_split_stride;
+  int32_t tiles_m, tiles_n;
+};
+
+constexpr int LDS_PAD = 8;
+
+__device__ __forceinline__ unsigned int perm(unsigned int hi_src, unsigned int lo_src,
+                                             unsigned int sel) {
+  return __builtin_amdgcn_perm(hi_src, lo_src, sel);
+}
+
+// Global -> register -> LDS staging of one operand tile (ROWS x BK, stored in
+// LDS as [ROWS][BK + pad], K contiguous).
+//   X_T = 0: the operand is contiguous along K; one item is a 16-byte chunk.
+//   X_T = 1: the operand is contiguous along ROWS; one item is KR consecutive
+//            K-rows x 8 ROWS (KR 16-byte loads), transposed in registers with
+//            v_perm into 8 K-contiguous runs of KR elements.
+template <int ROWS, int BK, int NT, int X_T>
+struct TileLoader {
+  static constexpr int KC = BK / 8;  // 16-byte chunks along K
+  static constexpr int KR = (KC * (ROWS / 8) >= NT) ? 8 : ((BK / 4) * (ROWS / 8) >= NT ? 4 : 2);
+  static constexpr int N_ITEMS = X_T == 0 ? ROWS * KC / NT : ((BK / KR) * (ROWS / 8)) / NT;
+  static constexpr int N_REGS = X_T == 0 ? N_ITEMS : N_ITEMS * KR;
+  static_assert(N_ITEMS >= 1, "tile too small for the thread count");
+  static_assert(X_T == 0 ? (ROWS * KC) % NT == 0 : ((BK / KR) * (ROWS / 8)) % NT == 0,
+                "uneven tile split");
+  u32x4 r[N_REGS];
+
+  // base points at element (row 0, k 0) of this operand for the current block;
+  // rows are row0.., valid below row_lim; k runs k0.., valid below k_lim.
+  __device__ __forceinline__ void load(const u16* __restrict__ base, int64_t ld, int64_t row0,
+                                       int64_t row_lim, int64_t k0, int64_t k_lim, int tid) {
+    const u32x4 z = {0u, 0u, 0u, 0u};
+    if (X_T == 0) {
+#pragma unroll
+      for (int i = 0; i < N_ITEMS; ++i) {
+        const int c = tid + i * NT;
+        const int rr = c / KC, kc = c % KC;
+        const int64_t row = row0 + rr, k = k0 + kc * 8;
+        r[i] = (row < row_lim && k < k_lim)
+                   ? *reinterpret_cast<const u32x4*>(base + row * ld + k)
+                   : z;
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < N_ITEMS; ++i) {
+        const int b = tid + i * NT;
+        const int kb = b / (ROWS / 8), mb = b % (ROWS / 8);
+        const int64_t m = row0 + mb * 8;
+        const bool mok = m < row_lim;
+#pragma unroll
+        for (int j = 0; j < KR; ++j) {
+          const int64_t k = k0 + kb * KR + j;
+          r[i * KR + j] = (mok && k < k_lim)
+                              ? *reinterpret_cast<const u32x4*>(base + k * ld + m)
+                              : z;
+        }
+      }
+    }
+  }
+
+  __device__ __forceinline__ void store(u16* __restrict__ lds, int tid) const {
+    constexpr int P = BK + LDS_PAD;
+    if (X_T == 0) {
+#pragma unroll
+      for (int i = 0; i < N_ITEMS; ++i) {
+        const int c = tid + i * NT;
+        const int rr = c / KC, kc = c % KC;
+        *reinterpret_cast<u32x4*>(lds + rr * P + kc * 8) = r[i];
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < N_ITEMS; ++i) {
+        const int b = tid + i * NT;
+        const int kb = b / (ROWS / 8), mb = b % (ROWS / 8);
+        // r[i*KR + j] holds k = kb*KR + j for m = mb*8 + 0..7 (two per dword);
+        // column mm becomes one K-contiguous run of KR elements.
+#pragma unroll
+        for (int mm = 0; mm < 8; ++mm) {
+          const unsigned int sel = (mm & 1) ? 0x07060302u : 0x05040100u;
+          const int dw = mm >> 1;
+          u16* dst = lds + (mb * 8 + mm) * P + kb * KR;
+          if (KR == 8) {
+            u32x4 o;
+#pragma unroll
+            for (int p = 0; p < 4; ++p)
+              o[p] = perm(r[i * KR + 2 * p + 1][dw], r[i * KR + 2 * p][dw], sel);
+            *reinterpret_cast<u32x4*>(dst) = o;
+          } else if (KR == 4) {
+            uint2 o;
+            o.x = perm(r[i * KR + 1][dw], r[i * KR + 0][dw], sel);
+            o.y = perm(r[i * KR + 3][dw], r[i * KR + 2][dw], sel);
+            *reinterpret_cast<uint2*>(dst) = o;
+          } else {
+            *reinterpret_cast<unsigned int*>(dst) = perm(r[i * KR + 1][dw], r[i * KR + 0][dw], sel);
+          }
+        }
+      }
+    }
+  }
+};
+
+template <typename OutT>
+__device__ __forceinline__ void store_out(OutT* p, float v);
+template <>
+__device__ __forceinline__ void store_out<float>(float* p, float v) {
+  *p = v;
+}
+template <>
+__device__ __forceinline__ void store_out<bf16>(bf16* p, float v) {
+  *p = (bf16)v;
+}
+
+__device__ __forceinline__ void tile_coords(int pid, int tiles_m, int tiles_n, int& pm, int& pn) {
+  const int num = tiles_m * tiles_n;
+  // keep neighbouring tiles on one XCD (round-robin dispatch over 8 XCDs)
+  if ((num & 7) == 0) pid = (pid & 7) * (num >> 3) + (pid >> 3);
+  constexpr int GROUP_M = 8;
+  const int in_group = GROUP_M * tiles_n;
+  const int gid = pid / in_group;
+  const int first = gid * GROUP_M;
+  const int gsz = min(tiles_m - first, GROUP_M);
+  const int r = pid % in_group;
+  pm = first + r % gsz;
+  pn = r / gsz;
+}
+
+template <int BM, int BN, int BK, int WGM, int WGN, int A_T, int B_T, typename OutT, typename RT,
+          bool HAS_R>
+__global__ __launch_bounds__(WGM* WGN * 64) void gemm_bf16_kernel(GemmLaunch L) {
+  constexpr int NT = WGM * WGN * 64;
+  constexpr int WTM = BM / WGM, WTN = BN / WGN;
+  constexpr int FM = WTM / 32, FN = WTN / 32;
+  constexpr int P = BK + LDS_PAD;
+  static_assert(FM >= 1 && FN >= 1 && BK % 16 == 0, "bad tile");
+  __shared__ u16 sA[2][BM * P];
+  __shared__ u16 sB[2][BN * P];
+
+  const GemmArgs& g = L.g;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WGN, wn = wave % WGN;
+
+  int pm, pn, z = blockIdx.z;
+  if (L.g.group_mode == 1) {
+    // rows grouped by expert: blockIdx.x enumerates (m-tile, n-tile) over the
+    // concatenation of every expert's m-tiles; walk the offsets to find ours
+    const int t = blockIdx.x / L.tiles_n;
+    pn = blockIdx.x % L.tiles_n;
+    int acc_tiles = 0, e = 0;
+    for (; e < L.g.n_groups; ++e) {
+      const int64_t rows = L.g.group_off[e + 1] - L.g.group_off[e];
+      const int nt = (int)((rows + BM - 1) / BM);
+      if (t < acc_tiles + nt) break;
+      acc_tiles += nt;
+    }
+    if (e >= L.g.n_groups) return;
+    z = e;
+    pm = t - acc_tiles;
+  } else {
+    tile_coords(blockIdx.x, L.tiles_m, L.tiles_n, pm, pn);
+  }
+  const int64_t m0 = (int64_t)pm * BM, n0 = (int64_t)pn * BN;
+
+  // ---- operand bases, row limits and contraction range for this block
+  const u16* Ab = reinterpret_cast<const u16*>(g.A);
+  const u16* Bb = reinterpret_cast<const u16*>(g.B);
+  int64_t a_row0 = m0;       // absolute row of A/C holding tile row 0
+  int64_t row_lim = g.M;     // absolute rows of A/C below row_lim are valid
+  int64_t kb = 0, ke = g.K;  // contraction range
+  int64_t c_off = 0, r_off = 0;
+  if (g.group_mode == 1) {
+    const int64_t r0 = g.group_off[z], r1 = g.group_off[z + 1];
+    if (m0 >= r1 - r0) return;
+    a_row0 = r0 + m0;
+    row_lim = r1;
+    Bb += z * g.b_gs;
+  } else if (g.group_mode == 2) {
+    kb = g.group_off[z];
+    ke = g.group_off[z + 1];
+    c_off = z * g.c_gs;
+  } else if (L.ksplit > 1) {
+    kb = (int64_t)z * L.kchunk;
+    ke = min(g.K, kb + L.kchunk);
+    c_off = z * L.c_split_stride;
+  } else {
+    const int zo = z / g.inner, zi = z % g.inner;
+    Ab += zo * g.a_so + (zi / g.a_div) * g.a_si;
+    Bb += zo * g.b_so + (zi / g.b_div) * g.b_si;
+    c_off = zo * g.c_so + (zi / g.c_div) * g.c_si;
+    r_off = c_off;
+  }
+  if (g.causal == 1 && n0 >= m0 + BM) return;
+  if (g.causal == 2) ke = min(ke, m0 + BM);
+  if (g.causal == 3) kb = m0;  // BM is a multiple of BK
+
+  TileLoader<BM, BK, NT, A_T> la;
+  TileLoader<BN, BK, NT, B_T> lb;
+
+  f32x16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  const int64_t nk = ke > kb ? (ke - kb + BK - 1) / BK : 0;
+  if (nk > 0) {
+    la.load(Ab, g.lda, a_row0, row_lim, kb, ke, tid);
+    lb.load(Bb, g.ldb, n0, g.N, kb, ke, tid);
+    la.store(sA[0], tid);
+    lb.store(sB[0], tid);
+    __syncthreads();
+  }
+  for (int64_t kt = 0; kt < nk; ++kt) {
+    const int buf = (int)(kt & 1);
+    const bool more = kt + 1 < nk;
+    if (more) {
+      const int64_t k0 = kb + (kt + 1) * BK;
+      la.load(Ab, g.lda, a_row0, row_lim, k0, ke, tid);
+      lb.load(Bb, g.ldb, n0, g.N, k0, ke, tid);
+    }
+    const u16* pa = sA[buf] + (wm * WTM + (lane & 31)) * P + (lane >> 5) * 8;
+    const u16* pb = sB[buf] + (wn * WTN + (lane & 31)) * P + (lane >> 5) * 8;
+#pragma unroll
+    for (int kk = 0; kk < BK / 16; ++kk) {
+      bf16x8 fa[FM], fb[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+        fa[i] = *reinterpret_cast<const bf16x8*>(pa + i * 32 * P + kk * 16);
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        fb[j] = *reinterpret_cast<const bf16x8*>(pb + j * 32 * P + kk * 16);
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+    }
+    if (more) {
+      la.store(sA[buf ^ 1], tid);
+      lb.store(sB[buf ^ 1], tid);
+    }
+    __syncthreads();
+  }
+
+  // ---- epilogue: 32x32 accumulator layout: acc[r] is row 8*(r/4) + 4*(lane/32) + r%4,
+  // column lane%32 of the block
+  OutT* C = reinterpret_cast<OutT*>(g.C) + c_off;
+  const RT* R = HAS_R ? reinterpret_cast<const RT*>(g.R) + r_off : nullptr;
+  const int64_t row_base = a_row0 - m0;  // grouped rows are absolute
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int64_t n = n0 + wn * WTN + j * 32 + (lane & 31);
+      if (n >= g.N) continue;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t m = m0 + wm * WTM + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+        const int64_t mrow = m + row_base;
+        if (mrow >= row_lim) continue;
+        float v = acc[i][j][r] * g.alpha;
+        if (HAS_R) v += to_f(R[mrow * g.ldr + n]);
+        store_out<OutT>(C + mrow * g.ldc + n, v);
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------- fp32 GEMM
+// Plain LDS-tiled FMA kernel for fp32 problems (the fp32 single-linear
+// workload); 64x64 tile, 16-deep K slices, 4x4 outputs per thread.
+template <int A_T, int B_T>
+__global__ __launch_bounds__(256) void gemm_f32_kernel(GemmLaunch L) {
+  const GemmArgs& g = L.g;
+  __shared__ float sA[16][64 + 1];
+  __shared__ float sB[16][64 + 1];
+  const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
+  const int64_t m0 = (int64_t)blockIdx.y * 64, n0 = (int64_t)blockIdx.x * 64;
+  const float* A = reinterpret_cast<const float*>(g.A);
+  const float* B = reinterpret_cast<const float*>(g.B);
+  int64_t kb = 0, ke = g.K, c_off = 0;
+  if (L.ksplit > 1) {
+    kb = (int64_t)blockIdx.z * L.kchunk;
+    ke = min(g.K, kb + L.kchunk);
+    c_off = blockIdx.z * L.c_split_stride;
+  }
+  float acc[4][4] = {};
+  for (int64_t k0 = kb; k0 < ke; k0 += 16) {
+    for (int e = threadIdx.x; e < 16 * 64; e += 256) {
+      const int kk = e / 64, mm = e % 64;
+      const int64_t k = k0 + kk, m = m0 + mm, n = n0 + mm;
+      float va = 0.f, vb = 0.f;
+      if (k < ke && m < g.M) va = A_T ? A[k * g.lda + m] : A[m * g.lda + k];
+      if (k < ke && n < g.N) vb = B_T ? B[k * g.ldb + n] : B[n * g.ldb + k];
+      sA[kk][mm] = va;
+      sB[kk][mm] = vb;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < 16; ++kk) {
+      float a[4], b[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        a[i] = sA[kk][ty * 4 + i];
+        b[i] = sB[kk][tx * 4 + i];
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+  float* C = reinterpret_cast<float*>(g.C) + c_off;
+  const float* R = reinterpret_cast<const float*>(g.R);
+  for (int i = 0; i < 4; ++i) {
+    const int64_t m = m0 + ty * 4 + i;
+    if (m >= g.M) continue;
+    for (int j = 0; j < 4; ++j) {
+      const int64_t n = n0 + tx * 4 + j;
+      if (n >= g.N) continue;
+      float v = acc[i][j] * g.alpha;
+      if (R) v += R[m * g.ldr + n];
+      C[m * g.ldc + n] = v;
+    }
+  }
+}
+
+// --------------------------------------------------------------- dispatch
+
+template <int BM, int BN, int WGM, int WGN, int A_T, int B_T, typename OutT, typename RT>
+static void launch_cfg(GemmLaunch& L, hipStream_t stream) {
+  constexpr int BK = 64;
+  const GemmArgs& g = L.g;
+  // grouped rows: at most ceil(M/BM) + E m-tiles over all experts together
+  L.tiles_m = g.group_mode == 1 ? (int)((g.M + BM - 1) / BM + g.n_groups)
+                                : (int)((g.M + BM - 1) / BM);
+  L.tiles_n = (int)((g.N + BN - 1) / BN);
+  int zdim = g.group_mode == 2 ? g.n_groups
+                               : (g.group_mode == 1 ? 1 : (L.ksplit > 1 ? L.ksplit : g.batch));
+  dim3 grid((unsigned)(L.tiles_m * L.tiles_n), 1, (unsigned)zdim);
+  dim3 block(WGM * WGN * 64);
+  if (g.R)
+    hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, BK, WGM, WGN, A_T, B_T, OutT, RT, true>), grid,
+                       block, 0, stream, L);
+  else
+    hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, BK, WGM, WGN, A_T, B_T, OutT, RT, false>), grid,
+                       block, 0, stream, L);
+}
+
+template <int A_T, int B_T, typename OutT, typename RT>
+static void launch_bf16(GemmLaunch& L, hipStream_t stream) {
+  const GemmArgs& g = L.g;
+  int64_t rows = g.group_mode == 1 ? g.max_rows_per_group : g.M;
+  if (rows <= 0) rows = g.M;
+  // large output tiles for the big projections, 128x128 for thin problems
+  if (rows >= 256 && g.N >= 256 && !(g.causal == 2 || g.causal == 3))
+    launch_cfg<256, 256, 2, 4, A_T, B_T, OutT, RT>(L, stream);
+  else
+    launch_cfg<128, 128, 2, 2, A_T, B_T, OutT, RT>(L, stream);
+}
+
+template <typename OutT, typename RT>
+static void launch_layout(GemmLaunch& L, int a_t, int b_t, hipStream_t stream) {
+  if (a_t == 0 && b_t == 0) launch_bf16<0, 0, OutT, RT>(L, stream);
+  else if (a_t == 0 && b_t == 1) launch_bf16<0, 1, OutT, RT>(L, stream);
+  else if (a_t == 1 && b_t == 1) launch_bf16<1, 1, OutT, RT>(L, stream);
+  else launch_bf16<1, 0, OutT, RT>(L, stream);
+}
+
+catq_status gemm_run_split(const GemmArgs& a, int a_t, int b_t, catq_dtype in_dtype,
+                           catq_dtype c_dtype, int ksplit, int64_t c_split_stride,
+                           hipStream_t stream, catq_dtype r_dtype) {
+  GemmLaunch L;
+  L.g = a;
+  L.ksplit = ksplit > 1 ? ksplit : 1;
+  L.kchunk = a.K;
+  if (L.ksplit > 1) {
+    CATQ_REQUIRE(a.group_mode == 0 && a.batch == 1 && a.causal == 0, CATQ_ERR_VALUE,
+                 "split-K needs a dense unbatched problem");
+    L.kchunk = (a.K + L.ksplit - 1) / L.ksplit;
+    L.kchunk = (L.kchunk + 63) / 64 * 64;
+    L.ksplit = (int)((a.K + L.kchunk - 1) / L.kchunk);
+  }
+  L.c_split_stride = c_split_stride;
+  L.tiles_m = L.tiles_n = 0;
+  if (a.M <= 0 || a.N <= 0 || a.K <= 0) return CATQ_OK;
+  if (in_dtype == CATQ_F32) {
+    CATQ_REQUIRE(c_dtype == CATQ_F32 && a.group_mode == 0 && a.batch == 1 && a.causal == 0 &&
+                     (a.R == nullptr || r_dtype == CATQ_F32),
+                 CATQ_ERR_DTYPE, "fp32 GEMM supports dense, unbatched fp32 problems only");
+    dim3 grid((unsigned)((a.N + 63) / 64), (unsigned)((a.M + 63) / 64), (unsigned)L.ksplit);
+    if (a_t == 0 && b_t == 0)
+      hipLaunchKernelGGL((gemm_f32_kernel<0, 0>), grid, dim3(256), 0, stream, L);
+    else if (a_t == 0 && b_t == 1)
+      hipLaunchKernelGGL((gemm_f32_kernel<0, 1>), grid, dim3(256), 0, stream, L);
+    else if (a_t == 1 && b_t == 1)
+      hipLaunchKernelGGL((gemm_f32_kernel<1, 1>), grid, dim3(256), 0, stream, L);
+    else
+      hipLaunchKernelGGL((gemm_f32_kernel<1, 0>), grid, dim3(256), 0, stream, L);
+    CATQ_CHECK_LAUNCH("gemm f32");
+    return CATQ_OK;
+  }
+  CATQ_REQUIRE(in_dtype == CATQ_BF16, CATQ_ERR_DTYPE, "GEMM inputs must be bf16 or f32");
+  if (c_dtype == CATQ_BF16) {
+    CATQ_REQUIRE(a.R == nullptr || r_dtype == CATQ_BF16, CATQ_ERR_DTYPE,
+                 "a bf16 output takes a bf16 residual");
+    launch_layout<bf16, bf16>(L, a_t, b_t, stream);
+  } else if (a.R != nullptr && r_dtype == CATQ_BF16) {
+    launch_layout<float, bf16>(L, a_t, b_t, stream);
+  } else {
+    launch_layout<float, float>(L, a_t, b_t, stream);
+  }
+  CATQ_CHECK_LAUNCH("gemm bf16");
+  return CATQ_OK;
+}
+
+catq_status gemm_run(const GemmArgs& a, int a_t, int b_t, catq_dtype in_dtype, catq_dtype c_dtype,
+                     hipStream_t stream, catq_dtype r_dtype) {
+  return gemm_run_split(a, a_t, b_t, in_dtype, c_dtype, 1, 0, stream, r_dtype);
+}
+
+int gemm_split_count(const GemmArgs& a, int ksplit) {
+  if (ksplit <= 1) return 1;
+  int64_t kchunk = (a.K + ksplit - 1) / ksplit;
+  kchunk = (kchunk + 63) / 64 * 64;
+  return (int)((a.K + kchunk - 1) / kchunk);
+}
+
+}  // namespace catq

@@ -1,0 +1,69 @@
+// Internal launchers shared between the HIP translation units of libcatq.
+#pragma once
+
+#include "catq_internal.h"
+
+namespace catq {
+
+// ------------------------------------------------------------------ LM + ST
+
+// Factor gradients from G = dL/dW_fake (fp32, [n_rows][d_in]) for one weight
+// matrix (or all experts' matrices stacked along rows).  `ws_shared` holds
+// 3*n_groups floats and is used only when some factor stride is 0.
+catq_status launch_factor_grads(const float* G, const void* W, catq_dtype w_dtype, int64_t n_rows,
+                                int64_t d_in, const float* stats, const float* d_mu,
+                                const float* d_alpha, const float* d_delta,
+                                const catq_lmst_params* p, float* g_mu, float* g_alpha,
+                                float* g_delta, float* ws_shared, hipStream_t stream);
+
+catq_status check_lmst_params(const catq_lmst_params* p, int64_t d_in);
+
+// -------------------------------------------------------------------- GEMM
+//
+// C[m][n] = alpha * sum_k A(m,k) B(n,k) (+ R[m][n])
+//   A(m,k) = A[m*lda + k]   (a_t = 0, K contiguous)  or  A[k*lda + m]  (a_t = 1)
+//   B(n,k) = B[n*ldb + k]   (b_t = 0, K contiguous)  or  B[k*ldb + n]  (b_t = 1)
+// Batches: blockIdx.z = z, zo = z / inner, zi = z % inner; operand X is offset
+// by zo*x_so + (zi / x_div)*x_si elements.
+// Causal modes (square attention-score problems, rows = queries):
+//   1  skip output tiles lying wholly above the diagonal (n0 >= m0 + BM)
+//   2  contraction limited to k < m0 + BM          (P.V, dS.K)
+//   3  contraction starts at k = m0 (rounded down)  (P^T.dO, dS^T.Q)
+// Expert grouping through a device array off[E+1] (int64):
+//   group_mode 1: rows of A and C grouped (row range off[e]..off[e+1]), B
+//                 offset by e*b_gs; blockIdx.z = expert
+//   group_mode 2: contraction grouped (k range off[e]..off[e+1]) ; C offset by
+//                 e*c_gs; blockIdx.z = expert
+struct GemmArgs {
+  const void* A;
+  const void* B;
+  void* C;
+  const void* R;
+  int64_t M, N, K;
+  int64_t lda, ldb, ldc, ldr;
+  int64_t a_so, a_si, b_so, b_si, c_so, c_si;
+  int32_t a_div, b_div, c_div, inner;
+  int32_t batch;
+  float alpha;
+  int32_t causal;
+  const int64_t* group_off;
+  int32_t group_mode;
+  int32_t n_groups;
+  int64_t b_gs, c_gs;
+  int64_t max_rows_per_group;  // group_mode 1: bound used to size the grid
+};
+
+GemmArgs gemm_args_default();
+// dtype of A, B (both bf16, or both f32); c_dtype of C; r_dtype of the residual R
+// (a bf16 C takes a bf16 R; an fp32 C takes either).
+catq_status gemm_run(const GemmArgs& a, int a_t, int b_t, catq_dtype in_dtype, catq_dtype c_dtype,
+                     hipStream_t stream, catq_dtype r_dtype = CATQ_BF16);
+// Split-K over the contraction (dense, unbatched): split i writes its partial
+// product to C + i*c_split_stride.  Returns the number of splits actually used
+// through gemm_split_count (chunks are multiples of 64).
+catq_status gemm_run_split(const GemmArgs& a, int a_t, int b_t, catq_dtype in_dtype,
+                           catq_dtype c_dtype, int ksplit, int64_t c_split_stride,
+                           hipStream_t stream, catq_dtype r_dtype = CATQ_BF16);
+int gemm_split_count(const GemmArgs& a, int ksplit);
+
+}  // namespace catq

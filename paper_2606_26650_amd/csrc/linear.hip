@@ -1,0 +1,189 @@
+// C ABI of the fake-ternary linear layer: forward, and backward to the input
+// and to the learnable factors (Sec. 2.2-2.4).
+#include "kernels.h"
+
+namespace catq {
+
+// Split of the token contraction of G = dY^T X so that the (N/256)x(K/256)
+// output tiles times the splits fill the 256 compute units at least twice;
+// each split keeps >= 1024 tokens.
+static int choose_ksplit(int64_t M, int64_t N, int64_t K, int32_t n_experts) {
+  if (n_experts > 1) return 1;
+  const int64_t tiles = ((N + 255) / 256) * ((K + 255) / 256);
+  int ks = 1;
+  while (tiles * ks < 512 && M / (ks * 2) >= 1024) ks *= 2;
+  return ks;
+}
+
+static int splits_used(int64_t M, int64_t N, int64_t K, int32_t n_experts) {
+  GemmArgs a = gemm_args_default();
+  a.M = N;
+  a.N = K;
+  a.K = M;
+  return gemm_split_count(a, choose_ksplit(M, N, K, n_experts));
+}
+
+// Sum of split-K partials (fp32) into dst.
+__global__ __launch_bounds__(256) void sum_splits_kernel(const float* src, int nsplit,
+                                                         int64_t stride, int64_t n4, float* dst) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n4) return;
+  f32x4 acc = reinterpret_cast<const f32x4*>(src)[i];
+  for (int s = 1; s < nsplit; ++s) acc += reinterpret_cast<const f32x4*>(src + s * stride)[i];
+  reinterpret_cast<f32x4*>(dst)[i] = acc;
+}
+
+static catq_status check_linear_common(const void* X, const void* W_fake, catq_dtype dtype,
+                                       int64_t M, int64_t N, int64_t K, int32_t n_experts,
+                                       const int64_t* row_offsets) {
+  CATQ_REQUIRE(X && W_fake, CATQ_ERR_NULL, "X and W_fake must not be NULL");
+  CATQ_REQUIRE(M > 0 && N > 0 && K > 0, CATQ_ERR_SHAPE, "M, N, K must be > 0");
+  CATQ_REQUIRE(dtype_ok(dtype), CATQ_ERR_DTYPE, "bad dtype");
+  CATQ_REQUIRE(K % 8 == 0, CATQ_ERR_SHAPE, "K must be a multiple of 8");
+  CATQ_REQUIRE(n_experts >= 1, CATQ_ERR_SHAPE, "n_experts must be >= 1");
+  CATQ_REQUIRE(n_experts == 1 || row_offsets != nullptr, CATQ_ERR_NULL,
+               "row_offsets required for n_experts > 1");
+  CATQ_REQUIRE(n_experts == 1 || dtype == CATQ_BF16, CATQ_ERR_DTYPE,
+               "routed experts run in bf16 only");
+  return CATQ_OK;
+}
+
+}  // namespace catq
+
+using namespace catq;
+
+extern "C" size_t catq_workspace_size(int32_t which_call, int64_t M, int64_t N, int64_t K,
+                                      int32_t n_experts) {
+  if (M <= 0 || N <= 0 || K <= 0 || n_experts < 1) return 0;
+  if (which_call == CATQ_WS_LINEAR_BWD) {
+    const int64_t E = n_experts;
+    const int ns = splits_used(M, N, K, n_experts);
+    size_t g = round_up((size_t)(E * N * K) * 4 * (size_t)ns, 256);
+    size_t shared = round_up((size_t)3 * (size_t)(E * N * K / 16) * 4, 256);
+    return g + shared;
+  }
+  if (which_call == CATQ_WS_LOSS) return 4096 * sizeof(double);
+  return 0;
+}
+
+extern "C" catq_status catq_fakeq_linear_fwd(const void* X, const void* W_fake, catq_dtype dtype,
+                                             void* Y, catq_dtype y_dtype, int64_t M, int64_t N,
+                                             int64_t K, int32_t n_experts,
+                                             const int64_t* row_offsets, const void* residual,
+                                             catq_dtype r_dtype, hipStream_t stream) {
+  clear_error();
+  CATQ_TRY(check_linear_common(X, W_fake, dtype, M, N, K, n_experts, row_offsets));
+  CATQ_REQUIRE(Y != nullptr, CATQ_ERR_NULL, "Y must not be NULL");
+  CATQ_REQUIRE(dtype_ok(y_dtype) && dtype_ok(r_dtype), CATQ_ERR_DTYPE, "bad y or residual dtype");
+  CATQ_REQUIRE(dtype == CATQ_BF16 || (y_dtype == CATQ_F32 && r_dtype == CATQ_F32), CATQ_ERR_DTYPE,
+               "fp32 inputs give an fp32 output and take an fp32 residual");
+  CATQ_REQUIRE(y_dtype == CATQ_F32 || residual == nullptr || r_dtype == CATQ_BF16,
+               CATQ_ERR_DTYPE, "a bf16 output takes a bf16 residual");
+  CATQ_REQUIRE(residual == nullptr || n_experts == 1, CATQ_ERR_VALUE,
+               "residual is supported for dense layers only");
+  CATQ_REQUIRE(aligned16(X) && aligned16(W_fake) && aligned16(Y) && aligned16(residual),
+               CATQ_ERR_ALIGN, "pointers must be 16-byte aligned");
+  GemmArgs a = gemm_args_default();
+  a.A = X;
+  a.B = W_fake;
+  a.C = Y;
+  a.R = residual;
+  a.M = M;
+  a.N = N;
+  a.K = K;
+  a.lda = K;
+  a.ldb = K;
+  a.ldc = N;
+  a.ldr = N;
+  if (n_experts > 1) {
+    a.group_mode = 1;
+    a.group_off = row_offsets;
+    a.n_groups = n_experts;
+    a.b_gs = N * K;
+    a.max_rows_per_group = (M + n_experts - 1) / n_experts;
+  }
+  return gemm_run(a, 0, 0, dtype, y_dtype, stream, r_dtype);
+}
+
+extern "C" catq_status catq_fakeq_linear_bwd(
+    const void* dY, const void* X, const void* W_fake, catq_dtype dtype, int64_t M, int64_t N,
+    int64_t K, int32_t n_experts, const int64_t* row_offsets, const void* W, catq_dtype w_dtype,
+    const float* stats, const float* d_mu, const float* d_alpha, const float* d_delta,
+    const catq_lmst_params* p, void* dX, float* g_d_mu, float* g_d_alpha, float* g_d_delta,
+    float* dW_fake, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  clear_error();
+  CATQ_TRY(check_linear_common(X, W_fake, dtype, M, N, K, n_experts, row_offsets));
+  CATQ_REQUIRE(dY && W && stats && d_mu && d_alpha && d_delta && g_d_mu && g_d_alpha && g_d_delta,
+               CATQ_ERR_NULL, "dY, W, stats, factors and factor-gradient outputs are required");
+  CATQ_REQUIRE(dtype_ok(w_dtype), CATQ_ERR_DTYPE, "bad w_dtype");
+  CATQ_REQUIRE(N % 8 == 0, CATQ_ERR_SHAPE, "N must be a multiple of 8");
+  CATQ_TRY(check_lmst_params(p, K));
+  CATQ_REQUIRE(aligned16(dY) && aligned16(X) && aligned16(W_fake) && aligned16(W) &&
+                   aligned16(dX) && aligned16(dW_fake) && aligned16(workspace) && aligned16(stats),
+               CATQ_ERR_ALIGN, "pointers must be 16-byte aligned");
+  const size_t need = catq_workspace_size(CATQ_WS_LINEAR_BWD, M, N, K, n_experts);
+  CATQ_REQUIRE(workspace != nullptr && workspace_bytes >= need, CATQ_ERR_WORKSPACE,
+               "workspace of %zu bytes needed (got %zu)", need, workspace_bytes);
+  const int64_t E = n_experts;
+  const int ns = splits_used(M, N, K, n_experts);
+  const size_t g_bytes = round_up((size_t)(E * N * K) * 4 * (size_t)ns, 256);
+  float* Gbuf = (dW_fake && ns == 1) ? dW_fake : reinterpret_cast<float*>(workspace);
+  float* shared_ws = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) + g_bytes);
+
+  // dX = dY . W_fake  (W_fake contracted over its rows)
+  if (dX) {
+    GemmArgs a = gemm_args_default();
+    a.A = dY;
+    a.B = W_fake;
+    a.C = dX;
+    a.M = M;
+    a.N = K;
+    a.K = N;
+    a.lda = N;
+    a.ldb = K;
+    a.ldc = K;
+    if (n_experts > 1) {
+      a.group_mode = 1;
+      a.group_off = row_offsets;
+      a.n_groups = n_experts;
+      a.b_gs = N * K;
+      a.max_rows_per_group = (M + n_experts - 1) / n_experts;
+    }
+    CATQ_TRY(gemm_run(a, 0, 1, dtype, dtype, stream));
+  }
+  // G = dY^T . X  (contraction over the tokens), fp32
+  {
+    GemmArgs a = gemm_args_default();
+    a.A = dY;
+    a.B = X;
+    a.C = Gbuf;
+    a.M = N;
+    a.N = K;
+    a.K = M;
+    a.lda = N;
+    a.ldb = K;
+    a.ldc = K;
+    if (n_experts > 1) {
+      a.group_mode = 2;
+      a.group_off = row_offsets;
+      a.n_groups = n_experts;
+      a.c_gs = N * K;
+      CATQ_TRY(gemm_run(a, 1, 1, dtype, CATQ_F32, stream));
+    } else {
+      CATQ_TRY(gemm_run_split(a, 1, 1, dtype, CATQ_F32, choose_ksplit(M, N, K, 1), N * K,
+                              stream));
+    }
+  }
+  const float* Gsum = Gbuf;
+  if (ns > 1) {
+    // fold the split partials once; the factor kernel then reads one G
+    float* dst = dW_fake ? dW_fake : Gbuf;
+    const int64_t n4 = N * K / 4;
+    hipLaunchKernelGGL(sum_splits_kernel, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0,
+                       stream, Gbuf, ns, N * K, n4, dst);
+    CATQ_CHECK_LAUNCH("split-K reduction");
+    Gsum = dst;
+  }
+  return launch_factor_grads(Gsum, W, w_dtype, E * N, K, stats, d_mu, d_alpha, d_delta, p, g_d_mu,
+                             g_d_alpha, g_d_delta, shared_ws, stream);
+}
