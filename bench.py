@@ -1,0 +1,230 @@
+"""Throughput of the CAT-Q calibration step on one MI355X.
+
+Workload: one decoder block shaped like Qwen3-1.7B (hidden 2048, 16 q / 8 kv
+heads of 128, SwiGLU 6144, QK-norm, RoPE) on 4 synthetic calibration samples
+of 2048 tokens (Student-t(4) activations, N(0, 0.02^2) bf16 weights, seed 0).
+
+One step = every part of the hot path on one batch:
+  group statistics + learnable modulation + softened ternarisation of all
+  seven weights (s = 15, SOFT), block forward with the fake-ternary weights,
+  reconstruction loss against the cached full-precision output, backward to
+  the input and to every group's three factors, then hard ternarisation and
+  2-bit packing of all weights.
+The full-precision target is computed once before timing (it does not change
+during calibration).  Inputs are resident in HBM when the timed region starts.
+
+Prints one JSON line.  Per-kernel durations come from HIP events recorded by
+the library around its own launches, on the launch stream, inside the timed
+region; the CPU baseline times the float64 oracle on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "calibration block-steps/s + fake-ternary GEMM TFLOP/s and LM+ST kernel HBM GB/s"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 matrix-core peak
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E peak
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-gib", type=float, default=0.0,
+                    help="only run a plain device copy of this size (counter calibration)")
+    ap.add_argument("--breakdown", action="store_true", help="print the per-kernel table")
+    return ap.parse_args()
+
+
+def cpu_baseline(cfg, W, xb, row_frac=8):
+    """The float64 oracle on a bounded sample of the same step.
+    Weight side (LM+ST forward, factor gradients, final ternarise+pack): the
+    first 1/row_frac of the rows of every weight matrix, scaled by row_frac
+    (the work is elementwise per group, exactly linear in the weight count).
+    Token side (block forward+backward): ONE of the calibration samples with
+    all weights; samples are independent in the block, so a full step costs
+    t_weights + batch * t_sample."""
+    import dataclasses
+
+    import numpy as np
+
+    import synthgen as sg
+    from oracle import block, calib, lmst
+
+    try:
+        from threadpoolctl import threadpool_info
+        info = threadpool_info()
+        cores = max(int(i.get("num_threads", 1)) for i in info) if info else 1
+    except Exception:  # pragma: no cover
+        cores = 1
+    cores = min(cores, len(os.sched_getaffinity(0)))
+    Wo = {k: sg.bf16_bits_to_f32(v).astype(np.float64) for k, v in W.items()}
+    Ws = {k: v[: v.shape[0] // row_frac] for k, v in Wo.items()}
+    fac_s = {k: sg.init_factors(v.size // 128) for k, v in Ws.items()}
+    one = dataclasses.replace(cfg, batch=1)
+    x1 = sg.bf16_bits_to_f32(xb[: cfg.seq]).astype(np.float64)
+    # weight side on the row sample
+    t0 = time.perf_counter()
+    calib.fake_weights(Ws, fac_s, 128, lmst.SOFT, 15.0)
+    Gs = {k: np.ones_like(v) for k, v in Ws.items()}
+    t1 = time.perf_counter()
+    calib.factor_grads_all(Gs, Ws, fac_s, 128, lmst.SOFT, 15.0, 30.0)
+    for k, v in Ws.items():
+        lmst.pack_ternary(lmst.modulate_ternarize(v, 128, *fac_s[k], lmst.HARD)["codes"])
+    t2 = time.perf_counter()
+    t_weights = row_frac * ((t1 - t0) + (t2 - t1))
+    # token side: one sample through the whole block; the arithmetic does not
+    # depend on the weight values, so the bf16 weights stand in for alpha*T
+    # and the input for the cached target
+    t3 = time.perf_counter()
+    y_q, cache = block.block_forward(x1, Wo, one)
+    loss, dy = block.recon_loss(y_q, x1)
+    block.block_backward(dy, cache, Wo, one)
+    t4 = time.perf_counter()
+    t_sample = t4 - t3
+    step = t_weights + cfg.batch * t_sample
+    return {"value": 1.0 / step, "unit": "block-steps/s", "cores": cores, "kind": "oracle",
+            "sample": (f"float64 oracle, {cores} BLAS threads: LM+ST forward, factor gradients "
+                       f"and ternarise+pack on 1/{row_frac} of the rows of every weight "
+                       f"({(t2 - t0):.1f} s, x{row_frac}) plus block forward+backward of 1 of "
+                       f"the {cfg.batch} samples of {cfg.seq} tokens ({t_sample:.1f} s, "
+                       f"x{cfg.batch}); full-precision target excluded"),
+            "seconds_per_step": step}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(the sharding design is described in DESIGN.md); run with --gpus 1",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2606_26650_amd as cq
+    import synthgen as sg
+    from paper_2606_26650_amd.block import DenseBlock, bf16_tensor
+
+    torch.cuda.set_device(0)
+    if args.copy_gib > 0:
+        n = int(args.copy_gib * (1 << 30)) // 4
+        a = torch.ones(n, dtype=torch.float32, device="cuda")
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4}))
+        return
+
+    cfg = sg.QWEN3_1P7B
+    W = sg.block_weights(cfg, 0)
+    xb = sg.activations(cfg, 0)
+    blk = DenseBlock(cfg, W)
+    x = bf16_tensor(xb)
+    y_fp = blk.new_output()
+    blk.target(x, y_fp)
+    fin = blk.finalize_buffers()
+
+    def step():
+        blk.step(x, y_fp, mode=cq.SOFT, s=15.0, s_bwd=30.0, recompute_stats=True)
+        blk.finalize(fin)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    cq.catq_trace_enable(64 * max(args.steps, 1) + 64)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    recs = cq.trace_records()
+    cq.catq_trace_disable()
+    elapsed = t1 - t0
+    ms_step = 1000.0 * elapsed / args.steps
+    loss = float(blk.loss.item())
+
+    # per-kernel aggregation over the timed steps
+    agg = {}
+    for r in recs:
+        a = agg.setdefault(r["tag"], {"n": 0, "ms": 0.0, "flops": 0.0, "bytes": 0.0})
+        a["n"] += 1
+        a["ms"] += r["ms"]
+        a["flops"] += r["flops"]
+        a["bytes"] += r["bytes"]
+    gemm = {k: v for k, v in agg.items() if k.startswith("gemm") and v["flops"] > 0}
+    # dominant kernel: the GEMM variant with the largest share of step time
+    dom_tag, dom = max(gemm.items(), key=lambda kv: kv[1]["ms"])
+    dom_tflops = dom["flops"] / (dom["ms"] * 1e-3) / 1e12
+    all_gemm_ms = sum(v["ms"] for v in gemm.values())
+    all_gemm_flops = sum(v["flops"] for v in gemm.values())
+    lm_fwd = {k: v for k, v in agg.items() if k.startswith("lmst_fwd_kernel")}
+    lmf_ms = sum(v["ms"] for v in lm_fwd.values())
+    lmf_bytes = sum(v["bytes"] for v in lm_fwd.values())
+    lmb = agg.get("lmst_bwd_kernel<__bf16>", {"ms": 0.0, "bytes": 0.0})
+    step_gemm_flops = all_gemm_flops / args.steps
+
+    out = {
+        "metric": METRIC,
+        "value": args.steps / elapsed,
+        "unit": "block-steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "qwen3-1.7b-shaped decoder block, 4 x 2048 tokens, one CAT-Q "
+                               "calibration step (LM+ST s=15, fwd, loss, bwd to factors, "
+                               "ternarise+pack)",
+                   "hidden": cfg.hidden, "heads": [cfg.n_q, cfg.n_kv, cfg.head_dim],
+                   "ffn": cfg.ffn, "tokens": cfg.tokens, "group_size": 128,
+                   "weights": cfg.n_weights()},
+        "roofline": {
+            "bound": "mfma",
+            "kernel": dom_tag,
+            "achieved": dom_tflops,
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": dom_tflops / PEAK_BF16_TFLOPS,
+            "avg_launch_us": 1000.0 * dom["ms"] / dom["n"],
+            "flops_per_launch": dom["flops"] / dom["n"],
+            "traffic": None,
+        },
+        "gemm_tflops_all": all_gemm_flops / (all_gemm_ms * 1e-3) / 1e12,
+        "gemm_share_of_step": all_gemm_ms / args.steps / ms_step,
+        "step_gemm_tflop": step_gemm_flops / 1e12,
+        "lmst_fwd_gbs": lmf_bytes / (lmf_ms * 1e-3) / 1e9 if lmf_ms else None,
+        "lmst_fwd_frac_hbm": (lmf_bytes / (lmf_ms * 1e-3) / 1e9) / PEAK_HBM_GBS if lmf_ms else None,
+        "lmst_bwd_gbs": lmb["bytes"] / (lmb["ms"] * 1e-3) / 1e9 if lmb["ms"] else None,
+        "loss": loss,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, W, xb)
+    if args.breakdown:
+        for k, v in sorted(agg.items(), key=lambda kv: -kv[1]["ms"]):
+            tf = v["flops"] / (v["ms"] * 1e-3) / 1e12 if v["flops"] else 0
+            gb = v["bytes"] / (v["ms"] * 1e-3) / 1e9
+            print(f"{v['ms'] / args.steps:9.3f} ms/step {v['n'] // args.steps:3d}x "
+                  f"{tf:8.1f} TF/s {gb:8.1f} GB/s  {k}", file=sys.stderr)
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

@@ -304,6 +304,29 @@ catq_status catq_aux_adamw(float* p, const float* grad, float* m, float* v, int6
 catq_status catq_aux_add(const void* a, const void* b, void* y, catq_dtype dtype, int64_t n,
                          hipStream_t stream);
 
+/* ===================================================================== *
+ * Launch tracing (measurement aid).  While enabled, the library records a
+ * pair of HIP events around each of its kernel launches, on the launch
+ * stream, with the kernel's tag (its function and template arguments) and
+ * the algorithmic work of that launch.  Process-global, one host thread.
+ * ===================================================================== */
+typedef struct {
+  char tag[96];   /* kernel function and template arguments                 */
+  double flops;   /* algorithmic floating-point operations of the launch     */
+  double bytes;   /* algorithmic HBM bytes (each operand read/written once)  */
+  int64_t M, N, K;
+  float ms;       /* event-measured duration (filled by catq_trace_get)      */
+} catq_trace_rec;
+
+/* Create `capacity` event pairs and start recording (host memory only). */
+catq_status catq_trace_enable(int32_t capacity);
+void catq_trace_pause(int32_t paused);
+void catq_trace_reset(void);
+int32_t catq_trace_count(void);
+/* Waits for record i's stop event and returns the record with its duration. */
+catq_status catq_trace_get(int32_t i, catq_trace_rec* out);
+void catq_trace_disable(void);
+
 #ifdef __cplusplus
 }
 #endif

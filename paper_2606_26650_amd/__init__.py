@@ -21,7 +21,9 @@ __all__ = [
     "catq_aux_moe_route_workspace_bytes", "catq_aux_moe_gather", "catq_aux_moe_combine",
     "catq_aux_moe_combine_bwd", "catq_aux_moe_scatter_add", "catq_aux_adamw", "catq_aux_add",
     "lmst_params", "attn_desc", "IDENTITY", "SOFT", "HARD", "F32", "BF16", "CatqError",
-    "LmstParams", "AttnDesc", "lib",
+    "LmstParams", "AttnDesc", "lib", "catq_trace_enable", "catq_trace_pause",
+    "catq_trace_reset", "catq_trace_count", "catq_trace_get", "catq_trace_disable",
+    "trace_records",
 ]
 
 lib = _lib.load()
@@ -222,3 +224,34 @@ def catq_aux_adamw(p, grad, m, v, step, lr, beta1=0.9, beta2=0.999, eps=1e-8, lo
 def catq_aux_add(a, b, y, stream=None):
     st = lib.catq_aux_add(_ptr(a), _ptr(b), _ptr(y), _dt(a), a.numel(), _stream(stream))
     _lib.check("catq_aux_add", st)
+
+
+def catq_trace_enable(capacity):
+    _lib.check("catq_trace_enable", lib.catq_trace_enable(capacity))
+
+
+def catq_trace_pause(paused=True):
+    lib.catq_trace_pause(int(bool(paused)))
+
+
+def catq_trace_reset():
+    lib.catq_trace_reset()
+
+
+def catq_trace_count():
+    return int(lib.catq_trace_count())
+
+
+def catq_trace_get(i):
+    r = _lib.TraceRec()
+    _lib.check("catq_trace_get", lib.catq_trace_get(i, C.byref(r)))
+    return dict(tag=r.tag.decode(), flops=r.flops, bytes=r.bytes, M=r.M, N=r.N, K=r.K, ms=r.ms)
+
+
+def catq_trace_disable():
+    lib.catq_trace_disable()
+
+
+def trace_records():
+    """Every record since the last reset, with its event-measured duration."""
+    return [catq_trace_get(i) for i in range(catq_trace_count())]

@@ -30,6 +30,11 @@ class AttnDesc(C.Structure):
                 ("rope_theta", C.c_float), ("eps", C.c_float)]
 
 
+class TraceRec(C.Structure):
+    _fields_ = [("tag", C.c_char * 96), ("flops", C.c_double), ("bytes", C.c_double),
+                ("M", C.c_int64), ("N", C.c_int64), ("K", C.c_int64), ("ms", C.c_float)]
+
+
 class CatqError(RuntimeError):
     def __init__(self, fn, status, msg):
         super().__init__(f"{fn}: {STATUS.get(status, status)}: {msg}")
@@ -66,10 +71,17 @@ SIGNATURES = {
     "catq_aux_moe_scatter_add": [P, P, I64, I32, I64, P, P],
     "catq_aux_adamw": [P, P, P, P, I64, I64, F, F, F, F, F, F, P],
     "catq_aux_add": [P, P, P, I32, I64, P],
+    "catq_trace_enable": [I32],
+    "catq_trace_pause": [I32],
+    "catq_trace_reset": [],
+    "catq_trace_count": [],
+    "catq_trace_get": [I32, C.POINTER(TraceRec)],
+    "catq_trace_disable": [],
 }
 RESTYPES = {"catq_workspace_size": SZ, "catq_status_string": C.c_char_p,
             "catq_last_error_message": C.c_char_p, "catq_attn_saved_bytes": SZ,
-            "catq_attn_bwd_workspace_bytes": SZ, "catq_aux_moe_route_workspace_bytes": SZ}
+            "catq_attn_bwd_workspace_bytes": SZ, "catq_aux_moe_route_workspace_bytes": SZ,
+            "catq_trace_pause": None, "catq_trace_reset": None, "catq_trace_disable": None}
 
 _lib = None
 

@@ -18,7 +18,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libcatq.so")
 
-SOURCES = ["status.hip", "lmst.hip", "gemm.hip", "linear.hip", "loss.hip", "glue.hip",
+SOURCES = ["status.hip", "trace.hip", "lmst.hip", "gemm.hip", "linear.hip", "loss.hip", "glue.hip",
            "attention.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

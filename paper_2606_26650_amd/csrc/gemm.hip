@@ -17,6 +17,7 @@
 // consecutive tiles of a row band on one XCD (workgroups are dealt round-robin
 // to the 8 XCDs) and walks tiles in bands of 8 rows for L2 reuse.
 #include <cmath>
+#include <cstdio>
 
 #include "kernels.h"
 
@@ -379,6 +380,27 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmLaunch L) {
 
 // --------------------------------------------------------------- dispatch
 
+template <typename T>
+static const char* tname() {
+  return sizeof(T) == 2 ? "__bf16" : "float";
+}
+
+// Algorithmic work of one GEMM launch: 2MNK per problem (half of it for the
+// causal attention products), each operand read once and C written once.
+static void gemm_work(const GemmLaunch& L, int out_bytes, double& flops, double& bytes) {
+  const GemmArgs& g = L.g;
+  double nb = g.group_mode == 2 ? g.n_groups : (g.group_mode == 1 ? 1 : g.batch);
+  double f = 2.0 * (double)g.M * (double)g.N * (double)g.K * nb;
+  if (g.causal) f *= 0.5;
+  flops = f;
+  if (g.group_mode == 1)
+    bytes = 2.0 * ((double)g.M * g.K + (double)g.n_groups * g.N * g.K) + (double)out_bytes * g.M * g.N;
+  else if (g.group_mode == 2)
+    bytes = 2.0 * ((double)g.K * g.M + (double)g.K * g.N) + (double)out_bytes * g.n_groups * g.M * g.N;
+  else
+    bytes = nb * (2.0 * ((double)g.M * g.K + (double)g.N * g.K) + (double)out_bytes * g.M * g.N);
+}
+
 template <int BM, int BN, int WGM, int WGN, int A_T, int B_T, typename OutT, typename RT>
 static void launch_cfg(GemmLaunch& L, hipStream_t stream) {
   constexpr int BK = 64;
@@ -391,12 +413,19 @@ static void launch_cfg(GemmLaunch& L, hipStream_t stream) {
                                : (g.group_mode == 1 ? 1 : (L.ksplit > 1 ? L.ksplit : g.batch));
   dim3 grid((unsigned)(L.tiles_m * L.tiles_n), 1, (unsigned)zdim);
   dim3 block(WGM * WGN * 64);
+  char tag[96];
+  std::snprintf(tag, sizeof(tag), "gemm_bf16_kernel<%d, %d, %d, %d, %d, %d, %d, %s, %s, %s>", BM,
+                BN, BK, WGM, WGN, A_T, B_T, tname<OutT>(), tname<RT>(), g.R ? "true" : "false");
+  double flops, bytes;
+  gemm_work(L, (int)sizeof(OutT), flops, bytes);
   if (g.R)
-    hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, BK, WGM, WGN, A_T, B_T, OutT, RT, true>), grid,
-                       block, 0, stream, L);
+    CATQ_TRACED(stream, tag, flops, bytes, g.M, g.N, g.K,
+                hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, BK, WGM, WGN, A_T, B_T, OutT, RT, true>),
+                                   grid, block, 0, stream, L));
   else
-    hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, BK, WGM, WGN, A_T, B_T, OutT, RT, false>), grid,
-                       block, 0, stream, L);
+    CATQ_TRACED(stream, tag, flops, bytes, g.M, g.N, g.K,
+                hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, BK, WGM, WGN, A_T, B_T, OutT, RT, false>),
+                                   grid, block, 0, stream, L));
 }
 
 template <int A_T, int B_T, typename OutT, typename RT>

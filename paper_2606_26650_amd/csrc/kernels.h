@@ -5,6 +5,18 @@
 
 namespace catq {
 
+// ---------------------------------------------------------------- tracing
+int trace_begin(hipStream_t stream, const char* tag, double flops, double bytes, int64_t M,
+                int64_t N, int64_t K);
+void trace_end(int slot, hipStream_t stream);
+
+#define CATQ_TRACED(stream, tag, flops, bytes, M, N, K, launch)                   \
+  do {                                                                           \
+    const int slot_ = ::catq::trace_begin((stream), (tag), (flops), (bytes), (M), (N), (K)); \
+    launch;                                                                      \
+    ::catq::trace_end(slot_, (stream));                                          \
+  } while (0)
+
 // ------------------------------------------------------------------ LM + ST
 
 // Factor gradients from G = dL/dW_fake (fp32, [n_rows][d_in]) for one weight

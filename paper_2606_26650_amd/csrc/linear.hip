@@ -179,8 +179,9 @@ extern "C" catq_status catq_fakeq_linear_bwd(
     // fold the split partials once; the factor kernel then reads one G
     float* dst = dW_fake ? dW_fake : Gbuf;
     const int64_t n4 = N * K / 4;
-    hipLaunchKernelGGL(sum_splits_kernel, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0,
-                       stream, Gbuf, ns, N * K, n4, dst);
+    CATQ_TRACED(stream, "sum_splits_kernel", 0.0, 4.0 * (double)(N * K) * (ns + 1), N, K, ns,
+                hipLaunchKernelGGL(sum_splits_kernel, dim3((unsigned)((n4 + 255) / 256)),
+                                   dim3(256), 0, stream, Gbuf, ns, N * K, n4, dst));
     CATQ_CHECK_LAUNCH("split-K reduction");
     Gsum = dst;
   }

@@ -223,12 +223,31 @@ __global__ __launch_bounds__(256) void lmst_fwd_kernel(FwdArgs a) {
   if (a.Wf) store8<OT>(reinterpret_cast<OT*>(a.Wf) + o * 8, out);
 }
 
+template <typename T>
+static const char* tname() {
+  return sizeof(T) == 2 ? "__bf16" : "float";
+}
+
 template <typename WT, typename OT, int MODE>
 static void launch_fwd_mode(const FwdArgs& a, bool stats, dim3 grid, hipStream_t stream) {
+  char tag[96];
+  std::snprintf(tag, sizeof(tag), "lmst_fwd_kernel<%s, %s, %d, %s>", tname<WT>(), tname<OT>(),
+                MODE, stats ? "true" : "false");
+  // algorithmic bytes: W read once, W_fake / codes written once, per group
+  // the three factors read (or one shared value) and the stats read or written
+  const double n = (double)a.n_oct * 8.0;
+  const double ng = n / (8.0 * (1 << a.lg));
+  const double fac = 4.0 * ((a.s0 ? ng : 1) + (a.s1 ? ng : 1) + (a.s2 ? ng : 1));
+  const double bytes = n * sizeof(WT) + (a.Wf ? n * sizeof(OT) : 0.0) + (a.codes ? n : 0.0) +
+                       fac + 8.0 * ng + (a.alpha_out ? 4.0 * ng : 0.0);
   if (stats)
-    hipLaunchKernelGGL((lmst_fwd_kernel<WT, OT, MODE, true>), grid, dim3(256), 0, stream, a);
+    CATQ_TRACED(stream, tag, 0.0, bytes, (int64_t)n, 0, 0,
+                hipLaunchKernelGGL((lmst_fwd_kernel<WT, OT, MODE, true>), grid, dim3(256), 0,
+                                   stream, a));
   else
-    hipLaunchKernelGGL((lmst_fwd_kernel<WT, OT, MODE, false>), grid, dim3(256), 0, stream, a);
+    CATQ_TRACED(stream, tag, 0.0, bytes, (int64_t)n, 0, 0,
+                hipLaunchKernelGGL((lmst_fwd_kernel<WT, OT, MODE, false>), grid, dim3(256), 0,
+                                   stream, a));
 }
 
 template <typename WT, typename OT>
@@ -390,10 +409,14 @@ catq_status launch_factor_grads(const float* G, const void* W, catq_dtype w_dtyp
   const double s_use = (p->mode == CATQ_HARD) ? (double)p->s_bwd : (double)p->s;
   a.st = make_st(s_use > 0 ? s_use : 1.0);
   dim3 grid((unsigned)((a.n_oct + 255) / 256));
+  const double nn = (double)n, ngd = (double)a.n_groups;
+  const double bytes = nn * (4.0 + (w_dtype == CATQ_BF16 ? 2.0 : 4.0)) + ngd * (8.0 + 12.0 + 12.0);
   if (w_dtype == CATQ_BF16)
-    hipLaunchKernelGGL((lmst_bwd_kernel<bf16>), grid, dim3(256), 0, stream, a);
+    CATQ_TRACED(stream, "lmst_bwd_kernel<__bf16>", 0.0, bytes, n, 0, 0,
+                hipLaunchKernelGGL((lmst_bwd_kernel<bf16>), grid, dim3(256), 0, stream, a));
   else
-    hipLaunchKernelGGL((lmst_bwd_kernel<float>), grid, dim3(256), 0, stream, a);
+    CATQ_TRACED(stream, "lmst_bwd_kernel<float>", 0.0, bytes, n, 0, 0,
+                hipLaunchKernelGGL((lmst_bwd_kernel<float>), grid, dim3(256), 0, stream, a));
   CATQ_CHECK_LAUNCH("factor gradients");
   for (int i = 0; i < 3; ++i) {
     if (a.s[i] == 0) {
@@ -533,8 +556,9 @@ extern "C" catq_status catq_pack_ternary(const int8_t* codes, int64_t d_out, int
   const int64_t n16 = n / 16;
   const int64_t n_bytes = n / 4;
   const int64_t threads = n16 + (n_bytes - n16 * 4);
-  hipLaunchKernelGGL(pack_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream,
-                     codes, n16, n_bytes, packed);
+  CATQ_TRACED(stream, "pack_kernel", 0.0, (double)n + (double)n_bytes, n, 0, 0,
+              hipLaunchKernelGGL(pack_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256),
+                                 0, stream, codes, n16, n_bytes, packed));
   CATQ_CHECK_LAUNCH("pack_ternary");
   return CATQ_OK;
 }
