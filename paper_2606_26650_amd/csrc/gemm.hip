@@ -318,6 +318,138 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_bf16_kernel(GemmLaunch L) 
   }
 }
 
+// ------------------------------------------------ NT GEMM, direct to LDS
+//
+// Both operands contiguous along K (K % 64 == 0).  Tiles move from global
+// memory straight into LDS with global_load_lds_dwordx4 (no register
+// staging): each wave instruction fills 1 KB of LDS, lane l landing at
+// base + 16 l.  A tile is ROWS x 64 bf16 = ROWS*8 chunks of 16 B; chunk c of
+// row r sits in slot r*8 + (c ^ (r & 7)), a swizzle chosen by picking which
+// global chunk each lane fetches, so the MFMA fragment reads (8 consecutive
+// rows, same chunk) hit 8 distinct bank groups.  Two LDS stages; the next
+// tile is fetched while the current one is multiplied.  Rows past M or N are
+// clamped to the last row (their results are never stored).
+
+// 16-byte global -> LDS copy, lane l landing at lds_base + 16*l.  Issued as
+// inline assembly so that the compiler does not add conservative waits before
+// every LDS read; the kernel waits (vmcnt) itself before the barrier that
+// publishes the tile.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16(const void* g, const void* lds_base) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  const unsigned l = __builtin_amdgcn_readfirstlane(
+      (unsigned)(uintptr_t)(__attribute__((address_space(3))) const void*)lds_base);
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(l), "v"(g)
+               : "memory", "m0");
+#endif
+}
+#pragma clang diagnostic pop
+
+__device__ __forceinline__ void wait_vmem() {
+#if defined(__HIP_DEVICE_COMPILE__)
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+#endif
+}
+
+template <int BM, int BN, int WGM, int WGN, typename OutT, typename RT, bool HAS_R>
+__global__ __launch_bounds__(WGM* WGN * 64, 1) void gemm_nt_dma_kernel(GemmLaunch L) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  constexpr int NW = WGM * WGN;
+  constexpr int WTM = BM / WGM, WTN = BN / WGN;
+  constexpr int FM = WTM / 32, FN = WTN / 32;
+  constexpr int IA = BM / 8 / NW, IB = BN / 8 / NW;
+  static_assert(IA >= 1 && IB >= 1 && FM >= 1 && FN >= 1, "bad tile");
+  __shared__ uint4 sA[2][BM * 8];
+  __shared__ uint4 sB[2][BN * 8];
+  const GemmArgs& g = L.g;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WGN, wn = wave % WGN;
+  int pm, pn;
+  tile_coords(blockIdx.x, L.tiles_m, L.tiles_n, pm, pn);
+  const int64_t m0 = (int64_t)pm * BM, n0 = (int64_t)pn * BN;
+  int64_t kb = 0, ke = g.K, c_off = 0;
+  if (L.ksplit > 1) {
+    kb = (int64_t)blockIdx.z * L.kchunk;
+    ke = min(g.K, kb + L.kchunk);
+    c_off = (int64_t)blockIdx.z * L.c_split_stride;
+  }
+  const bf16* A = reinterpret_cast<const bf16*>(g.A);
+  const bf16* B = reinterpret_cast<const bf16*>(g.B);
+  // this lane fetches chunk cl of rows (wave*IA + i)*8 + rl
+  const int rl = lane >> 3, cl = (lane & 7) ^ (rl & 7);
+  const int64_t ra0 = m0 + (int64_t)wave * IA * 8 + rl, rb0 = n0 + (int64_t)wave * IB * 8 + rl;
+  auto issue = [&](int buf, int64_t k0) {
+#pragma unroll
+    for (int i = 0; i < IA; ++i) {
+      const int64_t row = min(ra0 + 8 * i, g.M - 1);
+      dma16(A + row * g.lda + k0 + cl * 8, &sA[buf][(wave * IA + i) * 64]);
+    }
+#pragma unroll
+    for (int i = 0; i < IB; ++i) {
+      const int64_t row = min(rb0 + 8 * i, g.N - 1);
+      dma16(B + row * g.ldb + k0 + cl * 8, &sB[buf][(wave * IB + i) * 64]);
+    }
+  };
+  f32x16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+  const int ra = wm * WTM + (lane & 31), rb = wn * WTN + (lane & 31);
+  const int hi = lane >> 5, sw = lane & 7;
+  const int nk = (int)((ke - kb) / 64);
+  if (nk > 0) {
+    issue(0, kb);
+    wait_vmem();
+    __syncthreads();
+  }
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < nk) issue(buf ^ 1, kb + (int64_t)(kt + 1) * 64);
+    const uint4* pa = &sA[buf][ra * 8];
+    const uint4* pb = &sB[buf][rb * 8];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const int cs = (kk * 2 + hi) ^ sw;
+      bf16x8 fa[FM], fb[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i) fa[i] = *reinterpret_cast<const bf16x8*>(&pa[i * 256 + cs]);
+#pragma unroll
+      for (int j = 0; j < FN; ++j) fb[j] = *reinterpret_cast<const bf16x8*>(&pb[j * 256 + cs]);
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+    }
+    wait_vmem();
+    __syncthreads();
+  }
+  OutT* C = reinterpret_cast<OutT*>(g.C) + c_off;
+  const RT* R = HAS_R ? reinterpret_cast<const RT*>(g.R) : nullptr;
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int64_t n = n0 + wn * WTN + j * 32 + (lane & 31);
+      if (n >= g.N) continue;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t m = m0 + wm * WTM + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+        if (m >= g.M) continue;
+        float v = acc[i][j][r] * g.alpha;
+        if (HAS_R) v += to_f(R[m * g.ldr + n]);
+        store_out<OutT>(C + m * g.ldc + n, v);
+      }
+    }
+  }
+#endif
+}
+
 // ------------------------------------------------------------- fp32 GEMM
 // Plain LDS-tiled FMA kernel for fp32 problems (the fp32 single-linear
 // workload); 64x64 tile, 16-deep K slices, 4x4 outputs per thread.
@@ -428,9 +560,48 @@ static void launch_cfg(GemmLaunch& L, hipStream_t stream) {
                                    grid, block, 0, stream, L));
 }
 
+template <int BM, int BN, int WGM, int WGN, typename OutT, typename RT>
+static void launch_dma(GemmLaunch& L, hipStream_t stream) {
+  const GemmArgs& g = L.g;
+  L.tiles_m = (int)((g.M + BM - 1) / BM);
+  L.tiles_n = (int)((g.N + BN - 1) / BN);
+  dim3 grid((unsigned)(L.tiles_m * L.tiles_n), 1, (unsigned)L.ksplit);
+  dim3 block(WGM * WGN * 64);
+  char tag[96];
+  std::snprintf(tag, sizeof(tag), "gemm_nt_dma_kernel<%d, %d, %d, %d, %s, %s, %s>", BM, BN, WGM,
+                WGN, tname<OutT>(), tname<RT>(), g.R ? "true" : "false");
+  double flops, bytes;
+  gemm_work(L, (int)sizeof(OutT), flops, bytes);
+  if (g.R)
+    CATQ_TRACED(stream, tag, flops, bytes, g.M, g.N, g.K,
+                hipLaunchKernelGGL((gemm_nt_dma_kernel<BM, BN, WGM, WGN, OutT, RT, true>), grid,
+                                   block, 0, stream, L));
+  else
+    CATQ_TRACED(stream, tag, flops, bytes, g.M, g.N, g.K,
+                hipLaunchKernelGGL((gemm_nt_dma_kernel<BM, BN, WGM, WGN, OutT, RT, false>), grid,
+                                   block, 0, stream, L));
+}
+
+// The direct-to-LDS NT kernel serves dense bf16 problems whose operands are
+// both K-contiguous with K (per split) a multiple of 64.
+static bool dma_ok(const GemmLaunch& L, int a_t, int b_t) {
+  const GemmArgs& g = L.g;
+  return a_t == 0 && b_t == 0 && g.group_mode == 0 && g.causal == 0 && g.batch == 1 &&
+         g.K % 64 == 0 && (L.ksplit <= 1 || L.kchunk % 64 == 0) && g.lda % 8 == 0 &&
+         g.ldb % 8 == 0 && aligned16(g.A) && aligned16(g.B);
+}
+
 template <int A_T, int B_T, typename OutT, typename RT>
 static void launch_bf16(GemmLaunch& L, hipStream_t stream) {
   const GemmArgs& g = L.g;
+  if (dma_ok(L, A_T, B_T)) {
+    const int64_t t256 = ((g.M + 255) / 256) * ((g.N + 255) / 256) * L.ksplit;
+    if (g.M >= 256 && g.N >= 256 && t256 >= 256)
+      launch_dma<256, 256, 2, 4, OutT, RT>(L, stream);
+    else
+      launch_dma<128, 128, 2, 2, OutT, RT>(L, stream);
+    return;
+  }
   int64_t rows = g.group_mode == 1 ? g.max_rows_per_group : g.M;
   if (rows <= 0) rows = g.M;
   // large output tiles for the big projections, 128x128 for thin problems

@@ -75,7 +75,8 @@ def _bwd_case(catq, M, N, K, mode, s=15.0, seed=4):
         assert max_norm_err(host(a), b) <= 2e-2
 
 
-@pytest.mark.parametrize("M,N,K", [(96, 256, 384), (4096, 256, 256), (1000, 384, 640)])
+@pytest.mark.parametrize("M,N,K", [(96, 256, 384), (4096, 256, 256), (1000, 384, 640),
+                                   (640, 136, 256), (2048, 1024, 512)])
 def test_bwd_soft(catq, M, N, K):
     _bwd_case(catq, M, N, K, catq.SOFT)
 
