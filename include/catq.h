@@ -243,17 +243,19 @@ typedef struct {
  * Causal grouped-query softmax attention on qkv [batch*seq][(n_q + 2 n_kv) d]
  * (q heads, then k heads, then v heads), output o [batch*seq][n_q d].
  * The forward keeps what the backward needs (and its own scratch) in `saved`,
- * at least catq_attn_saved_bytes(a) bytes; the backward needs a scratch
- * workspace of catq_attn_bwd_workspace_bytes(a) bytes and writes dqkv in the
- * layout of qkv.  qkv, o, d_o and dqkv are bf16.
+ * at least catq_attn_saved_bytes(a) bytes; the backward takes the forward's
+ * output o, needs a scratch workspace of catq_attn_bwd_workspace_bytes(a)
+ * bytes and writes dqkv in the layout of qkv.  qkv, o, d_o and dqkv are bf16.
+ * Head dims 64 and 128 run fused (flash) kernels that keep only the per-query
+ * log-sum-exp; 256 runs score matrices through the GEMM kernel.
  */
 size_t catq_attn_saved_bytes(const catq_attn_desc* a);
 size_t catq_attn_bwd_workspace_bytes(const catq_attn_desc* a);
 catq_status catq_aux_attention_fwd(const catq_attn_desc* a, const void* qkv, void* o, void* saved,
                                    size_t saved_bytes, hipStream_t stream);
-catq_status catq_aux_attention_bwd(const catq_attn_desc* a, const void* qkv, const void* saved,
-                                   const void* d_o, void* dqkv, void* workspace,
-                                   size_t workspace_bytes, hipStream_t stream);
+catq_status catq_aux_attention_bwd(const catq_attn_desc* a, const void* qkv, const void* o,
+                                   const void* saved, const void* d_o, void* dqkv,
+                                   void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* SwiGLU on gu [rows][2F] (gate | up): a = silu(gate) * up, [rows][F]. */
 catq_status catq_aux_swiglu_fwd(const void* gu, int64_t rows, int64_t F, void* a,

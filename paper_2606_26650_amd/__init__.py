@@ -154,10 +154,10 @@ def catq_aux_attention_fwd(desc, qkv, o, saved, stream=None):
     _lib.check("catq_aux_attention_fwd", st)
 
 
-def catq_aux_attention_bwd(desc, qkv, saved, d_o, dqkv, workspace, stream=None):
-    st = lib.catq_aux_attention_bwd(C.byref(desc), _ptr(qkv), _ptr(saved), _ptr(d_o), _ptr(dqkv),
-                                    _ptr(workspace), workspace.numel() * workspace.element_size(),
-                                    _stream(stream))
+def catq_aux_attention_bwd(desc, qkv, o, saved, d_o, dqkv, workspace, stream=None):
+    st = lib.catq_aux_attention_bwd(C.byref(desc), _ptr(qkv), _ptr(o), _ptr(saved), _ptr(d_o),
+                                    _ptr(dqkv), _ptr(workspace),
+                                    workspace.numel() * workspace.element_size(), _stream(stream))
     _lib.check("catq_aux_attention_bwd", st)
 
 

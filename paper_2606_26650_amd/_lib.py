@@ -60,7 +60,7 @@ SIGNATURES = {
     "catq_attn_saved_bytes": [PA],
     "catq_attn_bwd_workspace_bytes": [PA],
     "catq_aux_attention_fwd": [PA, P, P, P, SZ, P],
-    "catq_aux_attention_bwd": [PA, P, P, P, P, P, SZ, P],
+    "catq_aux_attention_bwd": [PA, P, P, P, P, P, P, SZ, P],
     "catq_aux_swiglu_fwd": [P, I64, I64, P, P],
     "catq_aux_swiglu_bwd": [P, P, I64, I64, P, P],
     "catq_aux_moe_route": [P, I64, I32, I32, P, P, P, P, P, SZ, P],

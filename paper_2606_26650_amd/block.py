@@ -177,7 +177,7 @@ class DenseBlock:
         lbwd("gu", self.dgu, self.xn2, self.dxn2)
         catq_aux_rmsnorm_bwd(self.h1, self.rstd2, self.dxn2, self.dh1, dres=self.dy)
         lbwd("o", self.dh1, self.attn, self.dattn)
-        catq_aux_attention_bwd(self.desc, self.qkv, self.saved, self.dattn, self.dqkv,
+        catq_aux_attention_bwd(self.desc, self.qkv, self.attn, self.saved, self.dattn, self.dqkv,
                                self.attn_ws)
         lbwd("qkv", self.dqkv, self.xn1, self.dxn1)
         catq_aux_rmsnorm_bwd(x, self.rstd1, self.dxn1, self.dx, dres=self.dh1)
@@ -347,7 +347,7 @@ class MoEBlock:
         catq_aux_moe_scatter_add(self.dxg, self.perm, self.dxn2, k)
         catq_aux_rmsnorm_bwd(self.h1, self.rstd2, self.dxn2, self.dh1, dres=self.dy)
         lbwd("o", self.dh1, self.attn, self.dattn, M)
-        catq_aux_attention_bwd(self.desc, self.qkv, self.saved, self.dattn, self.dqkv,
+        catq_aux_attention_bwd(self.desc, self.qkv, self.attn, self.saved, self.dattn, self.dqkv,
                                self.attn_ws)
         lbwd("qkv", self.dqkv, self.xn1, self.dxn1, M)
         catq_aux_rmsnorm_bwd(x, self.rstd1, self.dxn1, self.dx, dres=self.dh1)

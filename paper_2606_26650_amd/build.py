@@ -19,7 +19,7 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libcatq.so")
 
 SOURCES = ["status.hip", "trace.hip", "lmst.hip", "gemm.hip", "linear.hip", "loss.hip", "glue.hip",
-           "attention.hip"]
+           "attention.hip", "flash.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950",

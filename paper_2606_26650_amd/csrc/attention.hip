@@ -14,6 +14,7 @@
 // (fp32), and the prep-backward sums the q heads of each kv group, undoes the
 // rotation and the q/k RMSNorm and writes d(qkv).
 #include <cmath>
+#include <cstring>
 
 #include "kernels.h"
 
@@ -21,10 +22,11 @@ namespace catq {
 
 struct AttnLayout {
   int64_t B, S, Hq, Hkv, d, G, ld;  // ld = (Hq + 2 Hkv) d
-  // saved buffer (bytes offsets)
-  size_t o_qh, o_kh, o_p, o_rstd, o_cos, o_sin, o_sc, saved_total;
+  bool flash;                        // fused kernels (head_dim 64 or 128)
+  // saved buffer (byte offsets)
+  size_t o_qh, o_kh, o_vh, o_lse, o_p, o_rstd, o_cos, o_sin, o_sc, saved_total;
   // backward workspace
-  size_t o_dp, o_ds, o_dq, o_dk, o_dv, bwd_total;
+  size_t o_dp, o_ds, o_dq, o_dk, o_dv, o_dsum, bwd_total;
 };
 
 static AttnLayout attn_layout(const catq_attn_desc* a) {
@@ -36,27 +38,45 @@ static AttnLayout attn_layout(const catq_attn_desc* a) {
   L.d = a->head_dim;
   L.G = L.Hq / (L.Hkv > 0 ? L.Hkv : 1);
   L.ld = (L.Hq + 2 * L.Hkv) * L.d;
+  L.flash = (L.d == 64 || L.d == 128);
   size_t off = 0;
   auto take = [&](size_t bytes) {
     size_t o = off;
     off = round_up(off + bytes, 256);
     return o;
   };
-  const size_t BHq = (size_t)(L.B * L.Hq), SS = (size_t)(L.S * L.S);
+  const size_t BHq = (size_t)(L.B * L.Hq), BHk = (size_t)(L.B * L.Hkv),
+               SS = (size_t)(L.S * L.S);
   L.o_qh = take(BHq * L.S * L.d * 2);
-  L.o_kh = take((size_t)(L.B * L.Hkv) * L.S * L.d * 2);
-  L.o_p = take(BHq * SS * 2);
+  L.o_kh = take(BHk * L.S * L.d * 2);
   L.o_rstd = take((size_t)(L.B * L.S) * (L.Hq + L.Hkv) * 4);
   L.o_cos = take((size_t)L.S * (L.d / 2) * 4);
   L.o_sin = take((size_t)L.S * (L.d / 2) * 4);
-  L.o_sc = take(BHq * SS * 4);
+  if (L.flash) {
+    L.o_vh = take(BHk * L.S * L.d * 2);
+    L.o_lse = take(BHq * L.S * 4);
+    L.o_p = L.o_sc = 0;
+  } else {
+    L.o_p = take(BHq * SS * 2);
+    L.o_sc = take(BHq * SS * 4);
+    L.o_vh = L.o_lse = 0;
+  }
   L.saved_total = off;
   off = 0;
-  L.o_dp = take(BHq * SS * 4);
-  L.o_ds = take(BHq * SS * 2);
-  L.o_dq = take(BHq * L.S * L.d * 4);
-  L.o_dk = take(BHq * L.S * L.d * 4);
-  L.o_dv = take(BHq * L.S * L.d * 4);
+  if (L.flash) {
+    L.o_dsum = take(BHq * L.S * 4);
+    L.o_dq = take(BHq * L.S * L.d * 4);
+    L.o_dk = take(BHk * L.S * L.d * 4);
+    L.o_dv = take(BHk * L.S * L.d * 4);
+    L.o_dp = L.o_ds = 0;
+  } else {
+    L.o_dp = take(BHq * SS * 4);
+    L.o_ds = take(BHq * SS * 2);
+    L.o_dq = take(BHq * L.S * L.d * 4);
+    L.o_dk = take(BHq * L.S * L.d * 4);
+    L.o_dv = take(BHq * L.S * L.d * 4);
+    L.o_dsum = 0;
+  }
   L.bwd_total = off;
   return L;
 }
@@ -95,16 +115,22 @@ __global__ __launch_bounds__(256) void qk_prep_fwd_kernel(const bf16* qkv, int64
                                                           int Hq, int Hkv, int d, int ld,
                                                           int qk_norm, float eps, const float* cs,
                                                           const float* sn, bf16* Qh, bf16* Kh,
-                                                          float* rstd) {
+                                                          bf16* Vh, float* rstd) {
   const int H = Hq + Hkv;
+  const int Hall = Vh ? H + Hkv : H;
   const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  if (w >= B * S * H) return;
-  const int64_t t = w / H;
-  const int h = (int)(w % H);
+  if (w >= B * S * Hall) return;
+  const int64_t t = w / Hall;
+  const int h = (int)(w % Hall);
   const int64_t b = t / S, s = t % S;
   const int half = d / 2;
   const bf16* src = qkv + t * ld + (int64_t)h * d;
+  if (h >= H) {  // v head: head-major copy
+    bf16* dst = Vh + ((b * Hkv + (h - H)) * S + s) * d;
+    for (int i = lane; i < d; i += 64) dst[i] = src[i];
+    return;
+  }
   float x1[2], x2[2];
   const int np = (half + 63) / 64;
   float ss = 0.f;
@@ -208,7 +234,7 @@ __global__ __launch_bounds__(256) void softmax_bwd_kernel(const bf16* P, const f
 __global__ __launch_bounds__(256) void qk_prep_bwd_kernel(
     const bf16* qkv, const float* rstd, const float* cs, const float* sn, const float* dQ,
     const float* dKp, const float* dVp, int64_t B, int64_t S, int Hq, int Hkv, int d, int ld,
-    int qk_norm, bf16* dqkv) {
+    int qk_norm, int per_kv, bf16* dqkv) {
   const int H = Hq + 2 * Hkv;
   const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
@@ -224,7 +250,10 @@ __global__ __launch_bounds__(256) void qk_prep_bwd_kernel(
     const int kv = h - Hq - Hkv;
     for (int i = lane; i < d; i += 64) {
       float acc = 0.f;
-      for (int gq = 0; gq < G; ++gq) acc += dVp[((b * Hq + kv * G + gq) * S + s) * d + i];
+      if (per_kv)
+        acc = dVp[((b * Hkv + kv) * S + s) * d + i];
+      else
+        for (int gq = 0; gq < G; ++gq) acc += dVp[((b * Hq + kv * G + gq) * S + s) * d + i];
       dst[i] = (bf16)acc;
     }
     return;
@@ -236,6 +265,10 @@ __global__ __launch_bounds__(256) void qk_prep_bwd_kernel(
     if (i >= half) continue;
     if (h < Hq) {
       const float* src = dQ + ((b * Hq + h) * S + s) * d;
+      g1[p] = src[i];
+      g2[p] = src[i + half];
+    } else if (per_kv) {
+      const float* src = dKp + ((b * Hkv + (h - Hq)) * S + s) * d;
       g1[p] = src[i];
       g2[p] = src[i + half];
     } else {
@@ -338,6 +371,7 @@ extern "C" catq_status catq_aux_attention_fwd(const catq_attn_desc* a, const voi
   char* sv = reinterpret_cast<char*>(saved);
   bf16* Qh = reinterpret_cast<bf16*>(sv + L.o_qh);
   bf16* Kh = reinterpret_cast<bf16*>(sv + L.o_kh);
+  bf16* Vh = L.flash ? reinterpret_cast<bf16*>(sv + L.o_vh) : nullptr;
   bf16* P = reinterpret_cast<bf16*>(sv + L.o_p);
   float* rstd = reinterpret_cast<float*>(sv + L.o_rstd);
   float* cs = reinterpret_cast<float*>(sv + L.o_cos);
@@ -347,11 +381,27 @@ extern "C" catq_status catq_aux_attention_fwd(const catq_attn_desc* a, const voi
   hipLaunchKernelGGL(rope_table_kernel, dim3((unsigned)((L.S * half + 255) / 256)), dim3(256), 0,
                      stream, L.S, (int)L.d, std::log2((double)a->rope_theta), cs, sn);
   CATQ_CHECK_LAUNCH("rope table");
-  const int64_t nw = L.B * L.S * (L.Hq + L.Hkv);
+  const int64_t nw = L.B * L.S * (L.Hq + L.Hkv + (L.flash ? L.Hkv : 0));
   hipLaunchKernelGGL(qk_prep_fwd_kernel, dim3((unsigned)((nw + 3) / 4)), dim3(256), 0, stream,
                      (const bf16*)qkv, L.B, L.S, (int)L.Hq, (int)L.Hkv, (int)L.d, (int)L.ld,
-                     a->qk_norm, a->eps, cs, sn, Qh, Kh, rstd);
+                     a->qk_norm, a->eps, cs, sn, Qh, Kh, Vh, rstd);
   CATQ_CHECK_LAUNCH("qk prep");
+  if (L.flash) {
+    FaArgs f;
+    std::memset(&f, 0, sizeof(f));
+    f.Q = Qh;
+    f.K = Kh;
+    f.V = Vh;
+    f.O = reinterpret_cast<bf16*>(o);
+    f.lse = reinterpret_cast<float*>(sv + L.o_lse);
+    f.B = (int)L.B;
+    f.S = (int)L.S;
+    f.Hq = (int)L.Hq;
+    f.Hkv = (int)L.Hkv;
+    f.scale = (float)(1.0 / std::sqrt((double)L.d));
+    f.c = (float)(1.4426950408889634 / std::sqrt((double)L.d));
+    return flash_forward((int)L.d, f, stream);
+  }
   // scores
   {
     GemmArgs g = gemm_args_default();
@@ -407,14 +457,14 @@ extern "C" catq_status catq_aux_attention_fwd(const catq_attn_desc* a, const voi
 }
 
 extern "C" catq_status catq_aux_attention_bwd(const catq_attn_desc* a, const void* qkv,
-                                              const void* saved, const void* d_o, void* dqkv,
-                                              void* workspace, size_t workspace_bytes,
-                                              hipStream_t stream) {
+                                              const void* o, const void* saved, const void* d_o,
+                                              void* dqkv, void* workspace,
+                                              size_t workspace_bytes, hipStream_t stream) {
   clear_error();
   CATQ_TRY(check_desc(a));
-  CATQ_REQUIRE(qkv && saved && d_o && dqkv && workspace, CATQ_ERR_NULL, "NULL argument");
-  CATQ_REQUIRE(aligned16(qkv) && aligned16(saved) && aligned16(d_o) && aligned16(dqkv) &&
-                   aligned16(workspace),
+  CATQ_REQUIRE(qkv && o && saved && d_o && dqkv && workspace, CATQ_ERR_NULL, "NULL argument");
+  CATQ_REQUIRE(aligned16(qkv) && aligned16(o) && aligned16(saved) && aligned16(d_o) &&
+                   aligned16(dqkv) && aligned16(workspace),
                CATQ_ERR_ALIGN, "misaligned");
   const AttnLayout L = attn_layout(a);
   CATQ_REQUIRE(workspace_bytes >= L.bwd_total, CATQ_ERR_WORKSPACE,
@@ -432,6 +482,27 @@ extern "C" catq_status catq_aux_attention_bwd(const catq_attn_desc* a, const voi
   float* dQ = reinterpret_cast<float*>(ws + L.o_dq);
   float* dKp = reinterpret_cast<float*>(ws + L.o_dk);
   float* dVp = reinterpret_cast<float*>(ws + L.o_dv);
+  if (L.flash) {
+    FaArgs f;
+    std::memset(&f, 0, sizeof(f));
+    f.Q = Qh;
+    f.K = Kh;
+    f.V = reinterpret_cast<const bf16*>(sv + L.o_vh);
+    f.O = const_cast<bf16*>(reinterpret_cast<const bf16*>(o));
+    f.lse = const_cast<float*>(reinterpret_cast<const float*>(sv + L.o_lse));
+    f.dO = reinterpret_cast<const bf16*>(d_o);
+    f.Dsum = reinterpret_cast<float*>(ws + L.o_dsum);
+    f.dQ = dQ;
+    f.dK = dKp;
+    f.dV = dVp;
+    f.B = (int)L.B;
+    f.S = (int)L.S;
+    f.Hq = (int)L.Hq;
+    f.Hkv = (int)L.Hkv;
+    f.scale = (float)(1.0 / std::sqrt((double)L.d));
+    f.c = (float)(1.4426950408889634 / std::sqrt((double)L.d));
+    CATQ_TRY(flash_backward((int)L.d, f, stream));
+  } else {
   const bf16* V = reinterpret_cast<const bf16*>(qkv) + (L.Hq + L.Hkv) * L.d;
   // dP = dO V^T
   {
@@ -514,11 +585,12 @@ extern "C" catq_status catq_aux_attention_bwd(const catq_attn_desc* a, const voi
     g.b_si = L.d;
     CATQ_TRY(gemm_run(g, 1, 1, CATQ_BF16, CATQ_F32, stream));
   }
+  }
   const int64_t nw = L.B * L.S * (L.Hq + 2 * L.Hkv);
   hipLaunchKernelGGL(qk_prep_bwd_kernel, dim3((unsigned)((nw + 3) / 4)), dim3(256), 0, stream,
                      (const bf16*)qkv, rstd, cs, sn, (const float*)dQ, (const float*)dKp,
                      (const float*)dVp, L.B, L.S, (int)L.Hq, (int)L.Hkv, (int)L.d, (int)L.ld,
-                     a->qk_norm, (bf16*)dqkv);
+                     a->qk_norm, L.flash ? 1 : 0, (bf16*)dqkv);
   CATQ_CHECK_LAUNCH("qk prep bwd");
   return CATQ_OK;
 }

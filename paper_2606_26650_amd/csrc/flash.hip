@@ -1,0 +1,502 @@
+// Fused causal grouped-query attention (forward and backward) on matrix cores
+// (gfx950, v_mfma_f32_32x32x16_bf16), head dimension D in {64, 128}.
+//
+// Layout trick: every score tile is computed as S^T (keys x queries), so the
+// 32x32 accumulator gives each lane ONE query column and 16 key rows.  The
+// softmax over keys is then a reduction over the lane's own registers plus one
+// exchange with lane^32, and the accumulator registers are directly the MFMA
+// operand of the next product (P.V, dS.K, ...) once the other operand is read
+// from LDS in the same key order (keys 4g..4g+3 and 8+4g..8+4g+3 of each
+// 16-key slice, g = lane/32).
+//
+// Forward: one block = 4 wavefronts x 32 queries of one (batch, q head); key
+// tiles of 64 stream through LDS (K as [key][d], V transposed as [d][key]);
+// online softmax in base 2; O written token-major, and the per-query
+// log-sum-exp (base 2) kept for the backward.
+// Backward: dK/dV kernel (block = 4 x 32 keys of one kv head, looping over the
+// q heads of its group and the causal query tiles) and dQ kernel (block = 4 x
+// 32 queries, looping over key tiles); P and dS are recomputed from the saved
+// log-sum-exp and D = rowsum(dO * O).  No atomics: every output element is
+// owned by one lane.
+#include <cmath>
+
+#include "kernels.h"
+
+namespace catq {
+
+namespace fa {
+
+constexpr int BK = 64;   // keys (or queries) per streamed tile
+constexpr int NT = 256;  // 4 wavefronts
+constexpr int TP = BK + 4;  // pitch (elements) of transposed [d][64] tiles
+
+template <int D>
+struct Cfg {
+  static constexpr int KP = D + 8;             // pitch of [row][d] tiles (16-byte rows)
+  static constexpr int NCH = D / 8;            // 16-byte chunks per row
+  static constexpr int ITEMS = (BK / 4) * NCH;  // 4-row x 8-column items per tile
+  static constexpr int KS = D / 16;            // 16-wide slices of d
+  static constexpr int DB = D / 32;            // 32-row blocks of d
+};
+
+// Registers of one 64 x D tile: each thread owns rows 4*kb4 .. 4*kb4+3 and
+// columns 8*db .. 8*db+7 (db varies fastest across lanes: 16-byte loads of
+// consecutive lanes are contiguous in a row).
+template <int D>
+struct Tile {
+  u32x4 r[4];
+  bool active;
+  int kb4, db;
+  __device__ __forceinline__ void load(const bf16* __restrict__ base, int64_t ld, int64_t row0,
+                                       int64_t rows, int tid) {
+    active = tid < Cfg<D>::ITEMS;
+    db = tid % Cfg<D>::NCH;
+    kb4 = tid / Cfg<D>::NCH;
+    const u32x4 z = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t row = row0 + 4 * kb4 + j;
+      r[j] = (active && row < rows)
+                 ? *reinterpret_cast<const u32x4*>(base + row * ld + 8 * db)
+                 : z;
+    }
+  }
+  // [row][KP] layout
+  __device__ __forceinline__ void store_rows(u16* lds) const {
+    if (!active) return;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      *reinterpret_cast<u32x4*>(lds + (4 * kb4 + j) * Cfg<D>::KP + 8 * db) = r[j];
+  }
+  // [d][TP] layout, 4-element quads XOR-swizzled by (d >> 3) & 15
+  __device__ __forceinline__ void store_transposed(u16* lds) const {
+    if (!active) return;
+#pragma unroll
+    for (int mm = 0; mm < 8; ++mm) {
+      const unsigned sel = (mm & 1) ? 0x07060302u : 0x05040100u;
+      const int dw = mm >> 1;
+      uint2 o;
+      o.x = __builtin_amdgcn_perm(r[1][dw], r[0][dw], sel);
+      o.y = __builtin_amdgcn_perm(r[3][dw], r[2][dw], sel);
+      const int d = 8 * db + mm;
+      const int q = kb4 ^ ((d >> 3) & 15);
+      *reinterpret_cast<uint2*>(lds + d * TP + 4 * q) = o;
+    }
+  }
+};
+
+__device__ __forceinline__ bf16x8 frag_rows(const u16* lds, int row, int col, int pitch) {
+  return *reinterpret_cast<const bf16x8*>(lds + row * pitch + col);
+}
+
+// Operand fragment from a transposed [d][TP] tile: row d, keys
+// 16*slice + 4g .. +3 and 16*slice + 8 + 4g .. +3 (slice = 16-key slice index)
+__device__ __forceinline__ bf16x8 frag_tr(const u16* lds, int d, int slice, int g) {
+  const int s = (d >> 3) & 15;
+  const int q1 = (4 * slice + g) ^ s, q2 = (4 * slice + 2 + g) ^ s;
+  const uint2 a = *reinterpret_cast<const uint2*>(lds + d * TP + 4 * q1);
+  const uint2 b = *reinterpret_cast<const uint2*>(lds + d * TP + 4 * q2);
+  u32x4 v = {a.x, a.y, b.x, b.y};
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+// 8 accumulator values (regs 8h..8h+7 of a 32x32 block) -> bf16 operand
+__device__ __forceinline__ bf16x8 pack8(const f32x16& a, int h) {
+  u32x4 v;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) v[i] = pack_bf16x2(a[8 * h + 2 * i], a[8 * h + 2 * i + 1]);
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+__device__ __forceinline__ f32x16 zero16() {
+  f32x16 z;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) z[i] = 0.f;
+  return z;
+}
+
+// row (within a 32-row accumulator block) of register r for lane group g
+__device__ __forceinline__ int acc_row(int r, int g) { return 8 * (r >> 2) + 4 * g + (r & 3); }
+
+}  // namespace fa
+
+// ------------------------------------------------------------------ forward
+
+template <int D>
+__global__ __launch_bounds__(fa::NT, 1) void flash_fwd_kernel(FaArgs a) {
+  using C = fa::Cfg<D>;
+  __shared__ u16 sK[fa::BK * C::KP];
+  __shared__ u16 sV[D * fa::TP];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 5, l32 = lane & 31;
+  const int qt = blockIdx.x, h = blockIdx.y % a.Hq, b = blockIdx.y / a.Hq;
+  const int kvh = h / (a.Hq / a.Hkv);
+  const int q0 = qt * 128;
+  const int qme = q0 + 32 * w + l32;  // this lane's query
+  const bf16* Qb = a.Q + ((int64_t)(b * a.Hq + h) * a.S) * D;
+  const bf16* Kb = a.K + ((int64_t)(b * a.Hkv + kvh) * a.S) * D;
+  const bf16* Vb = a.V + ((int64_t)(b * a.Hkv + kvh) * a.S) * D;
+
+  // Q fragments (operand B of S^T = K Q^T): lane holds query qme, d slice t
+  bf16x8 qf[C::KS];
+#pragma unroll
+  for (int t = 0; t < C::KS; ++t) {
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (qme < a.S) v = *reinterpret_cast<const u32x4*>(Qb + (int64_t)qme * D + 16 * t + 8 * g);
+    qf[t] = __builtin_bit_cast(bf16x8, v);
+  }
+  f32x16 o[C::DB];
+#pragma unroll
+  for (int i = 0; i < C::DB; ++i) o[i] = fa::zero16();
+  float m = -INFINITY, l = 0.f;
+
+  const int q_last = min(q0 + 127, a.S - 1);
+  const int nkt = q_last / fa::BK + 1;
+  const int wave_last = q0 + 32 * w + 31;  // keys beyond this do not matter to the wave
+  fa::Tile<D> tk, tv;
+  tk.load(Kb, D, 0, a.S, tid);
+  tv.load(Vb, D, 0, a.S, tid);
+  for (int kt = 0; kt < nkt; ++kt) {
+    const int k0 = kt * fa::BK;
+    __syncthreads();  // previous tile fully consumed
+    tk.store_rows(sK);
+    tv.store_transposed(sV);
+    __syncthreads();
+    if (kt + 1 < nkt) {
+      tk.load(Kb, D, k0 + fa::BK, a.S, tid);
+      tv.load(Vb, D, k0 + fa::BK, a.S, tid);
+    }
+    if (k0 > wave_last) continue;
+    // S^T for the two 32-key blocks
+    f32x16 s[2];
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb) {
+      s[sb] = fa::zero16();
+#pragma unroll
+      for (int t = 0; t < C::KS; ++t)
+        s[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            fa::frag_rows(sK, sb * 32 + l32, 16 * t + 8 * g, C::KP), qf[t], s[sb], 0, 0, 0);
+    }
+    // scale to base 2, causal and length mask, tile max
+    float mt = -INFINITY;
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = k0 + sb * 32 + fa::acc_row(r, g);
+        float x = s[sb][r] * a.c;
+        if (key > qme || key >= a.S) x = -INFINITY;
+        s[sb][r] = x;
+        mt = fmaxf(mt, x);
+      }
+    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+    const float mn = fmaxf(m, mt);
+    // a lane whose query lies past the sequence end sees only masked keys
+    const float msafe = (mn == -INFINITY) ? 0.f : mn;
+    const float alpha = exp2f(m - msafe);
+    float rs = 0.f;
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float p = exp2f(s[sb][r] - msafe);
+        s[sb][r] = p;
+        rs += p;
+      }
+    rs += __shfl_xor(rs, 32, 64);
+    l = l * alpha + rs;
+    m = mn;
+#pragma unroll
+    for (int i = 0; i < C::DB; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[i][r] *= alpha;
+    // O^T += V^T P^T
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const bf16x8 pf = fa::pack8(s[sb], hh);
+#pragma unroll
+        for (int i = 0; i < C::DB; ++i)
+          o[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              fa::frag_tr(sV, i * 32 + l32, 2 * sb + hh, g), pf, o[i], 0, 0, 0);
+      }
+  }
+  if (qme < a.S) {
+    const float inv = 1.0f / l;
+    bf16* Ob = a.O + ((int64_t)b * a.S + qme) * (int64_t)(a.Hq * D) + (int64_t)h * D;
+#pragma unroll
+    for (int i = 0; i < C::DB; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) Ob[i * 32 + fa::acc_row(r, g)] = (bf16)(o[i][r] * inv);
+    if (g == 0) a.lse[(int64_t)(b * a.Hq + h) * a.S + qme] = m + log2f(l);
+  }
+}
+
+// D = rowsum(dO * O) per (batch, q head, query); one wavefront per row pair.
+template <int D>
+__global__ __launch_bounds__(256) void flash_dsum_kernel(FaArgs a) {
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);  // (b*S + q)*Hq + h
+  const int lane = threadIdx.x & 63;
+  if (row >= (int64_t)a.B * a.S * a.Hq) return;
+  const int h = (int)(row % a.Hq);
+  const int64_t t = row / a.Hq;  // token b*S + q
+  const bf16* o = a.O + t * (int64_t)(a.Hq * D) + (int64_t)h * D;
+  const bf16* d = a.dO + t * (int64_t)(a.Hq * D) + (int64_t)h * D;
+  float acc = 0.f;
+  for (int i = lane; i < D; i += 64) acc = fmaf(to_f(o[i]), to_f(d[i]), acc);
+  acc = wave_sum(acc);
+  if (lane == 0) {
+    const int64_t b = t / a.S, q = t % a.S;
+    a.Dsum[(b * a.Hq + h) * a.S + q] = acc;
+  }
+}
+
+// ------------------------------------------------------------- dK and dV
+
+template <int D>
+__global__ __launch_bounds__(fa::NT, 1) void flash_bwd_dkdv_kernel(FaArgs a) {
+  using C = fa::Cfg<D>;
+  __shared__ u16 sQ[fa::BK * C::KP];
+  __shared__ u16 sQt[D * fa::TP];
+  __shared__ u16 sO[fa::BK * C::KP];   // dO rows
+  __shared__ u16 sOt[D * fa::TP];      // dO transposed
+  __shared__ float sL[fa::BK], sD[fa::BK];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 5, l32 = lane & 31;
+  const int kt = blockIdx.x, kvh = blockIdx.y % a.Hkv, b = blockIdx.y / a.Hkv;
+  const int G = a.Hq / a.Hkv;
+  const int k0 = kt * 128;
+  const int kme = k0 + 32 * w + l32;  // this lane's key (column of S^T[q][key])
+  const bf16* Kb = a.K + ((int64_t)(b * a.Hkv + kvh) * a.S) * D;
+  const bf16* Vb = a.V + ((int64_t)(b * a.Hkv + kvh) * a.S) * D;
+  // K and V fragments of this lane's key (operand B of S^T = Q K^T and dP^T = dO V^T)
+  bf16x8 kf[C::KS], vf[C::KS];
+#pragma unroll
+  for (int t = 0; t < C::KS; ++t) {
+    u32x4 kv = {0u, 0u, 0u, 0u}, vv = {0u, 0u, 0u, 0u};
+    if (kme < a.S) {
+      kv = *reinterpret_cast<const u32x4*>(Kb + (int64_t)kme * D + 16 * t + 8 * g);
+      vv = *reinterpret_cast<const u32x4*>(Vb + (int64_t)kme * D + 16 * t + 8 * g);
+    }
+    kf[t] = __builtin_bit_cast(bf16x8, kv);
+    vf[t] = __builtin_bit_cast(bf16x8, vv);
+  }
+  f32x16 dk[C::DB], dv[C::DB];
+#pragma unroll
+  for (int i = 0; i < C::DB; ++i) {
+    dk[i] = fa::zero16();
+    dv[i] = fa::zero16();
+  }
+  const int wave_first = k0 + 32 * w;  // queries below this see none of the wave's keys
+  const int qt0 = k0 / fa::BK;
+  const int nqt = (a.S + fa::BK - 1) / fa::BK;
+  for (int gq = 0; gq < G; ++gq) {
+    const int h = kvh * G + gq;
+    const bf16* Qb = a.Q + ((int64_t)(b * a.Hq + h) * a.S) * D;
+    const float* Lb = a.lse + (int64_t)(b * a.Hq + h) * a.S;
+    const float* Db = a.Dsum + (int64_t)(b * a.Hq + h) * a.S;
+    const bf16* dOb = a.dO + (int64_t)b * a.S * (a.Hq * D) + (int64_t)h * D;
+    fa::Tile<D> tq, to;
+    tq.load(Qb, D, (int64_t)qt0 * fa::BK, a.S, tid);
+    to.load(dOb, (int64_t)a.Hq * D, (int64_t)qt0 * fa::BK, a.S, tid);
+    for (int qt = qt0; qt < nqt; ++qt) {
+      const int q0 = qt * fa::BK;
+      __syncthreads();
+      tq.store_rows(sQ);
+      tq.store_transposed(sQt);
+      to.store_rows(sO);
+      to.store_transposed(sOt);
+      if (tid < fa::BK) {
+        const int q = q0 + tid;
+        sL[tid] = q < a.S ? Lb[q] : 0.f;
+        sD[tid] = q < a.S ? Db[q] : 0.f;
+      }
+      __syncthreads();
+      if (qt + 1 < nqt) {
+        tq.load(Qb, D, (int64_t)(q0 + fa::BK), a.S, tid);
+        to.load(dOb, (int64_t)a.Hq * D, (int64_t)(q0 + fa::BK), a.S, tid);
+      }
+      if (q0 + fa::BK - 1 < wave_first) continue;
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb) {
+        // S^T[q][key] and dP^T[q][key] for 32 queries
+        f32x16 s = fa::zero16(), dp = fa::zero16();
+#pragma unroll
+        for (int t = 0; t < C::KS; ++t) {
+          s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              fa::frag_rows(sQ, qb * 32 + l32, 16 * t + 8 * g, C::KP), kf[t], s, 0, 0, 0);
+          dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              fa::frag_rows(sO, qb * 32 + l32, 16 * t + 8 * g, C::KP), vf[t], dp, 0, 0, 0);
+        }
+        // P and dS (rows = queries of this lane's registers)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int qi = qb * 32 + fa::acc_row(r, g);
+          const int q = q0 + qi;
+          float p = exp2f(s[r] * a.c - sL[qi]);
+          if (q < kme || q >= a.S || kme >= a.S) p = 0.f;
+          s[r] = p;
+          dp[r] = p * (dp[r] - sD[qi]);
+        }
+        // dV[key][d] += P^T dO ; dK[key][d] += dS^T Q  (contraction over queries)
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          const bf16x8 pf = fa::pack8(s, hh), df = fa::pack8(dp, hh);
+#pragma unroll
+          for (int i = 0; i < C::DB; ++i) {
+            dv[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                pf, fa::frag_tr(sOt, i * 32 + l32, 2 * qb + hh, g), dv[i], 0, 0, 0);
+            dk[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                df, fa::frag_tr(sQt, i * 32 + l32, 2 * qb + hh, g), dk[i], 0, 0, 0);
+          }
+        }
+      }
+    }
+  }
+  // dv[i][r]: key row = 32w + acc_row(r, g) within the block, d column = 32i + l32
+  float* dKb = a.dK + ((int64_t)(b * a.Hkv + kvh) * a.S) * D;
+  float* dVb = a.dV + ((int64_t)(b * a.Hkv + kvh) * a.S) * D;
+#pragma unroll
+  for (int i = 0; i < C::DB; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int key = k0 + 32 * w + fa::acc_row(r, g);
+      if (key < a.S) {
+        dKb[(int64_t)key * D + 32 * i + l32] = dk[i][r] * a.scale;
+        dVb[(int64_t)key * D + 32 * i + l32] = dv[i][r];
+      }
+    }
+}
+
+// ------------------------------------------------------------------- dQ
+
+template <int D>
+__global__ __launch_bounds__(fa::NT, 1) void flash_bwd_dq_kernel(FaArgs a) {
+  using C = fa::Cfg<D>;
+  __shared__ u16 sK[fa::BK * C::KP];
+  __shared__ u16 sKt[D * fa::TP];
+  __shared__ u16 sV[fa::BK * C::KP];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 5, l32 = lane & 31;
+  const int qt = blockIdx.x, h = blockIdx.y % a.Hq, b = blockIdx.y / a.Hq;
+  const int kvh = h / (a.Hq / a.Hkv);
+  const int q0 = qt * 128;
+  const int qme = q0 + 32 * w + l32;
+  const bf16* Qb = a.Q + ((int64_t)(b * a.Hq + h) * a.S) * D;
+  const bf16* Kb = a.K + ((int64_t)(b * a.Hkv + kvh) * a.S) * D;
+  const bf16* Vb = a.V + ((int64_t)(b * a.Hkv + kvh) * a.S) * D;
+  const bf16* dOb = a.dO + (int64_t)b * a.S * (a.Hq * D) + (int64_t)h * D;
+  bf16x8 qf[C::KS], of[C::KS];
+#pragma unroll
+  for (int t = 0; t < C::KS; ++t) {
+    u32x4 qv = {0u, 0u, 0u, 0u}, ov = {0u, 0u, 0u, 0u};
+    if (qme < a.S) {
+      qv = *reinterpret_cast<const u32x4*>(Qb + (int64_t)qme * D + 16 * t + 8 * g);
+      ov = *reinterpret_cast<const u32x4*>(dOb + (int64_t)qme * (a.Hq * D) + 16 * t + 8 * g);
+    }
+    qf[t] = __builtin_bit_cast(bf16x8, qv);
+    of[t] = __builtin_bit_cast(bf16x8, ov);
+  }
+  const float lse = qme < a.S ? a.lse[(int64_t)(b * a.Hq + h) * a.S + qme] : 0.f;
+  const float dsum = qme < a.S ? a.Dsum[(int64_t)(b * a.Hq + h) * a.S + qme] : 0.f;
+  f32x16 dq[C::DB];
+#pragma unroll
+  for (int i = 0; i < C::DB; ++i) dq[i] = fa::zero16();
+  const int q_last = min(q0 + 127, a.S - 1);
+  const int nkt = q_last / fa::BK + 1;
+  const int wave_last = q0 + 32 * w + 31;
+  fa::Tile<D> tk, tv;
+  tk.load(Kb, D, 0, a.S, tid);
+  tv.load(Vb, D, 0, a.S, tid);
+  for (int kt = 0; kt < nkt; ++kt) {
+    const int k0 = kt * fa::BK;
+    __syncthreads();
+    tk.store_rows(sK);
+    tk.store_transposed(sKt);
+    tv.store_rows(sV);
+    __syncthreads();
+    if (kt + 1 < nkt) {
+      tk.load(Kb, D, k0 + fa::BK, a.S, tid);
+      tv.load(Vb, D, k0 + fa::BK, a.S, tid);
+    }
+    if (k0 > wave_last) continue;
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb) {
+      f32x16 s = fa::zero16(), dp = fa::zero16();
+#pragma unroll
+      for (int t = 0; t < C::KS; ++t) {
+        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            fa::frag_rows(sK, sb * 32 + l32, 16 * t + 8 * g, C::KP), qf[t], s, 0, 0, 0);
+        dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            fa::frag_rows(sV, sb * 32 + l32, 16 * t + 8 * g, C::KP), of[t], dp, 0, 0, 0);
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = k0 + sb * 32 + fa::acc_row(r, g);
+        float p = exp2f(s[r] * a.c - lse);
+        if (key > qme || key >= a.S || qme >= a.S) p = 0.f;
+        dp[r] = p * (dp[r] - dsum);
+      }
+      // dQ^T[d][q] += K^T dS  (contraction over keys)
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const bf16x8 df = fa::pack8(dp, hh);
+#pragma unroll
+        for (int i = 0; i < C::DB; ++i)
+          dq[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              fa::frag_tr(sKt, i * 32 + l32, 2 * sb + hh, g), df, dq[i], 0, 0, 0);
+      }
+    }
+  }
+  if (qme < a.S) {
+    float* dQb = a.dQ + ((int64_t)(b * a.Hq + h) * a.S + qme) * D;
+#pragma unroll
+    for (int i = 0; i < C::DB; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) dQb[i * 32 + fa::acc_row(r, g)] = dq[i][r] * a.scale;
+  }
+}
+
+// ------------------------------------------------------------------ launch
+
+catq_status flash_forward(int D, FaArgs& a, hipStream_t stream) {
+  dim3 grid((unsigned)((a.S + 127) / 128), (unsigned)(a.B * a.Hq)), block(fa::NT);
+  const double f = 2.0 * 2.0 * (double)a.B * a.Hq * (double)a.S * a.S * D * 0.5;
+  const double by = 2.0 * (double)a.B * a.S * D * (2.0 * a.Hq + 2.0 * a.Hkv) + 4.0 * a.B * a.Hq * a.S;
+  if (D == 128)
+    CATQ_TRACED(stream, "flash_fwd_kernel<128>", f, by, a.S, a.Hq, D,
+                hipLaunchKernelGGL(flash_fwd_kernel<128>, grid, block, 0, stream, a));
+  else
+    CATQ_TRACED(stream, "flash_fwd_kernel<64>", f, by, a.S, a.Hq, D,
+                hipLaunchKernelGGL(flash_fwd_kernel<64>, grid, block, 0, stream, a));
+  CATQ_CHECK_LAUNCH("flash forward");
+  return CATQ_OK;
+}
+
+catq_status flash_backward(int D, FaArgs& a, hipStream_t stream) {
+  const int64_t rows = (int64_t)a.B * a.S * a.Hq;
+  dim3 gs((unsigned)((rows + 3) / 4));
+  if (D == 128)
+    hipLaunchKernelGGL(flash_dsum_kernel<128>, gs, dim3(256), 0, stream, a);
+  else
+    hipLaunchKernelGGL(flash_dsum_kernel<64>, gs, dim3(256), 0, stream, a);
+  CATQ_CHECK_LAUNCH("flash dsum");
+  const double half = 0.5 * 2.0 * (double)a.B * a.Hq * (double)a.S * a.S * D;
+  dim3 gkv((unsigned)((a.S + 127) / 128), (unsigned)(a.B * a.Hkv)), block(fa::NT);
+  if (D == 128)
+    CATQ_TRACED(stream, "flash_bwd_dkdv_kernel<128>", 4.0 * half, 0.0, a.S, a.Hkv, D,
+                hipLaunchKernelGGL(flash_bwd_dkdv_kernel<128>, gkv, block, 0, stream, a));
+  else
+    CATQ_TRACED(stream, "flash_bwd_dkdv_kernel<64>", 4.0 * half, 0.0, a.S, a.Hkv, D,
+                hipLaunchKernelGGL(flash_bwd_dkdv_kernel<64>, gkv, block, 0, stream, a));
+  CATQ_CHECK_LAUNCH("flash dK dV");
+  dim3 gq((unsigned)((a.S + 127) / 128), (unsigned)(a.B * a.Hq));
+  if (D == 128)
+    CATQ_TRACED(stream, "flash_bwd_dq_kernel<128>", 3.0 * half, 0.0, a.S, a.Hq, D,
+                hipLaunchKernelGGL(flash_bwd_dq_kernel<128>, gq, block, 0, stream, a));
+  else
+    CATQ_TRACED(stream, "flash_bwd_dq_kernel<64>", 3.0 * half, 0.0, a.S, a.Hq, D,
+                hipLaunchKernelGGL(flash_bwd_dq_kernel<64>, gq, block, 0, stream, a));
+  CATQ_CHECK_LAUNCH("flash dQ");
+  return CATQ_OK;
+}
+
+}  // namespace catq

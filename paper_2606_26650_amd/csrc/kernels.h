@@ -78,4 +78,23 @@ catq_status gemm_run_split(const GemmArgs& a, int a_t, int b_t, catq_dtype in_dt
                            hipStream_t stream, catq_dtype r_dtype = CATQ_BF16);
 int gemm_split_count(const GemmArgs& a, int ksplit);
 
+// ---------------------------------------------------------- fused attention
+struct FaArgs {
+  const bf16* Q;      // [B][Hq][S][D]
+  const bf16* K;      // [B][Hkv][S][D]
+  const bf16* V;      // [B][Hkv][S][D]
+  bf16* O;            // token-major [B*S][Hq*D]
+  float* lse;         // [B][Hq][S], base 2
+  const bf16* dO;     // token-major [B*S][Hq*D]
+  float* Dsum;        // [B][Hq][S]
+  float* dQ;          // [B][Hq][S][D]
+  float* dK;          // [B][Hkv][S][D]
+  float* dV;          // [B][Hkv][S][D]
+  int B, S, Hq, Hkv;
+  float c;            // softmax scale * log2(e)
+  float scale;        // softmax scale
+};
+catq_status flash_forward(int D, FaArgs& a, hipStream_t stream);
+catq_status flash_backward(int D, FaArgs& a, hipStream_t stream);
+
 }  // namespace catq

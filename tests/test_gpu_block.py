@@ -35,7 +35,7 @@ def _oracle_attention(qkv, cfg, dO):
 
 
 @pytest.mark.parametrize("S,d,qk", [(80, 64, True), (136, 128, True), (264, 64, False),
-                                    (512, 128, True)])
+                                    (512, 128, True), (200, 256, True), (1000, 128, False)])
 def test_attention_parity(catq, S, d, qk):
     import torch
     cfg = sg.small_dense(batch=2, seq=S, n_q=4, n_kv=2, head_dim=d, qk_norm=qk)
@@ -50,7 +50,7 @@ def test_attention_parity(catq, S, d, qk):
     o = torch.empty(M, cfg.n_q * d, dtype=torch.bfloat16, device="cuda")
     dqkv = torch.empty(M, ld, dtype=torch.bfloat16, device="cuda")
     catq.catq_aux_attention_fwd(desc, qkv, o, saved)
-    catq.catq_aux_attention_bwd(desc, qkv, saved, dO, dqkv, ws)
+    catq.catq_aux_attention_bwd(desc, qkv, o, saved, dO, dqkv, ws)
     torch.cuda.synchronize()
     Oref, dref = _oracle_attention(f64(qb), cfg, f64(gb))
     assert max_norm_err(host(o), Oref) <= 2e-2
