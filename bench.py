@@ -218,6 +218,16 @@ def main():
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, W, xb)
     if args.breakdown:
+        shp = {}
+        for r in recs:
+            if r["flops"] > 0:
+                a = shp.setdefault((r["tag"], r["M"], r["N"], r["K"]), [0, 0.0, 0.0])
+                a[0] += 1
+                a[1] += r["ms"]
+                a[2] += r["flops"]
+        for (t, m, n, k), (c, ms, fl) in sorted(shp.items(), key=lambda kv: -kv[1][1]):
+            print(f"{ms / args.steps:9.3f} ms/step {c // args.steps:3d}x {fl / (ms * 1e-3) / 1e12:8.1f} TF/s"
+                  f"  M={m} N={n} K={k}  {t}", file=sys.stderr)
         for k, v in sorted(agg.items(), key=lambda kv: -kv[1]["ms"]):
             tf = v["flops"] / (v["ms"] * 1e-3) / 1e12 if v["flops"] else 0
             gb = v["bytes"] / (v["ms"] * 1e-3) / 1e9

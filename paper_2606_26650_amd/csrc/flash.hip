@@ -123,12 +123,14 @@ __device__ __forceinline__ int acc_row(int r, int g) { return 8 * (r >> 2) + 4 *
 // ------------------------------------------------------------------ forward
 
 template <int D>
-__global__ __launch_bounds__(fa::NT, 1) void flash_fwd_kernel(FaArgs a) {
+__global__ __launch_bounds__(fa::NT, 2) void flash_fwd_kernel(FaArgs a) {
   using C = fa::Cfg<D>;
   __shared__ u16 sK[fa::BK * C::KP];
   __shared__ u16 sV[D * fa::TP];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 5, l32 = lane & 31;
-  const int qt = blockIdx.x, h = blockIdx.y % a.Hq, b = blockIdx.y / a.Hq;
+  // grid (B*Hq, query tiles): the longest causal rows are dispatched first
+  const int qt = (int)gridDim.y - 1 - (int)blockIdx.y;
+  const int h = blockIdx.x % a.Hq, b = blockIdx.x / a.Hq;
   const int kvh = h / (a.Hq / a.Hkv);
   const int q0 = qt * 128;
   const int qme = q0 + 32 * w + l32;  // this lane's query
@@ -147,11 +149,11 @@ __global__ __launch_bounds__(fa::NT, 1) void flash_fwd_kernel(FaArgs a) {
   f32x16 o[C::DB];
 #pragma unroll
   for (int i = 0; i < C::DB; ++i) o[i] = fa::zero16();
-  float m = -INFINITY, l = 0.f;
+  float m = -INFINITY, l = 0.f;  // running max (base-2 units) and sum
 
   const int q_last = min(q0 + 127, a.S - 1);
   const int nkt = q_last / fa::BK + 1;
-  const int wave_last = q0 + 32 * w + 31;  // keys beyond this do not matter to the wave
+  const int wave_first = q0 + 32 * w, wave_last = wave_first + 31;
   fa::Tile<D> tk, tv;
   tk.load(Kb, D, 0, a.S, tid);
   tv.load(Vb, D, 0, a.S, tid);
@@ -176,39 +178,50 @@ __global__ __launch_bounds__(fa::NT, 1) void flash_fwd_kernel(FaArgs a) {
         s[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
             fa::frag_rows(sK, sb * 32 + l32, 16 * t + 8 * g, C::KP), qf[t], s[sb], 0, 0, 0);
     }
-    // scale to base 2, causal and length mask, tile max
+    // causal / length mask, only on tiles that cross the wave's diagonal or
+    // the sequence end; then the tile max of the raw scores (the scale c > 0
+    // commutes with the max)
     float mt = -INFINITY;
+    if (k0 + fa::BK - 1 > wave_first || k0 + fa::BK > a.S) {
 #pragma unroll
-    for (int sb = 0; sb < 2; ++sb)
+      for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = k0 + sb * 32 + fa::acc_row(r, g);
-        float x = s[sb][r] * a.c;
-        if (key > qme || key >= a.S) x = -INFINITY;
-        s[sb][r] = x;
-        mt = fmaxf(mt, x);
-      }
+        for (int r = 0; r < 16; ++r) {
+          const int key = k0 + sb * 32 + fa::acc_row(r, g);
+          if (key > qme || key >= a.S) s[sb][r] = -INFINITY;
+          mt = fmaxf(mt, s[sb][r]);
+        }
+    } else {
+#pragma unroll
+      for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[sb][r]);
+    }
     mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-    const float mn = fmaxf(m, mt);
+    const float mn = fmaxf(m, mt * a.c);
     // a lane whose query lies past the sequence end sees only masked keys
     const float msafe = (mn == -INFINITY) ? 0.f : mn;
-    const float alpha = exp2f(m - msafe);
+    const float alpha = __builtin_amdgcn_exp2f(m - msafe);
     float rs = 0.f;
 #pragma unroll
     for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float p = exp2f(s[sb][r] - msafe);
+        const float p = __builtin_amdgcn_exp2f(fmaf(s[sb][r], a.c, -msafe));
         s[sb][r] = p;
         rs += p;
       }
     rs += __shfl_xor(rs, 32, 64);
     l = l * alpha + rs;
+    // alpha == 1 exactly unless the running max moved: skip the rescale when
+    // it moved for no lane of the wave
+    if (__any(mn != m)) {
+#pragma unroll
+      for (int i = 0; i < C::DB; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[i][r] *= alpha;
+    }
     m = mn;
-#pragma unroll
-    for (int i = 0; i < C::DB; ++i)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) o[i][r] *= alpha;
     // O^T += V^T P^T
 #pragma unroll
     for (int sb = 0; sb < 2; ++sb)
@@ -262,7 +275,9 @@ __global__ __launch_bounds__(fa::NT, 1) void flash_bwd_dkdv_kernel(FaArgs a) {
   __shared__ u16 sOt[D * fa::TP];      // dO transposed
   __shared__ float sL[fa::BK], sD[fa::BK];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 5, l32 = lane & 31;
-  const int kt = blockIdx.x, kvh = blockIdx.y % a.Hkv, b = blockIdx.y / a.Hkv;
+  // grid (B*Hkv, key tiles): the low key tiles see the most queries and are
+  // dispatched first
+  const int kt = blockIdx.y, kvh = blockIdx.x % a.Hkv, b = blockIdx.x / a.Hkv;
   const int G = a.Hq / a.Hkv;
   const int k0 = kt * 128;
   const int kme = k0 + 32 * w + l32;  // this lane's key (column of S^T[q][key])
@@ -332,7 +347,7 @@ __global__ __launch_bounds__(fa::NT, 1) void flash_bwd_dkdv_kernel(FaArgs a) {
         for (int r = 0; r < 16; ++r) {
           const int qi = qb * 32 + fa::acc_row(r, g);
           const int q = q0 + qi;
-          float p = exp2f(s[r] * a.c - sL[qi]);
+          float p = __builtin_amdgcn_exp2f(fmaf(s[r], a.c, -sL[qi]));
           if (q < kme || q >= a.S || kme >= a.S) p = 0.f;
           s[r] = p;
           dp[r] = p * (dp[r] - sD[qi]);
@@ -370,13 +385,15 @@ __global__ __launch_bounds__(fa::NT, 1) void flash_bwd_dkdv_kernel(FaArgs a) {
 // ------------------------------------------------------------------- dQ
 
 template <int D>
-__global__ __launch_bounds__(fa::NT, 1) void flash_bwd_dq_kernel(FaArgs a) {
+__global__ __launch_bounds__(fa::NT, 2) void flash_bwd_dq_kernel(FaArgs a) {
   using C = fa::Cfg<D>;
   __shared__ u16 sK[fa::BK * C::KP];
   __shared__ u16 sKt[D * fa::TP];
   __shared__ u16 sV[fa::BK * C::KP];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 5, l32 = lane & 31;
-  const int qt = blockIdx.x, h = blockIdx.y % a.Hq, b = blockIdx.y / a.Hq;
+  // grid (B*Hq, query tiles): the longest causal rows are dispatched first
+  const int qt = (int)gridDim.y - 1 - (int)blockIdx.y;
+  const int h = blockIdx.x % a.Hq, b = blockIdx.x / a.Hq;
   const int kvh = h / (a.Hq / a.Hkv);
   const int q0 = qt * 128;
   const int qme = q0 + 32 * w + l32;
@@ -431,7 +448,7 @@ __global__ __launch_bounds__(fa::NT, 1) void flash_bwd_dq_kernel(FaArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int key = k0 + sb * 32 + fa::acc_row(r, g);
-        float p = exp2f(s[r] * a.c - lse);
+        float p = __builtin_amdgcn_exp2f(fmaf(s[r], a.c, -lse));
         if (key > qme || key >= a.S || qme >= a.S) p = 0.f;
         dp[r] = p * (dp[r] - dsum);
       }
@@ -458,7 +475,7 @@ __global__ __launch_bounds__(fa::NT, 1) void flash_bwd_dq_kernel(FaArgs a) {
 // ------------------------------------------------------------------ launch
 
 catq_status flash_forward(int D, FaArgs& a, hipStream_t stream) {
-  dim3 grid((unsigned)((a.S + 127) / 128), (unsigned)(a.B * a.Hq)), block(fa::NT);
+  dim3 grid((unsigned)(a.B * a.Hq), (unsigned)((a.S + 127) / 128)), block(fa::NT);
   const double f = 2.0 * 2.0 * (double)a.B * a.Hq * (double)a.S * a.S * D * 0.5;
   const double by = 2.0 * (double)a.B * a.S * D * (2.0 * a.Hq + 2.0 * a.Hkv) + 4.0 * a.B * a.Hq * a.S;
   if (D == 128)
@@ -480,7 +497,7 @@ catq_status flash_backward(int D, FaArgs& a, hipStream_t stream) {
     hipLaunchKernelGGL(flash_dsum_kernel<64>, gs, dim3(256), 0, stream, a);
   CATQ_CHECK_LAUNCH("flash dsum");
   const double half = 0.5 * 2.0 * (double)a.B * a.Hq * (double)a.S * a.S * D;
-  dim3 gkv((unsigned)((a.S + 127) / 128), (unsigned)(a.B * a.Hkv)), block(fa::NT);
+  dim3 gkv((unsigned)(a.B * a.Hkv), (unsigned)((a.S + 127) / 128)), block(fa::NT);
   if (D == 128)
     CATQ_TRACED(stream, "flash_bwd_dkdv_kernel<128>", 4.0 * half, 0.0, a.S, a.Hkv, D,
                 hipLaunchKernelGGL(flash_bwd_dkdv_kernel<128>, gkv, block, 0, stream, a));
@@ -488,7 +505,7 @@ catq_status flash_backward(int D, FaArgs& a, hipStream_t stream) {
     CATQ_TRACED(stream, "flash_bwd_dkdv_kernel<64>", 4.0 * half, 0.0, a.S, a.Hkv, D,
                 hipLaunchKernelGGL(flash_bwd_dkdv_kernel<64>, gkv, block, 0, stream, a));
   CATQ_CHECK_LAUNCH("flash dK dV");
-  dim3 gq((unsigned)((a.S + 127) / 128), (unsigned)(a.B * a.Hq));
+  dim3 gq((unsigned)(a.B * a.Hq), (unsigned)((a.S + 127) / 128));
   if (D == 128)
     CATQ_TRACED(stream, "flash_bwd_dq_kernel<128>", 3.0 * half, 0.0, a.S, a.Hq, D,
                 hipLaunchKernelGGL(flash_bwd_dq_kernel<128>, gq, block, 0, stream, a));

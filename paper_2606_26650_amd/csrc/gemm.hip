@@ -18,6 +18,7 @@
 // to the 8 XCDs) and walks tiles in bands of 8 rows for L2 reuse.
 #include <cmath>
 #include <cstdio>
+#include <type_traits>
 
 #include "kernels.h"
 
@@ -324,11 +325,16 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_bf16_kernel(GemmLaunch L) 
 // memory straight into LDS with global_load_lds_dwordx4 (no register
 // staging): each wave instruction fills 1 KB of LDS, lane l landing at
 // base + 16 l.  A tile is ROWS x 64 bf16 = ROWS*8 chunks of 16 B; chunk c of
-// row r sits in slot r*8 + (c ^ (r & 7)), a swizzle chosen by picking which
-// global chunk each lane fetches, so the MFMA fragment reads (8 consecutive
-// rows, same chunk) hit 8 distinct bank groups.  Two LDS stages; the next
-// tile is fetched while the current one is multiplied.  Rows past M or N are
-// clamped to the last row (their results are never stored).
+// row r sits in slot r*8 + (c ^ ((r >> 1) & 7)), a swizzle chosen by picking
+// which global chunk each lane fetches.  A 128-bit LDS read is served 16
+// lanes at a time over 64 four-byte banks (256 B); the MFMA fragment read of
+// 16 consecutive rows at one chunk then covers all 16 bank groups once
+// (rows of equal parity differ in (r >> 1) & 7).  Two LDS stages: the next
+// tile is fetched while the current one is multiplied.  Inside a tile the
+// fragment reads of sub-step kk+1 are interleaved one-for-one with the MFMAs
+// of sub-step kk, and the first reads of the next tile overlap the last
+// sub-step after the barrier.  Rows past M or N are clamped to the last row
+// (their results are never stored).
 
 // 16-byte global -> LDS copy, lane l landing at lds_base + 16*l.  Issued as
 // inline assembly so that the compiler does not add conservative waits before
@@ -353,13 +359,14 @@ __device__ __forceinline__ void wait_vmem() {
 }
 
 template <int BM, int BN, int WGM, int WGN, typename OutT, typename RT, bool HAS_R>
-__global__ __launch_bounds__(WGM* WGN * 64, 1) void gemm_nt_dma_kernel(GemmLaunch L) {
+__global__ __launch_bounds__(WGM* WGN * 64, 1)
+    __attribute__((amdgpu_waves_per_eu(1, (WGM * WGN + 3) / 4))) void gemm_nt_dma_kernel(GemmLaunch L) {
 #if defined(__HIP_DEVICE_COMPILE__)
   constexpr int NW = WGM * WGN;
   constexpr int WTM = BM / WGM, WTN = BN / WGN;
   constexpr int FM = WTM / 32, FN = WTN / 32;
   constexpr int IA = BM / 8 / NW, IB = BN / 8 / NW;
-  static_assert(IA >= 1 && IB >= 1 && FM >= 1 && FN >= 1, "bad tile");
+  static_assert(IA >= 1 && IB >= 1 && FM >= 1 && FN >= 1 && FM * FN >= FM + FN, "bad tile");
   __shared__ uint4 sA[2][BM * 8];
   __shared__ uint4 sB[2][BN * 8];
   const GemmArgs& g = L.g;
@@ -377,20 +384,41 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1) void gemm_nt_dma_kernel(GemmLaunc
   }
   const bf16* A = reinterpret_cast<const bf16*>(g.A);
   const bf16* B = reinterpret_cast<const bf16*>(g.B);
-  // this lane fetches chunk cl of rows (wave*IA + i)*8 + rl
-  const int rl = lane >> 3, cl = (lane & 7) ^ (rl & 7);
-  const int64_t ra0 = m0 + (int64_t)wave * IA * 8 + rl, rb0 = n0 + (int64_t)wave * IB * 8 + rl;
+  // this lane fetches, for tile row (blk*8 + rl), the chunk that belongs in
+  // physical slot (lane & 7) of that row
+  const int rl = lane >> 3;
+  auto src_chunk = [&](int blk) { return (lane & 7) ^ (((blk & 1) << 2) | (rl >> 1)); };
+  const bf16* rowA[IA];
+  const bf16* rowB[IB];
+#pragma unroll
+  for (int i = 0; i < IA; ++i) {
+    const int blk = wave * IA + i;
+    rowA[i] = A + min(m0 + blk * 8 + rl, g.M - 1) * g.lda + src_chunk(blk) * 8;
+  }
+#pragma unroll
+  for (int i = 0; i < IB; ++i) {
+    const int blk = wave * IB + i;
+    rowB[i] = B + min(n0 + blk * 8 + rl, g.N - 1) * g.ldb + src_chunk(blk) * 8;
+  }
   auto issue = [&](int buf, int64_t k0) {
 #pragma unroll
-    for (int i = 0; i < IA; ++i) {
-      const int64_t row = min(ra0 + 8 * i, g.M - 1);
-      dma16(A + row * g.lda + k0 + cl * 8, &sA[buf][(wave * IA + i) * 64]);
-    }
+    for (int i = 0; i < IA; ++i) dma16(rowA[i] + k0, &sA[buf][(wave * IA + i) * 64]);
 #pragma unroll
-    for (int i = 0; i < IB; ++i) {
-      const int64_t row = min(rb0 + 8 * i, g.N - 1);
-      dma16(B + row * g.ldb + k0 + cl * 8, &sB[buf][(wave * IB + i) * 64]);
-    }
+    for (int i = 0; i < IB; ++i) dma16(rowB[i] + k0, &sB[buf][(wave * IB + i) * 64]);
+  };
+  // MFMA fragments: lane reads row (lane & 31) of its 32-row slab, chunk
+  // kk*2 + (lane >> 5); the row's swizzle key is ((lane >> 1) & 7)
+  const int ra = wm * WTM + (lane & 31), rb = wn * WTN + (lane & 31);
+  const int hi = lane >> 5, sw = (lane >> 1) & 7;
+  bf16x8 fa[2][FM], fb[2][FN];
+  auto ldfrag = [&](int buf, int kk, int slot) {
+    const uint4* pa = &sA[buf][ra * 8];
+    const uint4* pb = &sB[buf][rb * 8];
+    const int cs = (kk * 2 + hi) ^ sw;
+#pragma unroll
+    for (int i = 0; i < FM; ++i) fa[slot][i] = *reinterpret_cast<const bf16x8*>(&pa[i * 256 + cs]);
+#pragma unroll
+    for (int j = 0; j < FN; ++j) fb[slot][j] = *reinterpret_cast<const bf16x8*>(&pb[j * 256 + cs]);
   };
   f32x16 acc[FM][FN];
 #pragma unroll
@@ -399,35 +427,50 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1) void gemm_nt_dma_kernel(GemmLaunc
     for (int j = 0; j < FN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-  const int ra = wm * WTM + (lane & 31), rb = wn * WTN + (lane & 31);
-  const int hi = lane >> 5, sw = lane & 7;
+  auto mfmas = [&](int slot) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[slot][i], fb[slot][j], acc[i][j], 0, 0, 0);
+  };
+  // one LDS read after each of the first FM+FN MFMAs, the rest back to back
+  auto interleave = [&]() {
+#pragma unroll
+    for (int q = 0; q < FM + FN; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    if constexpr (FM * FN > FM + FN) __builtin_amdgcn_sched_group_barrier(0x008, FM * FN - (FM + FN), 0);
+  };
+  // one 64-deep tile: sub-steps 0..2 with the next sub-step's reads
+  // interleaved, barrier, then sub-step 3 overlapped with the next tile's
+  // first reads.  MORE is false only for the last tile (no branches inside
+  // the steady-state body, so the interleaving spans it whole).
+  auto tile = [&](int kt, auto more_c) {
+    constexpr bool MORE = decltype(more_c)::value;
+    const int buf = kt & 1;
+    if (MORE) issue(buf ^ 1, kb + (int64_t)(kt + 1) * 64);
+#pragma unroll
+    for (int kk = 0; kk < 3; ++kk) {
+      ldfrag(buf, kk + 1, (kk & 1) ^ 1);
+      mfmas(kk & 1);
+      interleave();
+    }
+    wait_vmem();
+    __syncthreads();
+    if (MORE) ldfrag(buf ^ 1, 0, 0);
+    mfmas(1);
+    if (MORE) interleave();
+  };
   const int nk = (int)((ke - kb) / 64);
   if (nk > 0) {
     issue(0, kb);
     wait_vmem();
     __syncthreads();
-  }
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) issue(buf ^ 1, kb + (int64_t)(kt + 1) * 64);
-    const uint4* pa = &sA[buf][ra * 8];
-    const uint4* pb = &sB[buf][rb * 8];
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      const int cs = (kk * 2 + hi) ^ sw;
-      bf16x8 fa[FM], fb[FN];
-#pragma unroll
-      for (int i = 0; i < FM; ++i) fa[i] = *reinterpret_cast<const bf16x8*>(&pa[i * 256 + cs]);
-#pragma unroll
-      for (int j = 0; j < FN; ++j) fb[j] = *reinterpret_cast<const bf16x8*>(&pb[j * 256 + cs]);
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
-    }
-    wait_vmem();
-    __syncthreads();
+    ldfrag(0, 0, 0);
+    for (int kt = 0; kt < nk - 1; ++kt) tile(kt, std::true_type{});
+    tile(nk - 1, std::false_type{});
   }
   OutT* C = reinterpret_cast<OutT*>(g.C) + c_off;
   const RT* R = HAS_R ? reinterpret_cast<const RT*>(g.R) : nullptr;
