@@ -45,6 +45,35 @@ def parse():
     return ap.parse_args()
 
 
+def counted_traffic(kernel_tag):
+    """HBM bytes per launch of `kernel_tag` as last counted with rocprofv3
+    (FETCH_SIZE and WRITE_SIZE runs, scaled by a plain copy's reading; the
+    summary under profiles/ records the figure with a hash of the kernel
+    sources).  None when no summary covers this kernel or when the sources
+    changed since the count."""
+    import glob
+    import hashlib
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "traffic_*.md"))):
+        fields = {}
+        for line in open(path):
+            if ":" in line and not line.startswith(("|", "#", " ")):
+                k, _, v = line.partition(":")
+                fields[k.strip()] = v.strip()
+        if fields.get("kernel") != kernel_tag or "traffic_bytes_per_launch" not in fields:
+            continue
+        h = hashlib.sha256()
+        try:
+            for src in fields.get("sources", "").split():
+                with open(os.path.join(ROOT, src), "rb") as f:
+                    h.update(f.read())
+        except OSError:
+            return None
+        if h.hexdigest() != fields.get("source_sha256"):
+            return None
+        return float(fields["traffic_bytes_per_launch"])
+    return None
+
+
 def cpu_baseline(cfg, W, xb, row_frac=8):
     """The float64 oracle on a bounded sample of the same step.
     Weight side (LM+ST forward, factor gradients, final ternarise+pack): the
@@ -205,7 +234,7 @@ def main():
             "frac": dom_tflops / PEAK_BF16_TFLOPS,
             "avg_launch_us": 1000.0 * dom["ms"] / dom["n"],
             "flops_per_launch": dom["flops"] / dom["n"],
-            "traffic": None,
+            "traffic": counted_traffic(dom_tag),
         },
         "gemm_tflops_all": all_gemm_flops / (all_gemm_ms * 1e-3) / 1e12,
         "gemm_share_of_step": all_gemm_ms / args.steps / ms_step,
