@@ -319,22 +319,33 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_bf16_kernel(GemmLaunch L) 
   }
 }
 
-// ------------------------------------------------ NT GEMM, direct to LDS
+// ------------------------------------------- dense GEMM, direct to LDS
 //
-// Both operands contiguous along K (K % 64 == 0).  Tiles move from global
-// memory straight into LDS with global_load_lds_dwordx4 (no register
-// staging): each wave instruction fills 1 KB of LDS, lane l landing at
-// base + 16 l.  A tile is ROWS x 64 bf16 = ROWS*8 chunks of 16 B; chunk c of
-// row r sits in slot r*8 + (c ^ ((r >> 1) & 7)), a swizzle chosen by picking
-// which global chunk each lane fetches.  A 128-bit LDS read is served 16
-// lanes at a time over 64 four-byte banks (256 B); the MFMA fragment read of
-// 16 consecutive rows at one chunk then covers all 16 bank groups once
-// (rows of equal parity differ in (r >> 1) & 7).  Two LDS stages: the next
-// tile is fetched while the current one is multiplied.  Inside a tile the
-// fragment reads of sub-step kk+1 are interleaved one-for-one with the MFMAs
-// of sub-step kk, and the first reads of the next tile overlap the last
-// sub-step after the barrier.  Rows past M or N are clamped to the last row
-// (their results are never stored).
+// Tiles move from global memory straight into LDS with global_load_lds_dwordx4
+// (no register staging): each wave instruction fills 1 KB of LDS, lane l
+// landing at base + 16 l.  Each operand is in one of two layouts:
+//
+// * K-contiguous ("nt", stored [rows][K]): a tile is ROWS x 64 bf16 =
+//   ROWS*8 chunks of 16 B; chunk c of row r sits in slot r*8 + (c ^ ((r >> 1)
+//   & 7)).  A 128-bit LDS read is served 16 lanes at a time over 64 four-byte
+//   banks; the MFMA fragment read (16 consecutive rows at one chunk) then
+//   covers all 16 bank groups once.  Rows past the matrix are clamped to the
+//   last row (their results are never stored).
+// * K-major ("km", stored [K][cols]): a tile is 64 rows of k x COLS bf16;
+//   chunk c of row k sits in slot k*(COLS/8) + (c ^ (4*(k & 3))).  Fragments
+//   come from two ds_read_b64_tr_b16 each: within a block of 16 lanes, lane i
+//   receives element e of its 4 values from the lanes 4e..4e+3, column i mod 4
+//   of their 8-byte rows.  When those four lanes point at row k0+e, columns
+//   c0..c0+15, lane i gets column c0+i at rows k0..k0+3: the MFMA operand
+//   (one column, consecutive k) without any transpose pass.  The XOR puts the
+//   4 rows x 64 B that 32 lanes read in one cycle on 4 different 64-byte bank
+//   windows.  COLS must divide the matrix extent.
+//
+// The swizzles are chosen through the global address each lane fetches.  Two
+// LDS stages: the next tile is fetched while the current one is multiplied.
+// Inside a tile the fragment reads of sub-step kk+1 are interleaved with the
+// MFMAs of sub-step kk, and the first reads of the next tile overlap the last
+// sub-step after the barrier.
 
 // 16-byte global -> LDS copy, lane l landing at lds_base + 16*l.  Issued as
 // inline assembly so that the compiler does not add conservative waits before
@@ -358,15 +369,89 @@ __device__ __forceinline__ void wait_vmem() {
 #endif
 }
 
-template <int BM, int BN, int WGM, int WGN, typename OutT, typename RT, bool HAS_R>
+typedef short lds_v4s __attribute__((ext_vector_type(4)));
+
+// K-contiguous operand tile, ROWS x 64, for NW waves.
+template <int ROWS, int NW>
+struct DmaOpNT {
+  static constexpr int NI = ROWS / 8 / NW;  // 1 KB instructions per wave
+  static constexpr int READS = 1;           // LDS reads per fragment
+  static_assert(NI >= 1, "tile too small for the wave count");
+  const bf16* g[NI];
+  __device__ __forceinline__ void init(const bf16* base, int64_t ld, int64_t row0, int64_t rows,
+                                       int wave, int lane) {
+    const int rl = lane >> 3;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int blk = wave * NI + i;
+      const int c = (lane & 7) ^ (((blk & 1) << 2) | (rl >> 1));
+      g[i] = base + min(row0 + blk * 8 + rl, rows - 1) * ld + c * 8;
+    }
+  }
+  __device__ __forceinline__ void issue(uint4* lds, int64_t ld, int64_t k0, int wave) const {
+#pragma unroll
+    for (int i = 0; i < NI; ++i) dma16(g[i] + k0, &lds[(wave * NI + i) * 64]);
+  }
+  // rows row0 .. row0+31 (lane: row row0 + lane%32), k = 16 kk + 8 (lane/32) .. +7
+  __device__ __forceinline__ bf16x8 frag(const uint4* lds, int row0, int kk, int lane) const {
+    const int cs = (kk * 2 + (lane >> 5)) ^ ((lane >> 1) & 7);
+    return *reinterpret_cast<const bf16x8*>(&lds[(row0 + (lane & 31)) * 8 + cs]);
+  }
+};
+
+// K-major operand tile, 64 x COLS, for NW waves.
+template <int COLS, int NW>
+struct DmaOpKM {
+  static constexpr int CPR = COLS / 8;             // 16-byte chunks per row
+  static constexpr int RPI = 64 / CPR;             // rows per 1 KB instruction
+  static constexpr int NI = 64 * CPR / 64 / NW;    // instructions per wave
+  static constexpr int READS = 2;
+  static_assert(NI >= 1 && RPI >= 1, "tile too small for the wave count");
+  const bf16* g[NI];
+  __device__ __forceinline__ void init(const bf16* base, int64_t ld, int64_t col0, int64_t,
+                                       int wave, int lane) {
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int row = (wave * NI + i) * RPI + lane / CPR;
+      const int c = (lane % CPR) ^ (4 * (row & 3));
+      g[i] = base + (int64_t)row * ld + col0 + c * 8;
+    }
+  }
+  __device__ __forceinline__ void issue(uint4* lds, int64_t ld, int64_t k0, int wave) const {
+    const int64_t off = k0 * ld;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) dma16(g[i] + off, &lds[(wave * NI + i) * 64]);
+  }
+  // columns col0 .. col0+31 (lane: column col0 + lane%32), k = 16 kk + 8 (lane/32) .. +7
+  __device__ __forceinline__ bf16x8 frag(const uint4* lds, int col0, int kk, int lane) const {
+    const int blk = lane >> 4, s = lane & 15;
+    const int col = col0 + 16 * (blk & 1) + 4 * (s & 3);
+    u32x4 u;
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const int row = kk * 16 + 8 * (blk >> 1) + 4 * c + (s >> 2);
+      const int chunk = (col >> 3) ^ (4 * (row & 3));
+      const short* p = reinterpret_cast<const short*>(lds) + row * COLS + chunk * 8 + (col & 7);
+      const lds_v4s v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (__attribute__((address_space(3))) lds_v4s*)(p));
+      u[2 * c] = (unsigned)(unsigned short)v[0] | ((unsigned)(unsigned short)v[1] << 16);
+      u[2 * c + 1] = (unsigned)(unsigned short)v[2] | ((unsigned)(unsigned short)v[3] << 16);
+    }
+    return __builtin_bit_cast(bf16x8, u);
+  }
+};
+
+template <int BM, int BN, int WGM, int WGN, bool AKM, bool BKM, typename OutT, typename RT,
+          bool HAS_R>
 __global__ __launch_bounds__(WGM* WGN * 64, 1)
-    __attribute__((amdgpu_waves_per_eu(1, (WGM * WGN + 3) / 4))) void gemm_nt_dma_kernel(GemmLaunch L) {
+    __attribute__((amdgpu_waves_per_eu(1, (WGM * WGN + 3) / 4))) void gemm_dma_kernel(GemmLaunch L) {
 #if defined(__HIP_DEVICE_COMPILE__)
   constexpr int NW = WGM * WGN;
   constexpr int WTM = BM / WGM, WTN = BN / WGN;
   constexpr int FM = WTM / 32, FN = WTN / 32;
-  constexpr int IA = BM / 8 / NW, IB = BN / 8 / NW;
-  static_assert(IA >= 1 && IB >= 1 && FM >= 1 && FN >= 1 && FM * FN >= FM + FN, "bad tile");
+  static_assert(FM >= 1 && FN >= 1 && FM * FN >= FM + FN, "bad tile");
+  using OA = std::conditional_t<AKM, DmaOpKM<BM, NW>, DmaOpNT<BM, NW>>;
+  using OB = std::conditional_t<BKM, DmaOpKM<BN, NW>, DmaOpNT<BN, NW>>;
   __shared__ uint4 sA[2][BM * 8];
   __shared__ uint4 sB[2][BN * 8];
   const GemmArgs& g = L.g;
@@ -382,43 +467,20 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
     ke = min(g.K, kb + L.kchunk);
     c_off = (int64_t)blockIdx.z * L.c_split_stride;
   }
-  const bf16* A = reinterpret_cast<const bf16*>(g.A);
-  const bf16* B = reinterpret_cast<const bf16*>(g.B);
-  // this lane fetches, for tile row (blk*8 + rl), the chunk that belongs in
-  // physical slot (lane & 7) of that row
-  const int rl = lane >> 3;
-  auto src_chunk = [&](int blk) { return (lane & 7) ^ (((blk & 1) << 2) | (rl >> 1)); };
-  const bf16* rowA[IA];
-  const bf16* rowB[IB];
-#pragma unroll
-  for (int i = 0; i < IA; ++i) {
-    const int blk = wave * IA + i;
-    rowA[i] = A + min(m0 + blk * 8 + rl, g.M - 1) * g.lda + src_chunk(blk) * 8;
-  }
-#pragma unroll
-  for (int i = 0; i < IB; ++i) {
-    const int blk = wave * IB + i;
-    rowB[i] = B + min(n0 + blk * 8 + rl, g.N - 1) * g.ldb + src_chunk(blk) * 8;
-  }
-  auto issue = [&](int buf, int64_t k0) {
-#pragma unroll
-    for (int i = 0; i < IA; ++i) dma16(rowA[i] + k0, &sA[buf][(wave * IA + i) * 64]);
-#pragma unroll
-    for (int i = 0; i < IB; ++i) dma16(rowB[i] + k0, &sB[buf][(wave * IB + i) * 64]);
-  };
-  // MFMA fragments: lane reads row (lane & 31) of its 32-row slab, chunk
-  // kk*2 + (lane >> 5); the row's swizzle key is ((lane >> 1) & 7)
-  const int ra = wm * WTM + (lane & 31), rb = wn * WTN + (lane & 31);
-  const int hi = lane >> 5, sw = (lane >> 1) & 7;
+  OA oa;
+  OB ob;
+  oa.init(reinterpret_cast<const bf16*>(g.A), g.lda, m0, g.M, wave, lane);
+  ob.init(reinterpret_cast<const bf16*>(g.B), g.ldb, n0, g.N, wave, lane);
   bf16x8 fa[2][FM], fb[2][FN];
   auto ldfrag = [&](int buf, int kk, int slot) {
-    const uint4* pa = &sA[buf][ra * 8];
-    const uint4* pb = &sB[buf][rb * 8];
-    const int cs = (kk * 2 + hi) ^ sw;
 #pragma unroll
-    for (int i = 0; i < FM; ++i) fa[slot][i] = *reinterpret_cast<const bf16x8*>(&pa[i * 256 + cs]);
+    for (int i = 0; i < FM; ++i) fa[slot][i] = oa.frag(sA[buf], wm * WTM + 32 * i, kk, lane);
 #pragma unroll
-    for (int j = 0; j < FN; ++j) fb[slot][j] = *reinterpret_cast<const bf16x8*>(&pb[j * 256 + cs]);
+    for (int j = 0; j < FN; ++j) fb[slot][j] = ob.frag(sB[buf], wn * WTN + 32 * j, kk, lane);
+  };
+  auto issue = [&](int buf, int64_t k0) {
+    oa.issue(sA[buf], g.lda, k0, wave);
+    ob.issue(sB[buf], g.ldb, k0, wave);
   };
   f32x16 acc[FM][FN];
 #pragma unroll
@@ -434,12 +496,17 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
       for (int j = 0; j < FN; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[slot][i], fb[slot][j], acc[i][j], 0, 0, 0);
   };
-  // one LDS read after each of the first FM+FN MFMAs, the rest back to back
+  // the first FM+FN MFMAs each followed by one fragment's LDS reads, the rest back to back
   auto interleave = [&]() {
 #pragma unroll
-    for (int q = 0; q < FM + FN; ++q) {
+    for (int q = 0; q < FM; ++q) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, OA::READS, 0);
+    }
+#pragma unroll
+    for (int q = 0; q < FN; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, OB::READS, 0);
     }
     if constexpr (FM * FN > FM + FN) __builtin_amdgcn_sched_group_barrier(0x008, FM * FN - (FM + FN), 0);
   };
@@ -603,7 +670,7 @@ static void launch_cfg(GemmLaunch& L, hipStream_t stream) {
                                    grid, block, 0, stream, L));
 }
 
-template <int BM, int BN, int WGM, int WGN, typename OutT, typename RT>
+template <int BM, int BN, int WGM, int WGN, bool AKM, bool BKM, typename OutT, typename RT>
 static void launch_dma(GemmLaunch& L, hipStream_t stream) {
   const GemmArgs& g = L.g;
   L.tiles_m = (int)((g.M + BM - 1) / BM);
@@ -611,38 +678,42 @@ static void launch_dma(GemmLaunch& L, hipStream_t stream) {
   dim3 grid((unsigned)(L.tiles_m * L.tiles_n), 1, (unsigned)L.ksplit);
   dim3 block(WGM * WGN * 64);
   char tag[96];
-  std::snprintf(tag, sizeof(tag), "gemm_nt_dma_kernel<%d, %d, %d, %d, %s, %s, %s>", BM, BN, WGM,
-                WGN, tname<OutT>(), tname<RT>(), g.R ? "true" : "false");
+  std::snprintf(tag, sizeof(tag), "gemm_dma_kernel<%d, %d, %d, %d, %s%s, %s, %s, %s>", BM, BN, WGM,
+                WGN, AKM ? "k" : "n", BKM ? "k" : "t", tname<OutT>(), tname<RT>(),
+                g.R ? "true" : "false");
   double flops, bytes;
   gemm_work(L, (int)sizeof(OutT), flops, bytes);
   if (g.R)
     CATQ_TRACED(stream, tag, flops, bytes, g.M, g.N, g.K,
-                hipLaunchKernelGGL((gemm_nt_dma_kernel<BM, BN, WGM, WGN, OutT, RT, true>), grid,
-                                   block, 0, stream, L));
+                hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WGM, WGN, AKM, BKM, OutT, RT, true>),
+                                   grid, block, 0, stream, L));
   else
     CATQ_TRACED(stream, tag, flops, bytes, g.M, g.N, g.K,
-                hipLaunchKernelGGL((gemm_nt_dma_kernel<BM, BN, WGM, WGN, OutT, RT, false>), grid,
-                                   block, 0, stream, L));
+                hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WGM, WGN, AKM, BKM, OutT, RT, false>),
+                                   grid, block, 0, stream, L));
 }
 
-// The direct-to-LDS NT kernel serves dense bf16 problems whose operands are
-// both K-contiguous with K (per split) a multiple of 64.
-static bool dma_ok(const GemmLaunch& L, int a_t, int b_t) {
+// The direct-to-LDS kernel serves dense bf16 problems with K (per split) a
+// multiple of 64; a K-major operand also needs its tile extent to divide the
+// matrix extent.
+static bool dma_ok(const GemmLaunch& L, int a_t, int b_t, int bm, int bn) {
   const GemmArgs& g = L.g;
-  return a_t == 0 && b_t == 0 && g.group_mode == 0 && g.causal == 0 && g.batch == 1 &&
-         g.K % 64 == 0 && (L.ksplit <= 1 || L.kchunk % 64 == 0) && g.lda % 8 == 0 &&
-         g.ldb % 8 == 0 && aligned16(g.A) && aligned16(g.B);
+  return g.group_mode == 0 && g.causal == 0 && g.batch == 1 && g.K % 64 == 0 &&
+         (L.ksplit <= 1 || L.kchunk % 64 == 0) && g.lda % 8 == 0 && g.ldb % 8 == 0 &&
+         aligned16(g.A) && aligned16(g.B) && (a_t == 0 || g.M % bm == 0) &&
+         (b_t == 0 || g.N % bn == 0);
 }
 
 template <int A_T, int B_T, typename OutT, typename RT>
 static void launch_bf16(GemmLaunch& L, hipStream_t stream) {
   const GemmArgs& g = L.g;
-  if (dma_ok(L, A_T, B_T)) {
-    const int64_t t256 = ((g.M + 255) / 256) * ((g.N + 255) / 256) * L.ksplit;
-    if (g.M >= 256 && g.N >= 256 && t256 >= 256)
-      launch_dma<256, 256, 2, 4, OutT, RT>(L, stream);
-    else
-      launch_dma<128, 128, 2, 2, OutT, RT>(L, stream);
+  const int64_t t256 = ((g.M + 255) / 256) * ((g.N + 255) / 256) * L.ksplit;
+  if (g.M >= 256 && g.N >= 256 && t256 >= 256 && dma_ok(L, A_T, B_T, 256, 256)) {
+    launch_dma<256, 256, 2, 4, A_T == 1, B_T == 1, OutT, RT>(L, stream);
+    return;
+  }
+  if (dma_ok(L, A_T, B_T, 128, 128)) {
+    launch_dma<128, 128, 2, 2, A_T == 1, B_T == 1, OutT, RT>(L, stream);
     return;
   }
   int64_t rows = g.group_mode == 1 ? g.max_rows_per_group : g.M;

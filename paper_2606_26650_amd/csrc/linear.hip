@@ -33,60 +33,6 @@ __global__ __launch_bounds__(256) void sum_splits_kernel(const float* src, int n
   reinterpret_cast<f32x4*>(dst)[i] = acc;
 }
 
-// dst[c][r] = src[r][c] for a bf16 [R][C] matrix; R % 8 == 0, C % 8 == 0.
-// 64x64 tiles through LDS: 16-byte reads along src rows, 16-byte writes along
-// dst rows.
-__global__ __launch_bounds__(256) void transpose_bf16_kernel(const u16* __restrict__ src,
-                                                             int64_t R, int64_t C,
-                                                             u16* __restrict__ dst) {
-  __shared__ u16 t[64][64 + 2];
-  const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
-  for (int q = threadIdx.x; q < 512; q += 256) {
-    const int rr = q >> 3, cc = (q & 7) * 8;
-    const int64_t r = r0 + rr, c = c0 + cc;
-    if (r < R && c < C) {
-      const u32x4 v = *reinterpret_cast<const u32x4*>(src + r * C + c);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        t[rr][cc + 2 * j] = (u16)(v[j] & 0xffffu);
-        t[rr][cc + 2 * j + 1] = (u16)(v[j] >> 16);
-      }
-    }
-  }
-  __syncthreads();
-  for (int q = threadIdx.x; q < 512; q += 256) {
-    const int cc = q >> 3, rr = (q & 7) * 8;
-    const int64_t c = c0 + cc, r = r0 + rr;
-    if (c < C && r < R) {
-      u32x4 v;
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        v[j] = (unsigned)t[rr + 2 * j][cc] | ((unsigned)t[rr + 2 * j + 1][cc] << 16);
-      *reinterpret_cast<u32x4*>(dst + c * R + r) = v;
-    }
-  }
-}
-
-static catq_status transpose_bf16(const void* src, int64_t R, int64_t C, void* dst,
-                                  hipStream_t stream) {
-  dim3 grid((unsigned)((C + 63) / 64), (unsigned)((R + 63) / 64));
-  CATQ_TRACED(stream, "transpose_bf16_kernel", 0.0, 4.0 * (double)R * (double)C, R, C, 0,
-              hipLaunchKernelGGL(transpose_bf16_kernel, grid, dim3(256), 0, stream,
-                                 (const u16*)src, R, C, (u16*)dst));
-  CATQ_CHECK_LAUNCH("transpose");
-  return CATQ_OK;
-}
-
-// The dense bf16 backward runs both contractions on the NT kernel after
-// transposing: dX = dY . (W_fake^T)^T needs the contraction N % 64 == 0, and
-// G = (dY^T) . (X^T)^T needs the token count M % 64 == 0.
-static bool nt_dx(catq_dtype dtype, int32_t E, int64_t N) {
-  return dtype == CATQ_BF16 && E == 1 && N % 64 == 0;
-}
-static bool nt_dw(catq_dtype dtype, int32_t E, int64_t M) {
-  return dtype == CATQ_BF16 && E == 1 && M % 64 == 0;
-}
-
 static catq_status check_linear_common(const void* X, const void* W_fake, catq_dtype dtype,
                                        int64_t M, int64_t N, int64_t K, int32_t n_experts,
                                        const int64_t* row_offsets) {
@@ -114,12 +60,7 @@ extern "C" size_t catq_workspace_size(int32_t which_call, int64_t M, int64_t N, 
     const int ns = splits_used(M, N, K, n_experts);
     size_t g = round_up((size_t)(E * N * K) * 4 * (size_t)ns, 256);
     size_t shared = round_up((size_t)3 * (size_t)(E * N * K / 16) * 4, 256);
-    // room for W_fake^T, dY^T and X^T (dense bf16 backward on the NT kernel)
-    size_t tr = n_experts == 1 ? round_up((size_t)(N * K) * 2, 256) +
-                                     round_up((size_t)(M * N) * 2, 256) +
-                                     round_up((size_t)(M * K) * 2, 256)
-                               : 0;
-    return g + shared + tr;
+    return g + shared;
   }
   if (which_call == CATQ_WS_LOSS) return 4096 * sizeof(double);
   return 0;
@@ -189,41 +130,29 @@ extern "C" catq_status catq_fakeq_linear_bwd(
   float* Gbuf = (dW_fake && ns == 1) ? dW_fake : reinterpret_cast<float*>(workspace);
   float* shared_ws = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) + g_bytes);
 
-  char* tr = reinterpret_cast<char*>(workspace) + g_bytes +
-             round_up((size_t)3 * (size_t)(E * N * K / 16) * 4, 256);
-  void* WfT = tr;
-  void* dYT = tr + round_up((size_t)(N * K) * 2, 256);
-  void* XT = reinterpret_cast<char*>(dYT) + round_up((size_t)(M * N) * 2, 256);
 
-  // dX = dY . W_fake  (W_fake contracted over its rows)
+  // dX = dY . W_fake  (W_fake contracted over its rows: a K-major operand)
   if (dX) {
     GemmArgs a = gemm_args_default();
     a.A = dY;
+    a.B = W_fake;
     a.C = dX;
     a.M = M;
     a.N = K;
     a.K = N;
     a.lda = N;
+    a.ldb = K;
     a.ldc = K;
-    if (nt_dx(dtype, n_experts, N)) {
-      CATQ_TRY(transpose_bf16(W_fake, N, K, WfT, stream));
-      a.B = WfT;
-      a.ldb = N;
-      CATQ_TRY(gemm_run(a, 0, 0, dtype, dtype, stream));
-    } else {
-      a.B = W_fake;
-      a.ldb = K;
-      if (n_experts > 1) {
-        a.group_mode = 1;
-        a.group_off = row_offsets;
-        a.n_groups = n_experts;
-        a.b_gs = N * K;
-        a.max_rows_per_group = (M + n_experts - 1) / n_experts;
-      }
-      CATQ_TRY(gemm_run(a, 0, 1, dtype, dtype, stream));
+    if (n_experts > 1) {
+      a.group_mode = 1;
+      a.group_off = row_offsets;
+      a.n_groups = n_experts;
+      a.b_gs = N * K;
+      a.max_rows_per_group = (M + n_experts - 1) / n_experts;
     }
+    CATQ_TRY(gemm_run(a, 0, 1, dtype, dtype, stream));
   }
-  // G = dY^T . X  (contraction over the tokens), fp32
+  // G = dY^T . X  (contraction over the tokens: both operands K-major), fp32
   {
     GemmArgs a = gemm_args_default();
     a.C = Gbuf;
@@ -241,15 +170,6 @@ extern "C" catq_status catq_fakeq_linear_bwd(
       a.n_groups = n_experts;
       a.c_gs = N * K;
       CATQ_TRY(gemm_run(a, 1, 1, dtype, CATQ_F32, stream));
-    } else if (nt_dw(dtype, n_experts, M)) {
-      CATQ_TRY(transpose_bf16(dY, M, N, dYT, stream));
-      CATQ_TRY(transpose_bf16(X, M, K, XT, stream));
-      a.A = dYT;
-      a.B = XT;
-      a.lda = M;
-      a.ldb = M;
-      CATQ_TRY(gemm_run_split(a, 0, 0, dtype, CATQ_F32, choose_ksplit(M, N, K, 1), N * K,
-                              stream));
     } else {
       a.A = dY;
       a.B = X;
