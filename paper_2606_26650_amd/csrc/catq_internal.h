@@ -36,7 +36,9 @@ void clear_error();
     if (st_ != CATQ_OK) return st_;    \
   } while (0)
 
-inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+__host__ __device__ inline bool aligned16(const void* p) {
+  return (reinterpret_cast<uintptr_t>(p) & 15u) == 0;
+}
 inline bool dtype_ok(int d) { return d == CATQ_F32 || d == CATQ_BF16; }
 inline size_t dtype_size(int d) { return d == CATQ_F32 ? 4 : 2; }
 inline size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }

@@ -319,6 +319,25 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_bf16_kernel(GemmLaunch L) 
   }
 }
 
+// four consecutive values <-> f32x4 (16-byte fp32 or 8-byte bf16 accesses)
+__device__ __forceinline__ f32x4 load4f(const float* p) { return *reinterpret_cast<const f32x4*>(p); }
+__device__ __forceinline__ f32x4 load4f(const bf16* p) {
+  const uint2 u = *reinterpret_cast<const uint2*>(p);
+  f32x4 v;
+  v[0] = __uint_as_float(u.x << 16);
+  v[1] = __uint_as_float(u.x & 0xffff0000u);
+  v[2] = __uint_as_float(u.y << 16);
+  v[3] = __uint_as_float(u.y & 0xffff0000u);
+  return v;
+}
+__device__ __forceinline__ void store4f(float* p, f32x4 v) { *reinterpret_cast<f32x4*>(p) = v; }
+__device__ __forceinline__ void store4f(bf16* p, f32x4 v) {
+  uint2 u;
+  u.x = pack_bf16x2(v[0], v[1]);
+  u.y = pack_bf16x2(v[2], v[3]);
+  *reinterpret_cast<uint2*>(p) = u;
+}
+
 // ------------------------------------------- dense GEMM, direct to LDS
 //
 // Tiles move from global memory straight into LDS with global_load_lds_dwordx4
@@ -541,19 +560,53 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
   }
   OutT* C = reinterpret_cast<OutT*>(g.C) + c_off;
   const RT* R = HAS_R ? reinterpret_cast<const RT*>(g.R) : nullptr;
+  // Epilogue.  Every wave has passed the last barrier, so no LDS read of the
+  // main loop is outstanding and each wave may reuse its own part of the
+  // operand buffers: a 32-row slab of its tile goes to LDS row-major (pitch
+  // WTN+8 floats, so the two row groups one store instruction touches fall on
+  // different banks), then comes back as 4 consecutive columns per lane (16
+  // lanes read one row) for vector global stores and residual loads.
+  const bool vec = g.N % 4 == 0 && g.ldc % 4 == 0 && c_off % 4 == 0 && aligned16(C) &&
+                   (!HAS_R || (g.ldr % 4 == 0 && aligned16(R)));
+  if (vec) {
+    constexpr int EP = WTN + 8;
+    constexpr int LPR = WTN / 4, RPP = 64 / LPR;  // lanes per row, rows per pass
+    static_assert(NW * 32 * EP * 4 <= (int)sizeof(sA) + (int)sizeof(sB), "epilogue staging");
+    float* st = reinterpret_cast<float*>(&sA[0][0]) + wave * (32 * EP);
 #pragma unroll
-  for (int i = 0; i < FM; ++i) {
+    for (int i = 0; i < FM; ++i) {
 #pragma unroll
-    for (int j = 0; j < FN; ++j) {
-      const int64_t n = n0 + wn * WTN + j * 32 + (lane & 31);
-      if (n >= g.N) continue;
+      for (int j = 0; j < FN; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int64_t m = m0 + wm * WTM + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-        if (m >= g.M) continue;
-        float v = acc[i][j][r] * g.alpha;
-        if (HAS_R) v += to_f(R[m * g.ldr + n]);
-        store_out<OutT>(C + m * g.ldc + n, v);
+        for (int r = 0; r < 16; ++r)
+          st[(8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * EP + j * 32 + (lane & 31)] = acc[i][j][r];
+#pragma unroll
+      for (int rr0 = 0; rr0 < 32; rr0 += RPP) {
+        const int rr = rr0 + lane / LPR, cc = (lane % LPR) * 4;
+        const int64_t m = m0 + wm * WTM + i * 32 + rr, n = n0 + wn * WTN + cc;
+        f32x4 v = *reinterpret_cast<const f32x4*>(st + rr * EP + cc);
+        if (m < g.M && n < g.N) {
+          v *= g.alpha;
+          if (HAS_R) v += load4f(R + m * g.ldr + n);
+          store4f(C + m * g.ldc + n, v);
+        }
+      }
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int64_t n = n0 + wn * WTN + j * 32 + (lane & 31);
+        if (n >= g.N) continue;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int64_t m = m0 + wm * WTM + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+          if (m >= g.M) continue;
+          float v = acc[i][j][r] * g.alpha;
+          if (HAS_R) v += to_f(R[m * g.ldr + n]);
+          store_out<OutT>(C + m * g.ldc + n, v);
+        }
       }
     }
   }
