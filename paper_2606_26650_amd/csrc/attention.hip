@@ -160,6 +160,72 @@ __global__ __launch_bounds__(256) void qk_prep_fwd_kernel(const bf16* qkv, int64
   }
 }
 
+// Vectorised q/k preparation for head sizes with half % 8 == 0 and half/8 a
+// power of two: LPH = half/8 lanes per (token, head), each lane owning
+// elements i0..i0+7 of both rotation halves (two 16-byte loads and stores).
+__global__ __launch_bounds__(256) void qk_prep_fwd_vec_kernel(
+    const bf16* qkv, int64_t B, int64_t S, int Hq, int Hkv, int d, int ld, int lph_log2,
+    int qk_norm, float eps, const float* cs, const float* sn, bf16* Qh, bf16* Kh, bf16* Vh,
+    float* rstd) {
+  const int H = Hq + Hkv;
+  const int Hall = Vh ? H + Hkv : H;
+  const int LPH = 1 << lph_log2;
+  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t unit = gid >> lph_log2;
+  const int sub = (int)(gid & (LPH - 1));
+  // whole units only: the grid covers units * LPH threads and LPH divides 64
+  if (unit >= B * S * Hall) return;
+  const int64_t t = unit / Hall;
+  const int h = (int)(unit % Hall);
+  const int64_t b = t / S, s = t % S;
+  const int half = d / 2, i0 = sub * 8;
+  const bf16* src = qkv + t * ld + (int64_t)h * d;
+  if (h >= H) {  // v head: head-major copy
+    bf16* dst = Vh + ((b * Hkv + (h - H)) * S + s) * d;
+    *reinterpret_cast<u32x4*>(dst + i0) = *reinterpret_cast<const u32x4*>(src + i0);
+    *reinterpret_cast<u32x4*>(dst + half + i0) = *reinterpret_cast<const u32x4*>(src + half + i0);
+    return;
+  }
+  float x1[8], x2[8];
+  load8<bf16>(src + i0, x1);
+  load8<bf16>(src + half + i0, x2);
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) ss = fmaf(x1[j], x1[j], fmaf(x2[j], x2[j], ss));
+  float r = 1.0f;
+  if (qk_norm) {
+    for (int m = LPH >> 1; m >= 1; m >>= 1) ss += __shfl_xor(ss, m, 64);
+    r = 1.0f / sqrtf(ss / (float)d + eps);
+  }
+  if (sub == 0) rstd[t * H + h] = r;
+  float c[8], sv[8];
+  load8<float>(cs + s * half + i0, c);
+  load8<float>(sn + s * half + i0, sv);
+  float o1[8], o2[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const float a = x1[j] * r, bb = x2[j] * r;
+    o1[j] = a * c[j] - bb * sv[j];
+    o2[j] = bb * c[j] + a * sv[j];
+  }
+  bf16* dst = h < Hq ? Qh + ((b * Hq + h) * S + s) * d : Kh + ((b * Hkv + (h - Hq)) * S + s) * d;
+  store8<bf16>(dst + i0, o1);
+  store8<bf16>(dst + half + i0, o2);
+}
+
+// log2 of the lanes per head of the vectorised q/k kernels, or 0 when the
+// layout does not allow them (half % 8, half/8 a power of two up to 64,
+// 16-byte aligned rows).
+static int qk_vec_lanes(int64_t d, int64_t ld, const void* qkv) {
+  const int64_t half = d / 2;
+  if (d % 16 != 0 || ld % 8 != 0 || !aligned16(qkv)) return 0;
+  const int64_t lanes = half / 8;
+  if (lanes < 2 || lanes > 64 || (lanes & (lanes - 1)) != 0) return 0;
+  int lg = 0;
+  while ((1 << lg) < lanes) ++lg;
+  return lg;
+}
+
 template <int MAXC>
 __global__ __launch_bounds__(256) void softmax_fwd_kernel(const float* Sc, int64_t S, bf16* P) {
   __shared__ float red[4];
@@ -315,6 +381,89 @@ __global__ __launch_bounds__(256) void qk_prep_bwd_kernel(
   }
 }
 
+// Vectorised backward of the q/k preparation (same lane layout as the forward).
+__global__ __launch_bounds__(256) void qk_prep_bwd_vec_kernel(
+    const bf16* qkv, const float* rstd, const float* cs, const float* sn, const float* dQ,
+    const float* dKp, const float* dVp, int64_t B, int64_t S, int Hq, int Hkv, int d, int ld,
+    int lph_log2, int qk_norm, int per_kv, bf16* dqkv) {
+  const int H = Hq + 2 * Hkv;
+  const int LPH = 1 << lph_log2;
+  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t unit = gid >> lph_log2;
+  const int sub = (int)(gid & (LPH - 1));
+  if (unit >= B * S * H) return;
+  const int64_t t = unit / H;
+  const int h = (int)(unit % H);
+  const int64_t b = t / S, s = t % S;
+  const int half = d / 2, i0 = sub * 8;
+  const int G = Hq / Hkv;
+  bf16* dst = dqkv + t * ld + (int64_t)h * d;
+  float g1[8], g2[8];
+  auto gather = [&](const float* base_of_head0, int64_t head_stride, int nh) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) g1[j] = g2[j] = 0.f;
+    for (int q = 0; q < nh; ++q) {
+      const float* src = base_of_head0 + q * head_stride;
+      float a[8], c[8];
+      load8<float>(src + i0, a);
+      load8<float>(src + half + i0, c);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        g1[j] += a[j];
+        g2[j] += c[j];
+      }
+    }
+  };
+  if (h >= Hq + Hkv) {  // v heads: sum over the q heads of the group
+    const int kv = h - Hq - Hkv;
+    if (per_kv)
+      gather(dVp + ((b * Hkv + kv) * S + s) * d, 0, 1);
+    else
+      gather(dVp + ((b * Hq + kv * G) * S + s) * d, S * d, G);
+    store8<bf16>(dst + i0, g1);
+    store8<bf16>(dst + half + i0, g2);
+    return;
+  }
+  if (h < Hq)
+    gather(dQ + ((b * Hq + h) * S + s) * d, 0, 1);
+  else if (per_kv)
+    gather(dKp + ((b * Hkv + (h - Hq)) * S + s) * d, 0, 1);
+  else
+    gather(dKp + ((b * Hq + (h - Hq) * G) * S + s) * d, S * d, G);
+  {
+    // undo the rotation (transpose of the forward rotation)
+    float c[8], sv[8];
+    load8<float>(cs + s * half + i0, c);
+    load8<float>(sn + s * half + i0, sv);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float a1 = g1[j] * c[j] + g2[j] * sv[j];
+      const float a2 = -g1[j] * sv[j] + g2[j] * c[j];
+      g1[j] = a1;
+      g2[j] = a2;
+    }
+  }
+  if (qk_norm) {
+    const bf16* src = qkv + t * ld + (int64_t)h * d;
+    const float r = rstd[t * (Hq + Hkv) + h];
+    float x1[8], x2[8];
+    load8<bf16>(src + i0, x1);
+    load8<bf16>(src + half + i0, x2);
+    float dot = 0.f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) dot = fmaf(x1[j], g1[j], fmaf(x2[j], g2[j], dot));
+    for (int m = LPH >> 1; m >= 1; m >>= 1) dot += __shfl_xor(dot, m, 64);
+    const float coef = r * r * r * dot / (float)d;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      g1[j] = r * g1[j] - x1[j] * coef;
+      g2[j] = r * g2[j] - x2[j] * coef;
+    }
+  }
+  store8<bf16>(dst + i0, g1);
+  store8<bf16>(dst + half + i0, g2);
+}
+
 static int row_chunks(int64_t S) {
   const int c = (int)((S + 255) / 256);
   return c <= 2 ? 2 : (c <= 4 ? 4 : (c <= 8 ? 8 : (c <= 16 ? 16 : 32)));
@@ -382,9 +531,17 @@ extern "C" catq_status catq_aux_attention_fwd(const catq_attn_desc* a, const voi
                      stream, L.S, (int)L.d, std::log2((double)a->rope_theta), cs, sn);
   CATQ_CHECK_LAUNCH("rope table");
   const int64_t nw = L.B * L.S * (L.Hq + L.Hkv + (L.flash ? L.Hkv : 0));
-  hipLaunchKernelGGL(qk_prep_fwd_kernel, dim3((unsigned)((nw + 3) / 4)), dim3(256), 0, stream,
-                     (const bf16*)qkv, L.B, L.S, (int)L.Hq, (int)L.Hkv, (int)L.d, (int)L.ld,
-                     a->qk_norm, a->eps, cs, sn, Qh, Kh, Vh, rstd);
+  const int lph = qk_vec_lanes(L.d, L.ld, qkv);
+  if (lph > 0) {
+    const int64_t nt = nw << lph;
+    hipLaunchKernelGGL(qk_prep_fwd_vec_kernel, dim3((unsigned)((nt + 255) / 256)), dim3(256), 0,
+                       stream, (const bf16*)qkv, L.B, L.S, (int)L.Hq, (int)L.Hkv, (int)L.d,
+                       (int)L.ld, lph, a->qk_norm, a->eps, cs, sn, Qh, Kh, Vh, rstd);
+  } else {
+    hipLaunchKernelGGL(qk_prep_fwd_kernel, dim3((unsigned)((nw + 3) / 4)), dim3(256), 0, stream,
+                       (const bf16*)qkv, L.B, L.S, (int)L.Hq, (int)L.Hkv, (int)L.d, (int)L.ld,
+                       a->qk_norm, a->eps, cs, sn, Qh, Kh, Vh, rstd);
+  }
   CATQ_CHECK_LAUNCH("qk prep");
   if (L.flash) {
     FaArgs f;
@@ -587,10 +744,20 @@ extern "C" catq_status catq_aux_attention_bwd(const catq_attn_desc* a, const voi
   }
   }
   const int64_t nw = L.B * L.S * (L.Hq + 2 * L.Hkv);
-  hipLaunchKernelGGL(qk_prep_bwd_kernel, dim3((unsigned)((nw + 3) / 4)), dim3(256), 0, stream,
-                     (const bf16*)qkv, rstd, cs, sn, (const float*)dQ, (const float*)dKp,
-                     (const float*)dVp, L.B, L.S, (int)L.Hq, (int)L.Hkv, (int)L.d, (int)L.ld,
-                     a->qk_norm, L.flash ? 1 : 0, (bf16*)dqkv);
+  const int lph = qk_vec_lanes(L.d, L.ld, qkv) > 0 && aligned16(dqkv) ? qk_vec_lanes(L.d, L.ld, qkv)
+                                                                     : 0;
+  if (lph > 0) {
+    const int64_t nt = nw << lph;
+    hipLaunchKernelGGL(qk_prep_bwd_vec_kernel, dim3((unsigned)((nt + 255) / 256)), dim3(256), 0,
+                       stream, (const bf16*)qkv, rstd, cs, sn, (const float*)dQ,
+                       (const float*)dKp, (const float*)dVp, L.B, L.S, (int)L.Hq, (int)L.Hkv,
+                       (int)L.d, (int)L.ld, lph, a->qk_norm, L.flash ? 1 : 0, (bf16*)dqkv);
+  } else {
+    hipLaunchKernelGGL(qk_prep_bwd_kernel, dim3((unsigned)((nw + 3) / 4)), dim3(256), 0, stream,
+                       (const bf16*)qkv, rstd, cs, sn, (const float*)dQ, (const float*)dKp,
+                       (const float*)dVp, L.B, L.S, (int)L.Hq, (int)L.Hkv, (int)L.d, (int)L.ld,
+                       a->qk_norm, L.flash ? 1 : 0, (bf16*)dqkv);
+  }
   CATQ_CHECK_LAUNCH("qk prep bwd");
   return CATQ_OK;
 }

@@ -245,20 +245,27 @@ __global__ __launch_bounds__(fa::NT, 2) void flash_fwd_kernel(FaArgs a) {
   }
 }
 
-// D = rowsum(dO * O) per (batch, q head, query); one wavefront per row pair.
+// D = rowsum(dO * O) per (batch, q head, query): D/8 lanes per row, each
+// lane one 16-byte chunk of O and of dO.
 template <int D>
 __global__ __launch_bounds__(256) void flash_dsum_kernel(FaArgs a) {
-  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);  // (b*S + q)*Hq + h
-  const int lane = threadIdx.x & 63;
-  if (row >= (int64_t)a.B * a.S * a.Hq) return;
+  constexpr int LPR = D / 8;
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t row = gid / LPR;  // (b*S + q)*Hq + h
+  const int sub = (int)(gid % LPR);
+  if (row >= (int64_t)a.B * a.S * a.Hq) return;  // whole rows: LPR divides 64
   const int h = (int)(row % a.Hq);
   const int64_t t = row / a.Hq;  // token b*S + q
-  const bf16* o = a.O + t * (int64_t)(a.Hq * D) + (int64_t)h * D;
-  const bf16* d = a.dO + t * (int64_t)(a.Hq * D) + (int64_t)h * D;
+  const int64_t off = t * (int64_t)(a.Hq * D) + (int64_t)h * D + 8 * sub;
+  float o[8], d[8];
+  load8<bf16>(a.O + off, o);
+  load8<bf16>(a.dO + off, d);
   float acc = 0.f;
-  for (int i = lane; i < D; i += 64) acc = fmaf(to_f(o[i]), to_f(d[i]), acc);
-  acc = wave_sum(acc);
-  if (lane == 0) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) acc = fmaf(o[j], d[j], acc);
+#pragma unroll
+  for (int m = LPR >> 1; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, 64);
+  if (sub == 0) {
     const int64_t b = t / a.S, q = t % a.S;
     a.Dsum[(b * a.Hq + h) * a.S + q] = acc;
   }
@@ -490,7 +497,7 @@ catq_status flash_forward(int D, FaArgs& a, hipStream_t stream) {
 
 catq_status flash_backward(int D, FaArgs& a, hipStream_t stream) {
   const int64_t rows = (int64_t)a.B * a.S * a.Hq;
-  dim3 gs((unsigned)((rows + 3) / 4));
+  dim3 gs((unsigned)((rows * (D / 8) + 255) / 256));
   if (D == 128)
     hipLaunchKernelGGL(flash_dsum_kernel<128>, gs, dim3(256), 0, stream, a);
   else

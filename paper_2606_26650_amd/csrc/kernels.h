@@ -22,11 +22,12 @@ void trace_end(int slot, hipStream_t stream);
 // Factor gradients from G = dL/dW_fake (fp32, [n_rows][d_in]) for one weight
 // matrix (or all experts' matrices stacked along rows).  `ws_shared` holds
 // 3*n_groups floats and is used only when some factor stride is 0.
-catq_status launch_factor_grads(const float* G, const void* W, catq_dtype w_dtype, int64_t n_rows,
-                                int64_t d_in, const float* stats, const float* d_mu,
-                                const float* d_alpha, const float* d_delta,
-                                const catq_lmst_params* p, float* g_mu, float* g_alpha,
-                                float* g_delta, float* ws_shared, hipStream_t stream);
+catq_status launch_factor_grads(const float* G, int nsplit, int64_t split_stride, float* G_out,
+                                const void* W, catq_dtype w_dtype, int64_t n_rows, int64_t d_in,
+                                const float* stats, const float* d_mu, const float* d_alpha,
+                                const float* d_delta, const catq_lmst_params* p, float* g_mu,
+                                float* g_alpha, float* g_delta, float* ws_shared,
+                                hipStream_t stream);
 
 catq_status check_lmst_params(const catq_lmst_params* p, int64_t d_in);
 

@@ -23,16 +23,6 @@ static int splits_used(int64_t M, int64_t N, int64_t K, int32_t n_experts) {
   return gemm_split_count(a, choose_ksplit(M, N, K, n_experts));
 }
 
-// Sum of split-K partials (fp32) into dst.
-__global__ __launch_bounds__(256) void sum_splits_kernel(const float* src, int nsplit,
-                                                         int64_t stride, int64_t n4, float* dst) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n4) return;
-  f32x4 acc = reinterpret_cast<const f32x4*>(src)[i];
-  for (int s = 1; s < nsplit; ++s) acc += reinterpret_cast<const f32x4*>(src + s * stride)[i];
-  reinterpret_cast<f32x4*>(dst)[i] = acc;
-}
-
 static catq_status check_linear_common(const void* X, const void* W_fake, catq_dtype dtype,
                                        int64_t M, int64_t N, int64_t K, int32_t n_experts,
                                        const int64_t* row_offsets) {
@@ -179,17 +169,9 @@ extern "C" catq_status catq_fakeq_linear_bwd(
                               stream));
     }
   }
-  const float* Gsum = Gbuf;
-  if (ns > 1) {
-    // fold the split partials once; the factor kernel then reads one G
-    float* dst = dW_fake ? dW_fake : Gbuf;
-    const int64_t n4 = N * K / 4;
-    CATQ_TRACED(stream, "sum_splits_kernel", 0.0, 4.0 * (double)(N * K) * (ns + 1), N, K, ns,
-                hipLaunchKernelGGL(sum_splits_kernel, dim3((unsigned)((n4 + 255) / 256)),
-                                   dim3(256), 0, stream, Gbuf, ns, N * K, n4, dst));
-    CATQ_CHECK_LAUNCH("split-K reduction");
-    Gsum = dst;
-  }
-  return launch_factor_grads(Gsum, W, w_dtype, E * N, K, stats, d_mu, d_alpha, d_delta, p, g_d_mu,
-                             g_d_alpha, g_d_delta, shared_ws, stream);
+  // the factor kernel folds the split partials itself (and writes the summed
+  // G when dW_fake is requested)
+  float* G_out = (dW_fake && ns > 1) ? dW_fake : nullptr;
+  return launch_factor_grads(Gbuf, ns, N * K, G_out, W, w_dtype, E * N, K, stats, d_mu, d_alpha,
+                             d_delta, p, g_d_mu, g_d_alpha, g_d_delta, shared_ws, stream);
 }

@@ -291,7 +291,10 @@ static int ilog2(int v) {
 // -------------------------------------------------------------- lmst bwd
 
 struct BwdArgs {
-  const float* G;
+  const float* G;     // nsplit partial sums, split i at G + i*split_stride
+  int64_t split_stride;
+  int32_t nsplit;
+  float* G_out;       // optional: the summed G
   const void* W;
   const float* stats;
   const float* dmu;
@@ -318,6 +321,15 @@ __global__ __launch_bounds__(256) void lmst_bwd_kernel(BwdArgs a) {
   float w[8], G[8];
   load8<WT>(reinterpret_cast<const WT*>(a.W) + o * 8, w);
   load8<float>(a.G + o * 8, G);
+  // split-K partials of G, folded in split order (the same order and
+  // rounding as a separate reduction pass)
+  for (int sp = 1; sp < a.nsplit; ++sp) {
+    float t[8];
+    load8<float>(a.G + sp * a.split_stride + o * 8, t);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) G[j] += t[j];
+  }
+  if (a.G_out) store8<float>(a.G_out + o * 8, G);
   const float mu0 = a.stats[2 * grp], alpha0 = a.stats[2 * grp + 1];
   GroupScalars gs = group_scalars(mu0, alpha0, a.dmu[grp * a.s[0]], a.dal[grp * a.s[1]],
                                   a.dde[grp * a.s[2]], a.delta0);
@@ -382,13 +394,17 @@ __global__ __launch_bounds__(1024) void shared_factor_reduce(const float* ws, in
   if (threadIdx.x == 0) out[0] = (float)red[0];
 }
 
-catq_status launch_factor_grads(const float* G, const void* W, catq_dtype w_dtype, int64_t n_rows,
+catq_status launch_factor_grads(const float* G, int nsplit, int64_t split_stride, float* G_out,
+                                const void* W, catq_dtype w_dtype, int64_t n_rows,
                                 int64_t d_in, const float* stats, const float* d_mu,
                                 const float* d_alpha, const float* d_delta,
                                 const catq_lmst_params* p, float* g_mu, float* g_alpha,
                                 float* g_delta, float* ws_shared, hipStream_t stream) {
   BwdArgs a;
   a.G = G;
+  a.nsplit = nsplit > 1 ? nsplit : 1;
+  a.split_stride = split_stride;
+  a.G_out = G_out;
   a.W = W;
   a.stats = stats;
   a.dmu = d_mu;
@@ -410,7 +426,8 @@ catq_status launch_factor_grads(const float* G, const void* W, catq_dtype w_dtyp
   a.st = make_st(s_use > 0 ? s_use : 1.0);
   dim3 grid((unsigned)((a.n_oct + 255) / 256));
   const double nn = (double)n, ngd = (double)a.n_groups;
-  const double bytes = nn * (4.0 + (w_dtype == CATQ_BF16 ? 2.0 : 4.0)) + ngd * (8.0 + 12.0 + 12.0);
+  const double bytes = nn * (4.0 * a.nsplit + (G_out ? 4.0 : 0.0) + (w_dtype == CATQ_BF16 ? 2.0 : 4.0)) +
+                       ngd * (8.0 + 12.0 + 12.0);
   if (w_dtype == CATQ_BF16)
     CATQ_TRACED(stream, "lmst_bwd_kernel<__bf16>", 0.0, bytes, n, 0, 0,
                 hipLaunchKernelGGL((lmst_bwd_kernel<bf16>), grid, dim3(256), 0, stream, a));
