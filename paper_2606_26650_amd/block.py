@@ -44,14 +44,23 @@ def empty(shape, dtype=torch.bfloat16):
 class QLinear:
     """A weight under learnable modulation: W frozen, three factor arrays
     (per group), cached group statistics, fake weight and factor gradients.
-    ``W`` is [rows][d_in] (experts stacked along rows)."""
+    ``W`` is [rows][d_in] (experts stacked along rows).  ``store`` supplies
+    views of a block arena for every per-weight array (else they are
+    allocated here)."""
 
-    def __init__(self, W: torch.Tensor, d_out: int, d_in: int, g: int = 128, n_experts: int = 1):
+    FIELDS = ("d_mu", "d_alpha", "d_delta", "stats", "W_fake", "g_mu", "g_alpha", "g_delta")
+
+    def __init__(self, W: torch.Tensor, d_out: int, d_in: int, g: int = 128, n_experts: int = 1,
+                 store: dict | None = None):
         self.W = W
         self.d_out, self.d_in, self.E = d_out, d_in, n_experts
         self.g = g
         ng = W.numel() // g
         self.n_groups = ng
+        if store is not None:
+            for k in self.FIELDS:
+                setattr(self, k, store[k])
+            return
         self.d_mu = torch.zeros(ng, dtype=torch.float32, device=DEV)
         self.d_alpha = torch.ones(ng, dtype=torch.float32, device=DEV)
         self.d_delta = torch.ones(ng, dtype=torch.float32, device=DEV)
@@ -72,6 +81,55 @@ class QLinear:
                                 stats_mode, W_fake=wf, codes=codes, alpha_out=alpha_out)
 
 
+class WeightArena:
+    """Every weight of a block in one flat allocation, with its factors,
+    statistics, fake weight and gradients alongside.  Groups never straddle
+    rows, so the flat view of the concatenated row-major matrices holds
+    exactly the per-matrix groups in order: LM+ST, the hard finalize and the
+    packing can each run as one launch over the whole block."""
+
+    def __init__(self, mats: list, g: int):
+        # mats: (name, tensor [rows][d_in], d_out, d_in, n_experts)
+        self.g = g
+        total = sum(t.numel() for _, t, *_ in mats)
+        self.P, self.n_groups = total, total // g
+        self.W = torch.empty(total, dtype=torch.bfloat16, device=DEV)
+        self.W_fake = torch.empty_like(self.W)
+        ng = self.n_groups
+        self.d_mu = torch.zeros(ng, dtype=torch.float32, device=DEV)
+        self.d_alpha = torch.ones(ng, dtype=torch.float32, device=DEV)
+        self.d_delta = torch.ones(ng, dtype=torch.float32, device=DEV)
+        self.stats = torch.zeros(ng, 2, dtype=torch.float32, device=DEV)
+        self.g_mu = torch.zeros(ng, dtype=torch.float32, device=DEV)
+        self.g_alpha = torch.zeros_like(self.g_mu)
+        self.g_delta = torch.zeros_like(self.g_mu)
+        self.spans = {}
+        self.lin = {}
+        o = 0
+        for name, t, d_out, d_in, E in mats:
+            n = t.numel()
+            shape = (n // d_in, d_in)
+            self.W[o:o + n].copy_(t.reshape(-1))
+            go, gn = o // g, n // g
+            store = {"W_fake": self.W_fake[o:o + n].view(shape),
+                     "stats": self.stats[go:go + gn]}
+            for k in ("d_mu", "d_alpha", "d_delta", "g_mu", "g_alpha", "g_delta"):
+                store[k] = getattr(self, k)[go:go + gn]
+            self.lin[name] = QLinear(self.W[o:o + n].view(shape), d_out, d_in, g, E, store)
+            self.spans[name] = (o, n, shape)
+            o += n
+
+    def flat(self, t):
+        """[P] (or [P]-sized) tensor seen as [P/g][g] for the flat calls."""
+        return t.view(self.P // self.g, self.g) if t is not None else None
+
+    def modulate(self, p, stats_mode, W_fake="self", codes=None, alpha_out=None):
+        wf = self.W_fake if W_fake == "self" else W_fake
+        catq_modulate_ternarize(self.flat(self.W), self.d_mu, self.d_alpha, self.d_delta, p,
+                                self.stats, stats_mode, W_fake=self.flat(wf),
+                                codes=self.flat(codes), alpha_out=alpha_out)
+
+
 class DenseBlock:
     """Pre-norm decoder block (RMSNorm, fused q|k|v, QK-norm, RoPE, causal GQA
     attention, o, residual, RMSNorm, fused gate|up, SwiGLU, down, residual)."""
@@ -84,13 +142,14 @@ class DenseBlock:
         self.M = c.batch * c.seq
         self.g = g
         dev_w = {k: bf16_tensor(v) for k, v in weights.items()}
-        self.lin = {
-            "qkv": QLinear(torch.cat([dev_w["Wq"], dev_w["Wk"], dev_w["Wv"]], 0).contiguous(),
-                           self.Nqkv, h, g),
-            "o": QLinear(dev_w["Wo"], h, c.n_q * hd, g),
-            "gu": QLinear(torch.cat([dev_w["Wg"], dev_w["Wu"]], 0).contiguous(), 2 * c.ffn, h, g),
-            "d": QLinear(dev_w["Wd"], h, c.ffn, g),
-        }
+        self.arena = WeightArena([
+            ("qkv", torch.cat([dev_w["Wq"], dev_w["Wk"], dev_w["Wv"]], 0), self.Nqkv, h, 1),
+            ("o", dev_w["Wo"], h, c.n_q * hd, 1),
+            ("gu", torch.cat([dev_w["Wg"], dev_w["Wu"]], 0), 2 * c.ffn, h, 1),
+            ("d", dev_w["Wd"], h, c.ffn, 1),
+        ], g)
+        self.lin = self.arena.lin
+        del dev_w
         M = self.M
         self.desc = attn_desc(c.batch, c.seq, c.n_q, c.n_kv, hd, c.qk_norm, c.rope_theta)
         # activations
@@ -127,9 +186,14 @@ class DenseBlock:
         return lmst_params(self.g, mode, 0.5, s if s else 1.0, s_bwd, strides)
 
     def modulate_all(self, p, recompute_stats=False):
+        """LM+ST of every weight: one launch over the arena (per-linear calls
+        when a factor is shared, since a shared factor is per matrix)."""
         mode_stats = 0 if (recompute_stats or not self.stats_ready) else 1
-        for L in self.lin.values():
-            L.modulate(p, mode_stats)
+        if all(st == 1 for st in p.factor_stride):
+            self.arena.modulate(p, mode_stats)
+        else:
+            for L in self.lin.values():
+                L.modulate(p, mode_stats)
         self.stats_ready = True
 
     # ---------------------------------------------------------------- forward
@@ -193,22 +257,27 @@ class DenseBlock:
         return self.loss
 
     def finalize_buffers(self):
-        out = {}
-        for name, L in self.lin.items():
-            out[name] = dict(codes=torch.empty(L.W.shape, dtype=torch.int8, device=DEV),
-                             alpha=torch.empty(L.n_groups, dtype=torch.float32, device=DEV),
-                             packed=torch.empty((L.W.shape[0], L.W.shape[1] // 4),
-                                                dtype=torch.uint8, device=DEV))
+        """Flat codes / scales / packed bytes for the whole arena, with
+        per-linear views."""
+        A = self.arena
+        flat = dict(codes=torch.empty(A.P, dtype=torch.int8, device=DEV),
+                    alpha=torch.empty(A.n_groups, dtype=torch.float32, device=DEV),
+                    packed=torch.empty(A.P // 4, dtype=torch.uint8, device=DEV))
+        out = {"_flat": flat}
+        for name, (o, n, shape) in A.spans.items():
+            out[name] = dict(codes=flat["codes"][o:o + n].view(shape),
+                             alpha=flat["alpha"][o // A.g:(o + n) // A.g],
+                             packed=flat["packed"][o // 4:(o + n) // 4].view(shape[0], shape[1] // 4))
         return out
 
     def finalize(self, bufs):
-        """Hard codes (Eq. 2), group scales and 2-bit packing of every weight."""
+        """Hard codes (Eq. 2), group scales and 2-bit packing of every weight
+        (one launch each over the arena)."""
         p = self.params(HARD)
-        for name, L in self.lin.items():
-            b = bufs[name]
-            L.modulate(p, 1 if self.stats_ready else 0, codes=b["codes"], alpha_out=b["alpha"],
-                       W_fake=None)
-            catq_pack_ternary(b["codes"], b["packed"])
+        A, f = self.arena, bufs["_flat"]
+        A.modulate(p, 1 if self.stats_ready else 0, W_fake=None, codes=f["codes"],
+                   alpha_out=f["alpha"])
+        catq_pack_ternary(A.flat(f["codes"]), f["packed"].view(A.P // A.g, A.g // 4))
         self.stats_ready = True
         return bufs
 
@@ -244,14 +313,15 @@ class MoEBlock:
         self.g = g
         dev_w = {k: bf16_tensor(v) for k, v in weights.items()}
         E, F = c.n_experts, c.expert_ffn
-        self.lin = {
-            "qkv": QLinear(torch.cat([dev_w["Wq"], dev_w["Wk"], dev_w["Wv"]], 0).contiguous(),
-                           self.Nqkv, h, g),
-            "o": QLinear(dev_w["Wo"], h, c.n_q * hd, g),
+        self.arena = WeightArena([
+            ("qkv", torch.cat([dev_w["Wq"], dev_w["Wk"], dev_w["Wv"]], 0), self.Nqkv, h, 1),
+            ("o", dev_w["Wo"], h, c.n_q * hd, 1),
             # experts' gate|up fused per expert: [E][2F][h]
-            "gu": QLinear(torch.cat([dev_w["Wg"], dev_w["Wu"]], 1).contiguous(), 2 * F, h, g, E),
-            "d": QLinear(dev_w["Wd"].contiguous(), h, F, g, E),
-        }
+            ("gu", torch.cat([dev_w["Wg"], dev_w["Wu"]], 1), 2 * F, h, E),
+            ("d", dev_w["Wd"], h, F, E),
+        ], g)
+        self.lin = self.arena.lin
+        del dev_w
         M, R = self.M, self.R
         self.logits = torch.from_numpy(np.ascontiguousarray(logits)).to(DEV)
         self.desc = attn_desc(c.batch, c.seq, c.n_q, c.n_kv, hd, c.qk_norm, c.rope_theta)

@@ -527,16 +527,22 @@ extern "C" catq_status catq_aux_attention_fwd(const catq_attn_desc* a, const voi
   float* sn = reinterpret_cast<float*>(sv + L.o_sin);
   float* Sc = reinterpret_cast<float*>(sv + L.o_sc);
   const int64_t half = L.d / 2;
-  hipLaunchKernelGGL(rope_table_kernel, dim3((unsigned)((L.S * half + 255) / 256)), dim3(256), 0,
-                     stream, L.S, (int)L.d, std::log2((double)a->rope_theta), cs, sn);
+  CATQ_TRACED(stream, "rope_table_kernel", 0.0, 8.0 * (double)L.S * half, L.S, half, 0,
+              hipLaunchKernelGGL(rope_table_kernel, dim3((unsigned)((L.S * half + 255) / 256)),
+                                 dim3(256), 0, stream, L.S, (int)L.d,
+                                 std::log2((double)a->rope_theta), cs, sn));
   CATQ_CHECK_LAUNCH("rope table");
   const int64_t nw = L.B * L.S * (L.Hq + L.Hkv + (L.flash ? L.Hkv : 0));
   const int lph = qk_vec_lanes(L.d, L.ld, qkv);
+  // q, k (and v for the fused path) read once as bf16 and written once, plus the rope tables
+  const double qby = 4.0 * (double)nw * L.d + 8.0 * (double)L.B * L.S * L.Hq * (L.d / 2);
   if (lph > 0) {
     const int64_t nt = nw << lph;
-    hipLaunchKernelGGL(qk_prep_fwd_vec_kernel, dim3((unsigned)((nt + 255) / 256)), dim3(256), 0,
-                       stream, (const bf16*)qkv, L.B, L.S, (int)L.Hq, (int)L.Hkv, (int)L.d,
-                       (int)L.ld, lph, a->qk_norm, a->eps, cs, sn, Qh, Kh, Vh, rstd);
+    CATQ_TRACED(stream, "qk_prep_fwd_vec_kernel", 0.0, qby, nw, L.d, 0,
+                hipLaunchKernelGGL(qk_prep_fwd_vec_kernel, dim3((unsigned)((nt + 255) / 256)),
+                                   dim3(256), 0, stream, (const bf16*)qkv, L.B, L.S, (int)L.Hq,
+                                   (int)L.Hkv, (int)L.d, (int)L.ld, lph, a->qk_norm, a->eps, cs,
+                                   sn, Qh, Kh, Vh, rstd));
   } else {
     hipLaunchKernelGGL(qk_prep_fwd_kernel, dim3((unsigned)((nw + 3) / 4)), dim3(256), 0, stream,
                        (const bf16*)qkv, L.B, L.S, (int)L.Hq, (int)L.Hkv, (int)L.d, (int)L.ld,
@@ -748,10 +754,14 @@ extern "C" catq_status catq_aux_attention_bwd(const catq_attn_desc* a, const voi
                                                                      : 0;
   if (lph > 0) {
     const int64_t nt = nw << lph;
-    hipLaunchKernelGGL(qk_prep_bwd_vec_kernel, dim3((unsigned)((nt + 255) / 256)), dim3(256), 0,
-                       stream, (const bf16*)qkv, rstd, cs, sn, (const float*)dQ,
-                       (const float*)dKp, (const float*)dVp, L.B, L.S, (int)L.Hq, (int)L.Hkv,
-                       (int)L.d, (int)L.ld, lph, a->qk_norm, L.flash ? 1 : 0, (bf16*)dqkv);
+    // fp32 gradients in (q, k, v per kv head), bf16 q|k|v in, bf16 dq|dk|dv out
+    const double bby = (double)nw * L.d * (4.0 + 2.0 + 2.0);
+    CATQ_TRACED(stream, "qk_prep_bwd_vec_kernel", 0.0, bby, nw, L.d, 0,
+                hipLaunchKernelGGL(qk_prep_bwd_vec_kernel, dim3((unsigned)((nt + 255) / 256)),
+                                   dim3(256), 0, stream, (const bf16*)qkv, rstd, cs, sn,
+                                   (const float*)dQ, (const float*)dKp, (const float*)dVp, L.B,
+                                   L.S, (int)L.Hq, (int)L.Hkv, (int)L.d, (int)L.ld, lph,
+                                   a->qk_norm, L.flash ? 1 : 0, (bf16*)dqkv));
   } else {
     hipLaunchKernelGGL(qk_prep_bwd_kernel, dim3((unsigned)((nw + 3) / 4)), dim3(256), 0, stream,
                        (const bf16*)qkv, rstd, cs, sn, (const float*)dQ, (const float*)dKp,

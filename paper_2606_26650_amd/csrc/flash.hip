@@ -498,10 +498,13 @@ catq_status flash_forward(int D, FaArgs& a, hipStream_t stream) {
 catq_status flash_backward(int D, FaArgs& a, hipStream_t stream) {
   const int64_t rows = (int64_t)a.B * a.S * a.Hq;
   dim3 gs((unsigned)((rows * (D / 8) + 255) / 256));
+  const double dby = (double)rows * (4.0 * D + 4.0);
   if (D == 128)
-    hipLaunchKernelGGL(flash_dsum_kernel<128>, gs, dim3(256), 0, stream, a);
+    CATQ_TRACED(stream, "flash_dsum_kernel<128>", 0.0, dby, rows, D, 0,
+                hipLaunchKernelGGL(flash_dsum_kernel<128>, gs, dim3(256), 0, stream, a));
   else
-    hipLaunchKernelGGL(flash_dsum_kernel<64>, gs, dim3(256), 0, stream, a);
+    CATQ_TRACED(stream, "flash_dsum_kernel<64>", 0.0, dby, rows, D, 0,
+                hipLaunchKernelGGL(flash_dsum_kernel<64>, gs, dim3(256), 0, stream, a));
   CATQ_CHECK_LAUNCH("flash dsum");
   const double half = 0.5 * 2.0 * (double)a.B * a.Hq * (double)a.S * a.S * D;
   dim3 gkv((unsigned)(a.B * a.Hkv), (unsigned)((a.S + 127) / 128)), block(fa::NT);

@@ -308,12 +308,16 @@ extern "C" catq_status catq_aux_rmsnorm_fwd(const void* x, catq_dtype x_dtype, i
   CATQ_REQUIRE(rows > 0 && n > 0 && n % 8 == 0, CATQ_ERR_SHAPE, "need rows > 0 and n a multiple of 8");
   CATQ_REQUIRE(eps >= 0, CATQ_ERR_VALUE, "eps must be >= 0");
   CATQ_REQUIRE(aligned16(x) && aligned16(y), CATQ_ERR_ALIGN, "misaligned");
+  const double xs = x_dtype == CATQ_BF16 ? 2.0 : 4.0;
+  const double by = (double)rows * n * (xs + 2.0) + (rstd ? 4.0 * rows : 0.0);
   if (x_dtype == CATQ_BF16)
-    hipLaunchKernelGGL(rmsnorm_fwd_kernel<bf16>, dim3((unsigned)rows), dim3(256), 0, stream,
-                       (const bf16*)x, n, eps, (bf16*)y, rstd);
+    CATQ_TRACED(stream, "rmsnorm_fwd_kernel<__bf16>", 0.0, by, rows, n, 0,
+                hipLaunchKernelGGL(rmsnorm_fwd_kernel<bf16>, dim3((unsigned)rows), dim3(256), 0,
+                                   stream, (const bf16*)x, n, eps, (bf16*)y, rstd));
   else
-    hipLaunchKernelGGL(rmsnorm_fwd_kernel<float>, dim3((unsigned)rows), dim3(256), 0, stream,
-                       (const float*)x, n, eps, (bf16*)y, rstd);
+    CATQ_TRACED(stream, "rmsnorm_fwd_kernel<float>", 0.0, by, rows, n, 0,
+                hipLaunchKernelGGL(rmsnorm_fwd_kernel<float>, dim3((unsigned)rows), dim3(256), 0,
+                                   stream, (const float*)x, n, eps, (bf16*)y, rstd));
   CATQ_CHECK_LAUNCH("rmsnorm fwd");
   return CATQ_OK;
 }
@@ -327,12 +331,18 @@ extern "C" catq_status catq_aux_rmsnorm_bwd(const void* x, catq_dtype x_dtype, c
   CATQ_REQUIRE(rows > 0 && n > 0 && n % 8 == 0, CATQ_ERR_SHAPE, "need rows > 0 and n a multiple of 8");
   CATQ_REQUIRE(aligned16(x) && aligned16(dy) && aligned16(dres) && aligned16(dx), CATQ_ERR_ALIGN,
                "misaligned");
+  const double xs = x_dtype == CATQ_BF16 ? 2.0 : 4.0;
+  const double by = (double)rows * n * (xs + 2.0 + (dres ? 2.0 : 0.0) + 2.0) + 4.0 * rows;
   if (x_dtype == CATQ_BF16)
-    hipLaunchKernelGGL(rmsnorm_bwd_kernel<bf16>, dim3((unsigned)rows), dim3(256), 0, stream,
-                       (const bf16*)x, rstd, (const bf16*)dy, (const bf16*)dres, n, (bf16*)dx);
+    CATQ_TRACED(stream, "rmsnorm_bwd_kernel<__bf16>", 0.0, by, rows, n, 0,
+                hipLaunchKernelGGL(rmsnorm_bwd_kernel<bf16>, dim3((unsigned)rows), dim3(256), 0,
+                                   stream, (const bf16*)x, rstd, (const bf16*)dy,
+                                   (const bf16*)dres, n, (bf16*)dx));
   else
-    hipLaunchKernelGGL(rmsnorm_bwd_kernel<float>, dim3((unsigned)rows), dim3(256), 0, stream,
-                       (const float*)x, rstd, (const bf16*)dy, (const bf16*)dres, n, (bf16*)dx);
+    CATQ_TRACED(stream, "rmsnorm_bwd_kernel<float>", 0.0, by, rows, n, 0,
+                hipLaunchKernelGGL(rmsnorm_bwd_kernel<float>, dim3((unsigned)rows), dim3(256), 0,
+                                   stream, (const float*)x, rstd, (const bf16*)dy,
+                                   (const bf16*)dres, n, (bf16*)dx));
   CATQ_CHECK_LAUNCH("rmsnorm bwd");
   return CATQ_OK;
 }
@@ -344,8 +354,9 @@ extern "C" catq_status catq_aux_swiglu_fwd(const void* gu, int64_t rows, int64_t
   CATQ_REQUIRE(rows > 0 && F > 0 && F % 8 == 0, CATQ_ERR_SHAPE, "need rows > 0 and F a multiple of 8");
   CATQ_REQUIRE(aligned16(gu) && aligned16(a), CATQ_ERR_ALIGN, "misaligned");
   const int64_t n = rows * (F / 8);
-  hipLaunchKernelGGL(swiglu_fwd_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream,
-                     (const bf16*)gu, rows, F, (bf16*)a);
+  CATQ_TRACED(stream, "swiglu_fwd_kernel", 0.0, 6.0 * (double)rows * F, rows, F, 0,
+              hipLaunchKernelGGL(swiglu_fwd_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256),
+                                 0, stream, (const bf16*)gu, rows, F, (bf16*)a));
   CATQ_CHECK_LAUNCH("swiglu fwd");
   return CATQ_OK;
 }
@@ -357,8 +368,9 @@ extern "C" catq_status catq_aux_swiglu_bwd(const void* gu, const void* da, int64
   CATQ_REQUIRE(rows > 0 && F > 0 && F % 8 == 0, CATQ_ERR_SHAPE, "need rows > 0 and F a multiple of 8");
   CATQ_REQUIRE(aligned16(gu) && aligned16(da) && aligned16(dgu), CATQ_ERR_ALIGN, "misaligned");
   const int64_t n = rows * (F / 8);
-  hipLaunchKernelGGL(swiglu_bwd_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream,
-                     (const bf16*)gu, (const bf16*)da, rows, F, (bf16*)dgu);
+  CATQ_TRACED(stream, "swiglu_bwd_kernel", 0.0, 10.0 * (double)rows * F, rows, F, 0,
+              hipLaunchKernelGGL(swiglu_bwd_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256),
+                                 0, stream, (const bf16*)gu, (const bf16*)da, rows, F, (bf16*)dgu));
   CATQ_CHECK_LAUNCH("swiglu bwd");
   return CATQ_OK;
 }

@@ -163,64 +163,92 @@ __device__ __forceinline__ void group_stats_lanes(const float (&w)[8], int L, fl
   alpha0 = (float)(t * (double)inv_g);
 }
 
+// Each thread handles FWD_U octets spaced by the grid size, so a wave keeps
+// FWD_U 16-byte loads of W (and their group scalars) in flight before it
+// computes anything; consecutive lanes still take consecutive octets, and a
+// group's lanes are always valid or invalid together (the grid size is a
+// multiple of 256 and n_oct a multiple of the lanes per group).
+constexpr int FWD_U = 4;
+
 template <typename WT, typename OT, int MODE, bool STATS>
 __global__ __launch_bounds__(256) void lmst_fwd_kernel(FwdArgs a) {
-  const int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (o >= a.n_oct) return;  // whole groups only: n_oct is a multiple of L
+  const int64_t T = (int64_t)gridDim.x * blockDim.x;
+  const int64_t o0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int L = 1 << a.lg;
-  const int64_t grp = o >> a.lg;
-  const int lane_in_g = (int)(o & (L - 1));
-  float w[8];
-  load8<WT>(reinterpret_cast<const WT*>(a.W) + o * 8, w);
-
-  float mu0, alpha0;
-  if (STATS) {
-    group_stats_lanes<WT>(w, L, a.inv_g, mu0, alpha0);
-    if (lane_in_g == 0) {
-      a.stats[2 * grp] = mu0;
-      a.stats[2 * grp + 1] = alpha0;
-    }
-  } else {
-    mu0 = a.stats[2 * grp];
-    alpha0 = a.stats[2 * grp + 1];
+  const int lane_in_g = (int)(o0 & (L - 1));
+  float w[FWD_U][8];
+  float st[FWD_U][2], fc[FWD_U][3];
+#pragma unroll
+  for (int u = 0; u < FWD_U; ++u) {
+    const int64_t o = o0 + u * T;
+    if (o < a.n_oct) load8<WT>(reinterpret_cast<const WT*>(a.W) + o * 8, w[u]);
   }
-  GroupScalars gs = group_scalars(mu0, alpha0, a.dmu[grp * a.s0], a.dal[grp * a.s1],
-                                  a.dde[grp * a.s2], a.delta0);
-  if (a.alpha_out && lane_in_g == 0) a.alpha_out[grp] = gs.alpha;
-
-  float out[8];
-  if (MODE == CATQ_IDENTITY) {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) out[j] = w[j];
-  } else if (MODE == CATQ_SOFT) {
-    const float inv_a = 1.0f / gs.alpha_div;
-    const float ED = one_minus_exp_neg(gs.delta * a.st.s4, gs.delta * a.st.s4l);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      float xs = (w[j] - gs.mu) * inv_a;
-      out[j] = gs.alpha * transition_f(xs, gs.delta, ED, a.st);
+  for (int u = 0; u < FWD_U; ++u) {
+    const int64_t o = o0 + u * T;
+    if (o >= a.n_oct) continue;
+    const int64_t grp = o >> a.lg;
+    if (!STATS) {
+      st[u][0] = a.stats[2 * grp];
+      st[u][1] = a.stats[2 * grp + 1];
     }
-  } else {  // HARD
-    const double theta = (double)gs.delta * (double)gs.alpha_div;
-    unsigned int lo = 0, hi = 0;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      float c = hard_code(w[j], gs.mu, theta);
-      out[j] = gs.alpha * c;
-      unsigned int byte = (unsigned int)(int)c & 0xffu;
-      if (j < 4)
-        lo |= byte << (8 * j);
-      else
-        hi |= byte << (8 * (j - 4));
-    }
-    if (a.codes) {
-      uint2 v;
-      v.x = lo;
-      v.y = hi;
-      *reinterpret_cast<uint2*>(a.codes + o * 8) = v;
-    }
+    fc[u][0] = a.dmu[grp * a.s0];
+    fc[u][1] = a.dal[grp * a.s1];
+    fc[u][2] = a.dde[grp * a.s2];
   }
-  if (a.Wf) store8<OT>(reinterpret_cast<OT*>(a.Wf) + o * 8, out);
+#pragma unroll
+  for (int u = 0; u < FWD_U; ++u) {
+    const int64_t o = o0 + u * T;
+    if (o >= a.n_oct) continue;  // whole groups: all lanes of a group agree
+    const int64_t grp = o >> a.lg;
+    float mu0, alpha0;
+    if (STATS) {
+      group_stats_lanes<WT>(w[u], L, a.inv_g, mu0, alpha0);
+      if (lane_in_g == 0) {
+        a.stats[2 * grp] = mu0;
+        a.stats[2 * grp + 1] = alpha0;
+      }
+    } else {
+      mu0 = st[u][0];
+      alpha0 = st[u][1];
+    }
+    GroupScalars gs = group_scalars(mu0, alpha0, fc[u][0], fc[u][1], fc[u][2], a.delta0);
+    if (a.alpha_out && lane_in_g == 0) a.alpha_out[grp] = gs.alpha;
+
+    float out[8];
+    if (MODE == CATQ_IDENTITY) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) out[j] = w[u][j];
+    } else if (MODE == CATQ_SOFT) {
+      const float inv_a = 1.0f / gs.alpha_div;
+      const float ED = one_minus_exp_neg(gs.delta * a.st.s4, gs.delta * a.st.s4l);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        float xs = (w[u][j] - gs.mu) * inv_a;
+        out[j] = gs.alpha * transition_f(xs, gs.delta, ED, a.st);
+      }
+    } else {  // HARD
+      const double theta = (double)gs.delta * (double)gs.alpha_div;
+      unsigned int lo = 0, hi = 0;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        float c = hard_code(w[u][j], gs.mu, theta);
+        out[j] = gs.alpha * c;
+        unsigned int byte = (unsigned int)(int)c & 0xffu;
+        if (j < 4)
+          lo |= byte << (8 * j);
+        else
+          hi |= byte << (8 * (j - 4));
+      }
+      if (a.codes) {
+        uint2 v;
+        v.x = lo;
+        v.y = hi;
+        *reinterpret_cast<uint2*>(a.codes + o * 8) = v;
+      }
+    }
+    if (a.Wf) store8<OT>(reinterpret_cast<OT*>(a.Wf) + o * 8, out);
+  }
 }
 
 template <typename T>
@@ -547,7 +575,7 @@ extern "C" catq_status catq_modulate_ternarize(const void* W, catq_dtype w_dtype
   a.delta0 = p->delta0;
   a.st = make_st(p->mode == CATQ_SOFT ? (double)p->s : 1.0);
   a.inv_g = 1.0f / (float)p->group_size;
-  dim3 grid((unsigned)((a.n_oct + 255) / 256));
+  dim3 grid((unsigned)((a.n_oct + 256 * FWD_U - 1) / (256 * FWD_U)));
   const bool st = stats_mode == 0;
   if (w_dtype == CATQ_BF16 && wf_dtype == CATQ_BF16)
     launch_fwd<bf16, bf16>(a, p->mode, st, grid, stream);

@@ -77,18 +77,21 @@ extern "C" catq_status catq_block_recon_loss(const void* Y_q, const void* Y_fp, 
   const float scale = (float)(2.0 / (double)n);
   double* partial = reinterpret_cast<double*>(workspace);
   dim3 g(nb), b(LOSS_THREADS);
-  if (dtype == CATQ_BF16 && dy_dtype == CATQ_BF16)
-    hipLaunchKernelGGL((loss_partial_kernel<bf16, bf16>), g, b, 0, stream, (const bf16*)Y_q,
-                       (const bf16*)Y_fp, n8, scale, (bf16*)dY_q, partial);
-  else if (dtype == CATQ_BF16)
-    hipLaunchKernelGGL((loss_partial_kernel<bf16, float>), g, b, 0, stream, (const bf16*)Y_q,
-                       (const bf16*)Y_fp, n8, scale, (float*)dY_q, partial);
-  else if (dy_dtype == CATQ_BF16)
-    hipLaunchKernelGGL((loss_partial_kernel<float, bf16>), g, b, 0, stream, (const float*)Y_q,
-                       (const float*)Y_fp, n8, scale, (bf16*)dY_q, partial);
-  else
-    hipLaunchKernelGGL((loss_partial_kernel<float, float>), g, b, 0, stream, (const float*)Y_q,
-                       (const float*)Y_fp, n8, scale, (float*)dY_q, partial);
+  const double lby = (double)n * ((dtype == CATQ_BF16 ? 4.0 : 8.0) + (dY_q ? (dy_dtype == CATQ_BF16 ? 2.0 : 4.0) : 0.0));
+  CATQ_TRACED(stream, "loss_partial_kernel", 0.0, lby, n, 0, 0, {
+    if (dtype == CATQ_BF16 && dy_dtype == CATQ_BF16)
+      hipLaunchKernelGGL((loss_partial_kernel<bf16, bf16>), g, b, 0, stream, (const bf16*)Y_q,
+                         (const bf16*)Y_fp, n8, scale, (bf16*)dY_q, partial);
+    else if (dtype == CATQ_BF16)
+      hipLaunchKernelGGL((loss_partial_kernel<bf16, float>), g, b, 0, stream, (const bf16*)Y_q,
+                         (const bf16*)Y_fp, n8, scale, (float*)dY_q, partial);
+    else if (dy_dtype == CATQ_BF16)
+      hipLaunchKernelGGL((loss_partial_kernel<float, bf16>), g, b, 0, stream, (const float*)Y_q,
+                         (const float*)Y_fp, n8, scale, (bf16*)dY_q, partial);
+    else
+      hipLaunchKernelGGL((loss_partial_kernel<float, float>), g, b, 0, stream, (const float*)Y_q,
+                         (const float*)Y_fp, n8, scale, (float*)dY_q, partial);
+  });
   CATQ_CHECK_LAUNCH("recon loss");
   hipLaunchKernelGGL(loss_final_kernel, dim3(1), dim3(LOSS_THREADS), 0, stream, partial, nb,
                      1.0 / (double)n, loss);
