@@ -201,6 +201,51 @@ def block_backward(dy, cache, W, cfg):
     return dx, ga
 
 
+# ------------------------------------------------- selected tokens only
+
+def attn_forward_rows(x, W, cfg, rows):
+    """h1 = x + o_proj(attention) for the token rows ``rows`` only (Eq. 7's
+    window forward restricted to some outputs).  Causal attention lets token
+    s of sample b see tokens 0..s of b alone, so the keys and values of that
+    prefix and the query of token s are all it needs; every step is the one
+    attn_forward takes, applied to that subset (checked against it)."""
+    S = cfg.seq
+    Hq, Hkv, hd = cfg.n_q, cfg.n_kv, cfg.head_dim
+    G = Hq // Hkv
+    cos, sin = rope_tables(S, hd, cfg.rope_theta)
+    rows = [int(t) for t in rows]
+    out = np.empty((len(rows), x.shape[1]))
+    by_sample = {}
+    for i, t in enumerate(rows):
+        by_sample.setdefault(t // S, []).append(i)
+    for b, idxs in by_sample.items():
+        last = max(rows[i] % S for i in idxs)
+        xn, _ = rmsnorm(x[b * S: b * S + last + 1])
+        k = (xn @ W["Wk"].T).reshape(1, last + 1, Hkv, hd)
+        v = (xn @ W["Wv"].T).reshape(1, last + 1, Hkv, hd)
+        if cfg.qk_norm:
+            k, _ = rmsnorm(k)
+        kr = rope(k, cos[:last + 1], sin[:last + 1])
+        for i in idxs:
+            s = rows[i] % S
+            q = (xn[s:s + 1] @ W["Wq"].T).reshape(1, 1, Hq, hd)
+            if cfg.qk_norm:
+                q, _ = rmsnorm(q)
+            qr = rope(q, cos[s:s + 1], sin[s:s + 1])
+            o = np.empty((Hq, hd))
+            for h in range(Hq):
+                sc = kr[0, :s + 1, h // G, :] @ qr[0, 0, h, :] / np.sqrt(hd)
+                e = np.exp(sc - sc.max())
+                o[h] = (e / e.sum()) @ v[0, :s + 1, h // G, :]
+            out[i] = x[rows[i]] + o.reshape(-1) @ W["Wo"].T
+    return out
+
+
+def block_forward_rows(x, W, cfg, rows):
+    """Block output for the token rows ``rows`` (the MLP half is per token)."""
+    return mlp_forward(attn_forward_rows(x, W, cfg, rows), W)[0]
+
+
 def recon_loss(y_q, y_fp):
     """Eq. 7 as a mean over all n outputs: L = (1/n) sum (y_q - y_fp)^2 and
     dL/dy_q = 2 (y_q - y_fp)/n."""

@@ -73,3 +73,25 @@ def moe_block_backward(dy, cache, W, cfg):
     dx, ga = block.attn_backward(dh1, ca, W, cfg)
     ga.update(gm)
     return dx, ga
+
+
+def moe_block_forward_rows(x, W, expert, logits, cfg, rows):
+    """Block output for the token rows ``rows``.  ``W`` holds the attention
+    weights; ``expert(e)`` returns expert e's (gate, up, down) weights, so
+    only the experts these tokens are routed to are ever formed.  Per token
+    this is moe_mlp_forward's arithmetic (checked against it)."""
+    rows = [int(t) for t in rows]
+    h1 = block.attn_forward_rows(x, W, cfg, rows)
+    idx, wts = route(np.asarray(logits)[rows], cfg.top_k)
+    xn2, _ = block.rmsnorm(h1)
+    y = h1.copy()
+    cache = {}
+    for i in range(len(rows)):
+        for j in range(cfg.top_k):
+            e = int(idx[i, j])
+            if e not in cache:
+                cache[e] = expert(e)
+            Wg, Wu, Wd = cache[e]
+            a = block.silu(xn2[i] @ Wg.T) * (xn2[i] @ Wu.T)
+            y[i] += wts[i, j] * (a @ Wd.T)
+    return y

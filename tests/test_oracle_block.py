@@ -258,3 +258,34 @@ def test_single_linear_schedule_and_steps():
         dm, da, dd = r["factors"]
         assert np.all(np.abs(dm) < 1) and np.all(da > 0) and np.all(dd > 0)
         assert np.isfinite(r["loss"])
+
+
+# ------------------------------------------------------ selected-token forward
+
+@pytest.mark.parametrize("cfg", [SMALL, sg.small_dense(batch=3, seq=7, hidden=128, n_q=4, n_kv=1,
+                                                       head_dim=32, ffn=192, qk_norm=False)])
+def test_block_forward_rows_matches_full(cfg):
+    """The selected-token forward (used for full-size sampled checks) equals
+    rows of the whole-block forward and of the torch mirror, including the
+    first and last token of every sample."""
+    W, x = _weights(cfg), _x(cfg)
+    S = cfg.seq
+    rows = sorted({0, S - 1, S, 2 * S - 1, cfg.tokens - 1, 3, S + 2})
+    got = block.block_forward_rows(x, W, cfg, rows)
+    ref = block.block_forward(x, W, cfg)[0][rows]
+    np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-12)
+    tw = {k: torch.from_numpy(v) for k, v in W.items()}
+    mirror = _t_block(torch.from_numpy(x), tw, cfg).numpy()[rows]
+    np.testing.assert_allclose(got, mirror, rtol=1e-10, atol=1e-12)
+
+
+def test_moe_forward_rows_matches_full():
+    cfg = sg.small_moe(batch=2, seq=12, hidden=128, n_q=4, n_kv=2, head_dim=32, n_experts=6,
+                       top_k=2, expert_ffn=64, router_bias_std=1.0)
+    W, x = _weights(cfg), _x(cfg)
+    logits = sg.router_logits(cfg, 0)
+    rows = [0, 5, 11, 12, 23]
+    got = moe.moe_block_forward_rows(x, W, lambda e: (W["Wg"][e], W["Wu"][e], W["Wd"][e]),
+                                     logits, cfg, rows)
+    ref = moe.moe_block_forward(x, W, logits, cfg)[0][rows]
+    np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-12)
