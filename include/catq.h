@@ -170,6 +170,11 @@ catq_status catq_fakeq_linear_fwd(const void* X, const void* W_fake, catq_dtype 
  *   workspace       device scratch of at least
  *                   catq_workspace_size(CATQ_WS_LINEAR_BWD, M, N, K, n_experts)
  *                   bytes (may be NULL when that size is 0)
+ * With g_d_mu, g_d_alpha, g_d_delta and dW_fake all NULL only dX is computed
+ * (W, w_dtype, stats, the factors, p and the workspace are then not read);
+ * a caller can so run the input-gradient half and the weight-gradient half
+ * (dX NULL) on two streams.  Otherwise all three gradient outputs are
+ * required.
  * Requires N % 8 == 0 and K % 8 == 0.
  */
 catq_status catq_fakeq_linear_bwd(const void* dY, const void* X, const void* W_fake,

@@ -180,6 +180,14 @@ class DenseBlock:
                                    device=DEV)
         self.loss = torch.zeros(1, dtype=torch.float32, device=DEV)
         self.stats_ready = False
+        self.side = None
+
+    def side_stream(self):
+        """Second stream (default priority) for the weight-gradient halves and
+        the hard finalize, which then overlap the input-gradient chain."""
+        if self.side is None:
+            self.side = torch.cuda.Stream(device=DEV)
+        return self.side
 
     # ------------------------------------------------------------------ LM+ST
     def params(self, mode, s=15.0, s_bwd=30.0, strides=(1, 1, 1)):
@@ -225,16 +233,33 @@ class DenseBlock:
         return self.forward(x, out)
 
     # --------------------------------------------------------------- backward
-    def backward(self, x, p):
+    def backward(self, x, p, overlap=True):
+        """Backward to the block input and to every factor.  With ``overlap``
+        each linear's weight-gradient half (G = dY^T X and the factor
+        gradients) runs on the side stream as soon as dY is ready, while the
+        main stream carries on with dX and the glue; the main stream waits
+        for the side stream at the end."""
         c, M = self.cfg, self.M
         h = c.hidden
         ws = self.lin_ws
+        main = torch.cuda.current_stream()
+        side = self.side_stream() if overlap else None
 
         def lbwd(name, dY, X, dX):
             L = self.lin[name]
+            if side is None:
+                catq_fakeq_linear_bwd(dY, X, L.W_fake, M, L.d_out, L.d_in, L.W, L.stats, L.d_mu,
+                                      L.d_alpha, L.d_delta, p, L.g_mu, L.g_alpha, L.g_delta, ws,
+                                      dX=dX)
+                return
+            ready = torch.cuda.Event()
+            ready.record(main)
+            side.wait_event(ready)
+            with torch.cuda.stream(side):
+                catq_fakeq_linear_bwd(dY, X, L.W_fake, M, L.d_out, L.d_in, L.W, L.stats, L.d_mu,
+                                      L.d_alpha, L.d_delta, p, L.g_mu, L.g_alpha, L.g_delta, ws)
             catq_fakeq_linear_bwd(dY, X, L.W_fake, M, L.d_out, L.d_in, L.W, L.stats, L.d_mu,
-                                  L.d_alpha, L.d_delta, p, L.g_mu, L.g_alpha, L.g_delta, ws,
-                                  dX=dX)
+                                  L.d_alpha, L.d_delta, p, None, None, None, None, dX=dX)
 
         lbwd("d", self.dy, self.a, self.da)
         catq_aux_swiglu_bwd(self.gu, self.da, self.dgu)
@@ -245,15 +270,31 @@ class DenseBlock:
                                self.attn_ws)
         lbwd("qkv", self.dqkv, self.xn1, self.dxn1)
         catq_aux_rmsnorm_bwd(x, self.rstd1, self.dxn1, self.dx, dres=self.dh1)
+        if side is not None:
+            main.wait_stream(side)
 
     # ------------------------------------------------------------------- step
-    def step(self, x, y_fp, mode=SOFT, s=15.0, s_bwd=30.0, recompute_stats=False):
-        """LM+ST -> forward -> loss -> backward.  Loss stays on the device."""
+    def step(self, x, y_fp, mode=SOFT, s=15.0, s_bwd=30.0, recompute_stats=False, overlap=True,
+             finalize=None):
+        """LM+ST -> forward -> loss -> backward.  Loss stays on the device.
+        ``finalize`` (buffers from finalize_buffers) also runs the hard
+        ternarisation + packing, on the side stream once LM+ST has the
+        statistics (it reads only W, the statistics and the factors)."""
         p = self.params(mode, s, s_bwd)
         self.modulate_all(p, recompute_stats)
+        if finalize is not None:
+            main = torch.cuda.current_stream()
+            side = self.side_stream() if overlap else main
+            ready = torch.cuda.Event()
+            ready.record(main)
+            side.wait_event(ready)
+            with torch.cuda.stream(side):
+                self.finalize(finalize)
         self.forward(x)
         catq_block_recon_loss(self.y, y_fp, self.loss, self.dy, self.loss_ws)
-        self.backward(x, p)
+        self.backward(x, p, overlap)
+        if finalize is not None and overlap:
+            torch.cuda.current_stream().wait_stream(self.side_stream())
         return self.loss
 
     def finalize_buffers(self):
@@ -364,8 +405,10 @@ class MoEBlock:
                                    device=DEV)
         self.loss = torch.zeros(1, dtype=torch.float32, device=DEV)
         self.stats_ready = False
+        self.side = None
 
     params = DenseBlock.params
+    side_stream = DenseBlock.side_stream
     modulate_all = DenseBlock.modulate_all
     new_output = DenseBlock.new_output
     finalize_buffers = DenseBlock.finalize_buffers
@@ -399,16 +442,31 @@ class MoEBlock:
         self.modulate_all(self.params(IDENTITY))
         return self.forward(x, out)
 
-    def backward(self, x, p):
+    def backward(self, x, p, overlap=True):
+        """As DenseBlock.backward, with the routed-expert MLP half."""
         c, M, R = self.cfg, self.M, self.R
         h, E, F, k = c.hidden, c.n_experts, c.expert_ffn, c.top_k
         ws = self.lin_ws
+        main = torch.cuda.current_stream()
+        side = self.side_stream() if overlap else None
 
         def lbwd(name, dY, X, dX, rows, E_=1, offs=None):
             L = self.lin[name]
+            if side is None:
+                catq_fakeq_linear_bwd(dY, X, L.W_fake, rows, L.d_out, L.d_in, L.W, L.stats, L.d_mu,
+                                      L.d_alpha, L.d_delta, p, L.g_mu, L.g_alpha, L.g_delta, ws,
+                                      dX=dX, n_experts=E_, row_offsets=offs)
+                return
+            ready = torch.cuda.Event()
+            ready.record(main)
+            side.wait_event(ready)
+            with torch.cuda.stream(side):
+                catq_fakeq_linear_bwd(dY, X, L.W_fake, rows, L.d_out, L.d_in, L.W, L.stats, L.d_mu,
+                                      L.d_alpha, L.d_delta, p, L.g_mu, L.g_alpha, L.g_delta, ws,
+                                      n_experts=E_, row_offsets=offs)
             catq_fakeq_linear_bwd(dY, X, L.W_fake, rows, L.d_out, L.d_in, L.W, L.stats, L.d_mu,
-                                  L.d_alpha, L.d_delta, p, L.g_mu, L.g_alpha, L.g_delta, ws,
-                                  dX=dX, n_experts=E_, row_offsets=offs)
+                                  L.d_alpha, L.d_delta, p, None, None, None, None, dX=dX,
+                                  n_experts=E_, row_offsets=offs)
 
         catq_aux_moe_combine_bwd(self.dy, self.perm, self.wts, self.dyg, k)
         lbwd("d", self.dyg, self.a, self.da, R, E, self.offs)
@@ -421,6 +479,8 @@ class MoEBlock:
                                self.attn_ws)
         lbwd("qkv", self.dqkv, self.xn1, self.dxn1, M)
         catq_aux_rmsnorm_bwd(x, self.rstd1, self.dxn1, self.dx, dres=self.dh1)
+        if side is not None:
+            main.wait_stream(side)
 
     step = DenseBlock.step
 

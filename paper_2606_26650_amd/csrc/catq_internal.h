@@ -122,4 +122,42 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// ------------------------------------------------ direct-to-LDS copies
+
+// 16-byte global -> LDS copy, lane l landing at lds_base + 16*l.  Issued as
+// inline assembly so that the compiler does not add conservative waits before
+// every LDS read; the kernel waits (vmcnt) itself before the barrier that
+// publishes the tile.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16(const void* g, const void* lds_base) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  const unsigned l = __builtin_amdgcn_readfirstlane(
+      (unsigned)(uintptr_t)(__attribute__((address_space(3))) const void*)lds_base);
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(l), "v"(g)
+               : "memory", "m0");
+#endif
+}
+#pragma clang diagnostic pop
+
+__device__ __forceinline__ void wait_vmem() {
+#if defined(__HIP_DEVICE_COMPILE__)
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+#endif
+}
+
+typedef short lds_v4s __attribute__((ext_vector_type(4)));
+
+// ds_read_b64_tr_b16 from an LDS address given as a generic pointer into a
+// __shared__ array.  Within a block of 16 lanes, output lane i receives
+// element e from lanes 4e..4e+3, column i mod 4 of their 8-byte rows.
+__device__ __forceinline__ lds_v4s lds_read_tr16(const void* p) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) lds_v4s*)(const_cast<void*>(p)));
+#else
+  return lds_v4s{0, 0, 0, 0};
+#endif
+}
+
 }  // namespace catq

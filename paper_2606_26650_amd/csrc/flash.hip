@@ -118,6 +118,61 @@ __device__ __forceinline__ f32x16 zero16() {
 // row (within a 32-row accumulator block) of register r for lane group g
 __device__ __forceinline__ int acc_row(int r, int g) { return 8 * (r >> 2) + 4 * g + (r & 3); }
 
+// Row-major 64 x D tiles filled by direct-to-LDS copies.  The 16-byte chunk
+// c of row r sits at slot r*(D/8) + (c ^ tswz(r)).  For D = 128 the key
+// ((r & 3) << 2) | ((r >> 2) & 3) puts both the 128-bit reads of 16
+// consecutive rows at one chunk (fragments of K, Q, dO, V rows) and the
+// transpose reads of 4 consecutive rows x 4 chunks (fragments of V^T, K^T,
+// Q^T, dO^T) on 16 distinct bank groups; for D = 64 (8 chunks a row, two
+// rows per 256-byte bank cycle) the key (r >> 1) & 7 does the former.
+template <int D>
+__device__ __forceinline__ int tswz(int r) {
+  if constexpr (D == 128)
+    return ((r & 3) << 2) | ((r >> 2) & 3);
+  else
+    return (r >> 1) & 7;
+}
+
+// 64 rows of D bf16 from row0 (rows at or past `rows` read the last row);
+// all four wavefronts of the block take part.
+template <int D>
+__device__ __forceinline__ void dma_tile(const bf16* base, int64_t ld, int64_t row0, int64_t rows,
+                                         uint4* lds, int wave, int lane) {
+  constexpr int CPR = D / 8, RPI = 64 / CPR, NI = 64 / RPI / 4;
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+    const int r = (wave * NI + i) * RPI + lane / CPR;
+    const int c = (lane % CPR) ^ tswz<D>(r);
+    dma16(base + min(row0 + r, rows - 1) * ld + c * 8, &lds[(wave * NI + i) * 64]);
+  }
+}
+
+// Fragment of row `row`, 16-byte chunk `chunk` (8 consecutive columns).
+template <int D>
+__device__ __forceinline__ bf16x8 tfrag_row(const uint4* lds, int row, int chunk) {
+  return *reinterpret_cast<const bf16x8*>(&lds[row * (D / 8) + (chunk ^ tswz<D>(row))]);
+}
+
+// Transposed fragment: column col0 + lane%32, rows 16*slice + 4g + 0..3 then
+// 16*slice + 8 + 4g + 0..3 (g = lane/32): the permuted key order of the
+// score accumulators, read with two transpose loads.
+template <int D>
+__device__ __forceinline__ bf16x8 tfrag_tr(const uint4* lds, int col0, int slice, int lane) {
+  const int blk = lane >> 4, s = lane & 15;
+  const int col = col0 + 16 * (blk & 1) + 4 * (s & 3);
+  u32x4 u;
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    const int row = 16 * slice + 4 * (blk >> 1) + 8 * c + (s >> 2);
+    const short* p = reinterpret_cast<const short*>(lds) + row * D +
+                     (((col >> 3) ^ tswz<D>(row)) << 3) + (col & 7);
+    const lds_v4s v = lds_read_tr16(p);
+    u[2 * c] = (unsigned)(unsigned short)v[0] | ((unsigned)(unsigned short)v[1] << 16);
+    u[2 * c + 1] = (unsigned)(unsigned short)v[2] | ((unsigned)(unsigned short)v[3] << 16);
+  }
+  return __builtin_bit_cast(bf16x8, u);
+}
+
 }  // namespace fa
 
 // ------------------------------------------------------------------ forward
@@ -125,9 +180,11 @@ __device__ __forceinline__ int acc_row(int r, int g) { return 8 * (r >> 2) + 4 *
 template <int D>
 __global__ __launch_bounds__(fa::NT, 2) void flash_fwd_kernel(FaArgs a) {
   using C = fa::Cfg<D>;
-  __shared__ u16 sK[fa::BK * C::KP];
-  __shared__ u16 sV[D * fa::TP];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 5, l32 = lane & 31;
+  constexpr int TW = 64 * D / 8;  // 16-byte slots of one 64 x D tile
+  __shared__ uint4 sK[2][TW];
+  __shared__ uint4 sV[2][TW];
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   // grid (B*Hq, query tiles): the longest causal rows are dispatched first
   const int qt = (int)gridDim.y - 1 - (int)blockIdx.y;
   const int h = blockIdx.x % a.Hq, b = blockIdx.x / a.Hq;
@@ -154,85 +211,87 @@ __global__ __launch_bounds__(fa::NT, 2) void flash_fwd_kernel(FaArgs a) {
   const int q_last = min(q0 + 127, a.S - 1);
   const int nkt = q_last / fa::BK + 1;
   const int wave_first = q0 + 32 * w, wave_last = wave_first + 31;
-  fa::Tile<D> tk, tv;
-  tk.load(Kb, D, 0, a.S, tid);
-  tv.load(Vb, D, 0, a.S, tid);
+  auto issue = [&](int buf, int k0) {
+    fa::dma_tile<D>(Kb, D, k0, a.S, sK[buf], w, lane);
+    fa::dma_tile<D>(Vb, D, k0, a.S, sV[buf], w, lane);
+  };
+  issue(0, 0);
+  wait_vmem();
+  __syncthreads();
   for (int kt = 0; kt < nkt; ++kt) {
-    const int k0 = kt * fa::BK;
-    __syncthreads();  // previous tile fully consumed
-    tk.store_rows(sK);
-    tv.store_transposed(sV);
-    __syncthreads();
-    if (kt + 1 < nkt) {
-      tk.load(Kb, D, k0 + fa::BK, a.S, tid);
-      tv.load(Vb, D, k0 + fa::BK, a.S, tid);
-    }
-    if (k0 > wave_last) continue;
-    // S^T for the two 32-key blocks
-    f32x16 s[2];
+    const int k0 = kt * fa::BK, buf = kt & 1;
+    // the next tile lands in the buffer every wave finished reading before
+    // the previous barrier
+    if (kt + 1 < nkt) issue(buf ^ 1, k0 + fa::BK);
+    if (k0 <= wave_last) {
+      // S^T for the two 32-key blocks
+      f32x16 s[2];
 #pragma unroll
-    for (int sb = 0; sb < 2; ++sb) {
-      s[sb] = fa::zero16();
+      for (int sb = 0; sb < 2; ++sb) {
+        s[sb] = fa::zero16();
 #pragma unroll
-      for (int t = 0; t < C::KS; ++t)
-        s[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            fa::frag_rows(sK, sb * 32 + l32, 16 * t + 8 * g, C::KP), qf[t], s[sb], 0, 0, 0);
-    }
-    // causal / length mask, only on tiles that cross the wave's diagonal or
-    // the sequence end; then the tile max of the raw scores (the scale c > 0
-    // commutes with the max)
-    float mt = -INFINITY;
-    if (k0 + fa::BK - 1 > wave_first || k0 + fa::BK > a.S) {
+        for (int t = 0; t < C::KS; ++t)
+          s[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              fa::tfrag_row<D>(sK[buf], sb * 32 + l32, 2 * t + g), qf[t], s[sb], 0, 0, 0);
+      }
+      // causal / length mask, only on tiles that cross the wave's diagonal or
+      // the sequence end; then the tile max of the raw scores (the scale c > 0
+      // commutes with the max)
+      float mt = -INFINITY;
+      if (k0 + fa::BK - 1 > wave_first || k0 + fa::BK > a.S) {
+#pragma unroll
+        for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = k0 + sb * 32 + fa::acc_row(r, g);
+            if (key > qme || key >= a.S) s[sb][r] = -INFINITY;
+            mt = fmaxf(mt, s[sb][r]);
+          }
+      } else {
+#pragma unroll
+        for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[sb][r]);
+      }
+      mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+      const float mn = fmaxf(m, mt * a.c);
+      // a lane whose query lies past the sequence end sees only masked keys
+      const float msafe = (mn == -INFINITY) ? 0.f : mn;
+      const float alpha = __builtin_amdgcn_exp2f(m - msafe);
+      float rs = 0.f;
 #pragma unroll
       for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int key = k0 + sb * 32 + fa::acc_row(r, g);
-          if (key > qme || key >= a.S) s[sb][r] = -INFINITY;
-          mt = fmaxf(mt, s[sb][r]);
+          const float p = __builtin_amdgcn_exp2f(fmaf(s[sb][r], a.c, -msafe));
+          s[sb][r] = p;
+          rs += p;
         }
-    } else {
+      rs += __shfl_xor(rs, 32, 64);
+      l = l * alpha + rs;
+      // alpha == 1 exactly unless the running max moved: skip the rescale when
+      // it moved for no lane of the wave
+      if (__any(mn != m)) {
+#pragma unroll
+        for (int i = 0; i < C::DB; ++i)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o[i][r] *= alpha;
+      }
+      m = mn;
+      // O^T += V^T P^T (V^T fragments by transpose reads of the V rows)
 #pragma unroll
       for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[sb][r]);
+        for (int hh = 0; hh < 2; ++hh) {
+          const bf16x8 pf = fa::pack8(s[sb], hh);
+#pragma unroll
+          for (int i = 0; i < C::DB; ++i)
+            o[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                fa::tfrag_tr<D>(sV[buf], i * 32, 2 * sb + hh, lane), pf, o[i], 0, 0, 0);
+        }
     }
-    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-    const float mn = fmaxf(m, mt * a.c);
-    // a lane whose query lies past the sequence end sees only masked keys
-    const float msafe = (mn == -INFINITY) ? 0.f : mn;
-    const float alpha = __builtin_amdgcn_exp2f(m - msafe);
-    float rs = 0.f;
-#pragma unroll
-    for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(s[sb][r], a.c, -msafe));
-        s[sb][r] = p;
-        rs += p;
-      }
-    rs += __shfl_xor(rs, 32, 64);
-    l = l * alpha + rs;
-    // alpha == 1 exactly unless the running max moved: skip the rescale when
-    // it moved for no lane of the wave
-    if (__any(mn != m)) {
-#pragma unroll
-      for (int i = 0; i < C::DB; ++i)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) o[i][r] *= alpha;
-    }
-    m = mn;
-    // O^T += V^T P^T
-#pragma unroll
-    for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        const bf16x8 pf = fa::pack8(s[sb], hh);
-#pragma unroll
-        for (int i = 0; i < C::DB; ++i)
-          o[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              fa::frag_tr(sV, i * 32 + l32, 2 * sb + hh, g), pf, o[i], 0, 0, 0);
-      }
+    wait_vmem();
+    __syncthreads();
   }
   if (qme < a.S) {
     const float inv = 1.0f / l;

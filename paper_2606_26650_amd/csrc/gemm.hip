@@ -366,29 +366,6 @@ __device__ __forceinline__ void store4f(bf16* p, f32x4 v) {
 // MFMAs of sub-step kk, and the first reads of the next tile overlap the last
 // sub-step after the barrier.
 
-// 16-byte global -> LDS copy, lane l landing at lds_base + 16*l.  Issued as
-// inline assembly so that the compiler does not add conservative waits before
-// every LDS read; the kernel waits (vmcnt) itself before the barrier that
-// publishes the tile.
-#pragma clang diagnostic push
-#pragma clang diagnostic ignored "-Winline-asm"
-__device__ __forceinline__ void dma16(const void* g, const void* lds_base) {
-#if defined(__HIP_DEVICE_COMPILE__)
-  const unsigned l = __builtin_amdgcn_readfirstlane(
-      (unsigned)(uintptr_t)(__attribute__((address_space(3))) const void*)lds_base);
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(l), "v"(g)
-               : "memory", "m0");
-#endif
-}
-#pragma clang diagnostic pop
-
-__device__ __forceinline__ void wait_vmem() {
-#if defined(__HIP_DEVICE_COMPILE__)
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-#endif
-}
-
-typedef short lds_v4s __attribute__((ext_vector_type(4)));
 
 // K-contiguous operand tile, ROWS x 64, for NW waves.
 template <int ROWS, int NW>

@@ -103,17 +103,25 @@ extern "C" catq_status catq_fakeq_linear_bwd(
     float* dW_fake, void* workspace, size_t workspace_bytes, hipStream_t stream) {
   clear_error();
   CATQ_TRY(check_linear_common(X, W_fake, dtype, M, N, K, n_experts, row_offsets));
-  CATQ_REQUIRE(dY && W && stats && d_mu && d_alpha && d_delta && g_d_mu && g_d_alpha && g_d_delta,
-               CATQ_ERR_NULL, "dY, W, stats, factors and factor-gradient outputs are required");
-  CATQ_REQUIRE(dtype_ok(w_dtype), CATQ_ERR_DTYPE, "bad w_dtype");
+  // with no factor gradient and no dW_fake requested only dX is computed
+  const bool want_g = g_d_mu || g_d_alpha || g_d_delta || dW_fake;
+  CATQ_REQUIRE(dY && (want_g || dX), CATQ_ERR_NULL, "dY, and dX or the factor gradients, are required");
   CATQ_REQUIRE(N % 8 == 0, CATQ_ERR_SHAPE, "N must be a multiple of 8");
-  CATQ_TRY(check_lmst_params(p, K));
-  CATQ_REQUIRE(aligned16(dY) && aligned16(X) && aligned16(W_fake) && aligned16(W) &&
-                   aligned16(dX) && aligned16(dW_fake) && aligned16(workspace) && aligned16(stats),
-               CATQ_ERR_ALIGN, "pointers must be 16-byte aligned");
-  const size_t need = catq_workspace_size(CATQ_WS_LINEAR_BWD, M, N, K, n_experts);
-  CATQ_REQUIRE(workspace != nullptr && workspace_bytes >= need, CATQ_ERR_WORKSPACE,
-               "workspace of %zu bytes needed (got %zu)", need, workspace_bytes);
+  if (!want_g) {
+    CATQ_REQUIRE(aligned16(dY) && aligned16(X) && aligned16(W_fake) && aligned16(dX), CATQ_ERR_ALIGN,
+                 "pointers must be 16-byte aligned");
+  } else {
+    CATQ_REQUIRE(W && stats && d_mu && d_alpha && d_delta && g_d_mu && g_d_alpha && g_d_delta,
+                 CATQ_ERR_NULL, "W, stats, factors and all three factor-gradient outputs are required");
+    CATQ_REQUIRE(dtype_ok(w_dtype), CATQ_ERR_DTYPE, "bad w_dtype");
+    CATQ_TRY(check_lmst_params(p, K));
+    CATQ_REQUIRE(aligned16(dY) && aligned16(X) && aligned16(W_fake) && aligned16(W) &&
+                     aligned16(dX) && aligned16(dW_fake) && aligned16(workspace) && aligned16(stats),
+                 CATQ_ERR_ALIGN, "pointers must be 16-byte aligned");
+    const size_t need = catq_workspace_size(CATQ_WS_LINEAR_BWD, M, N, K, n_experts);
+    CATQ_REQUIRE(workspace != nullptr && workspace_bytes >= need, CATQ_ERR_WORKSPACE,
+                 "workspace of %zu bytes needed (got %zu)", need, workspace_bytes);
+  }
   const int64_t E = n_experts;
   const int ns = splits_used(M, N, K, n_experts);
   const size_t g_bytes = round_up((size_t)(E * N * K) * 4 * (size_t)ns, 256);
@@ -142,6 +150,7 @@ extern "C" catq_status catq_fakeq_linear_bwd(
     }
     CATQ_TRY(gemm_run(a, 0, 1, dtype, dtype, stream));
   }
+  if (!want_g) return CATQ_OK;
   // G = dY^T . X  (contraction over the tokens: both operands K-major), fp32
   {
     GemmArgs a = gemm_args_default();

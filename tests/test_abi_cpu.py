@@ -102,6 +102,16 @@ def test_linear_and_loss_validation(cq):
     a3 = list(args)
     a3[5] = 252
     assert L.catq_fakeq_linear_bwd(*a3) == 2                   # N % 8
+    a4 = list(args)
+    a4[17] = None
+    assert L.catq_fakeq_linear_bwd(*a4) == 1                   # one factor gradient missing
+    a5 = list(args)
+    a5[16:20] = [None, None, None, None]
+    assert L.catq_fakeq_linear_bwd(*a5) == 1                   # neither dX nor gradients
+    a6 = list(args)
+    a6[17:20] = [None, None, None]
+    a6[16] = FAKE + 2
+    assert L.catq_fakeq_linear_bwd(*a6) == 5                   # dX-only path: alignment
     need = L.catq_workspace_size(0, 64, 256, 128, 1)
     assert need >= 256 * 128 * 4
     assert L.catq_block_recon_loss(FAKE, FAKE, 1, 12, FAKE, None, 1, FAKE, 1 << 20, None) == 2

@@ -178,6 +178,37 @@ def test_block_step_deterministic(catq):
         assert torch.equal(a, b)
 
 
+@pytest.mark.parametrize("kind", ["dense", "moe"])
+def test_overlapped_step_matches_serial(catq, kind):
+    """The two-stream schedule (weight-gradient halves and the finalize on a
+    side stream) gives bit for bit the one-stream results."""
+    import torch
+    if kind == "dense":
+        cfg = sg.small_dense(batch=2, seq=128, hidden=256, n_q=4, n_kv=2, head_dim=64, ffn=384)
+        blk, _, _, xb = _dense_setup(cfg)
+    else:
+        cfg = sg.small_moe(batch=1, seq=96, hidden=256, n_q=4, n_kv=2, head_dim=64, n_experts=8,
+                           top_k=2, expert_ffn=128, router_bias_std=1.0)
+        blk, _, _, xb, _ = _moe_setup(cfg)
+    x = to_dev_bf16(xb)
+    y_fp = blk.new_output()
+    blk.target(x, y_fp)
+    out = []
+    for overlap in (False, True):
+        fin = blk.finalize_buffers()
+        l = blk.step(x, y_fp, mode=lmst.SOFT, s=15.0, overlap=overlap, finalize=fin).clone()
+        torch.cuda.synchronize()
+        out.append((l, blk.dx.clone(), [t.clone() for L in blk.lin.values()
+                                        for t in (L.g_mu, L.g_alpha, L.g_delta)],
+                    fin["_flat"]["packed"].clone(), fin["_flat"]["alpha"].clone()))
+    a, b = out
+    assert torch.equal(a[0], b[0])
+    assert torch.equal(a[1].view(torch.int16), b[1].view(torch.int16))
+    for u, v in zip(a[2], b[2]):
+        assert torch.equal(u, v)
+    assert torch.equal(a[3], b[3]) and torch.equal(a[4], b[4])
+
+
 def test_full_size_block_properties(catq):
     """The 1.7B-shaped block at its real size (4 x 2048 tokens): identity
     branch gives loss 0, soft step gives a finite positive loss and finite
