@@ -52,6 +52,9 @@ def parse():
     ap.add_argument("--no-overlap", action="store_true",
                     help="run the step on one stream (no side stream for the weight-gradient "
                          "halves and the finalize)")
+    ap.add_argument("--window", type=int, default=1,
+                    help="calibrate this many consecutive blocks jointly (sliding-window "
+                         "reconstruction; 1 = the single-block step)")
     return ap.parse_args()
 
 
@@ -169,7 +172,12 @@ def main():
     cfg = sg.QWEN3_1P7B
     W = sg.block_weights(cfg, 0)
     xb = sg.activations(cfg, 0)
-    blk = DenseBlock(cfg, W)
+    if args.window > 1:
+        from paper_2606_26650_amd.window import Window
+        blk = Window([DenseBlock(cfg, W)] +
+                     [DenseBlock(cfg, sg.block_weights(cfg, i)) for i in range(1, args.window)])
+    else:
+        blk = DenseBlock(cfg, W)
     x = bf16_tensor(xb)
     y_fp = blk.new_output()
     blk.target(x, y_fp)
@@ -231,7 +239,7 @@ def main():
     out = {
         "metric": METRIC,
         "value": args.steps / elapsed,
-        "unit": "block-steps/s",
+        "unit": "block-steps/s" if args.window == 1 else "window-steps/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
@@ -241,9 +249,10 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": "qwen3-1.7b-shaped decoder block, 4 x 2048 tokens, one CAT-Q "
-                               "calibration step (LM+ST s=15, fwd, loss, bwd to factors, "
-                               "ternarise+pack)",
+        "config": {"workload": ("qwen3-1.7b-shaped decoder block" if args.window == 1 else
+                                f"window of {args.window} qwen3-1.7b-shaped decoder blocks") +
+                               ", 4 x 2048 tokens, one CAT-Q calibration step (LM+ST s=15, fwd, "
+                               "loss, bwd to factors, ternarise+pack)",
                    "hidden": cfg.hidden, "heads": [cfg.n_q, cfg.n_kv, cfg.head_dim],
                    "ffn": cfg.ffn, "tokens": cfg.tokens, "group_size": 128,
                    "weights": cfg.n_weights()},
@@ -268,7 +277,7 @@ def main():
         "lmst_bwd_gbs": lmb["bytes"] / (lmb["ms"] * 1e-3) / 1e9 if lmb["ms"] else None,
         "loss": loss,
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.window == 1:
         out["cpu_baseline"] = cpu_baseline(cfg, W, xb)
     if args.breakdown:
         shp = {}

@@ -233,12 +233,14 @@ class DenseBlock:
         return self.forward(x, out)
 
     # --------------------------------------------------------------- backward
-    def backward(self, x, p, overlap=True):
+    def backward(self, x, p, overlap=True, dy=None, join=True):
         """Backward to the block input and to every factor.  With ``overlap``
         each linear's weight-gradient half (G = dY^T X and the factor
         gradients) runs on the side stream as soon as dY is ready, while the
         main stream carries on with dX and the glue; the main stream waits
-        for the side stream at the end."""
+        for the side stream at the end (unless ``join`` is false: a window
+        of blocks joins once, after its first block).  ``dy`` is the
+        gradient of the block output (default: the loss's, in self.dy)."""
         c, M = self.cfg, self.M
         h = c.hidden
         ws = self.lin_ws
@@ -261,16 +263,17 @@ class DenseBlock:
             catq_fakeq_linear_bwd(dY, X, L.W_fake, M, L.d_out, L.d_in, L.W, L.stats, L.d_mu,
                                   L.d_alpha, L.d_delta, p, None, None, None, None, dX=dX)
 
-        lbwd("d", self.dy, self.a, self.da)
+        dy = self.dy if dy is None else dy
+        lbwd("d", dy, self.a, self.da)
         catq_aux_swiglu_bwd(self.gu, self.da, self.dgu)
         lbwd("gu", self.dgu, self.xn2, self.dxn2)
-        catq_aux_rmsnorm_bwd(self.h1, self.rstd2, self.dxn2, self.dh1, dres=self.dy)
+        catq_aux_rmsnorm_bwd(self.h1, self.rstd2, self.dxn2, self.dh1, dres=dy)
         lbwd("o", self.dh1, self.attn, self.dattn)
         catq_aux_attention_bwd(self.desc, self.qkv, self.attn, self.saved, self.dattn, self.dqkv,
                                self.attn_ws)
         lbwd("qkv", self.dqkv, self.xn1, self.dxn1)
         catq_aux_rmsnorm_bwd(x, self.rstd1, self.dxn1, self.dx, dres=self.dh1)
-        if side is not None:
+        if side is not None and join:
             main.wait_stream(side)
 
     # ------------------------------------------------------------------- step
@@ -442,7 +445,7 @@ class MoEBlock:
         self.modulate_all(self.params(IDENTITY))
         return self.forward(x, out)
 
-    def backward(self, x, p, overlap=True):
+    def backward(self, x, p, overlap=True, dy=None, join=True):
         """As DenseBlock.backward, with the routed-expert MLP half."""
         c, M, R = self.cfg, self.M, self.R
         h, E, F, k = c.hidden, c.n_experts, c.expert_ffn, c.top_k
@@ -468,18 +471,19 @@ class MoEBlock:
                                   L.d_alpha, L.d_delta, p, None, None, None, None, dX=dX,
                                   n_experts=E_, row_offsets=offs)
 
-        catq_aux_moe_combine_bwd(self.dy, self.perm, self.wts, self.dyg, k)
+        dy = self.dy if dy is None else dy
+        catq_aux_moe_combine_bwd(dy, self.perm, self.wts, self.dyg, k)
         lbwd("d", self.dyg, self.a, self.da, R, E, self.offs)
         catq_aux_swiglu_bwd(self.gu, self.da, self.dgu)
         lbwd("gu", self.dgu, self.xg, self.dxg, R, E, self.offs)
         catq_aux_moe_scatter_add(self.dxg, self.perm, self.dxn2, k)
-        catq_aux_rmsnorm_bwd(self.h1, self.rstd2, self.dxn2, self.dh1, dres=self.dy)
+        catq_aux_rmsnorm_bwd(self.h1, self.rstd2, self.dxn2, self.dh1, dres=dy)
         lbwd("o", self.dh1, self.attn, self.dattn, M)
         catq_aux_attention_bwd(self.desc, self.qkv, self.attn, self.saved, self.dattn, self.dqkv,
                                self.attn_ws)
         lbwd("qkv", self.dqkv, self.xn1, self.dxn1, M)
         catq_aux_rmsnorm_bwd(x, self.rstd1, self.dxn1, self.dx, dres=self.dh1)
-        if side is not None:
+        if side is not None and join:
             main.wait_stream(side)
 
     step = DenseBlock.step

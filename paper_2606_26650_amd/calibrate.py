@@ -45,8 +45,9 @@ def linear_lr(step: int, total: int, lr0: float = 1e-3) -> float:
 
 
 class BlockCalibrator:
-    """Calibrates one block (a DenseBlock or MoEBlock driver) on a cached set
-    of calibration samples already resident on the device.
+    """Calibrates one block (a DenseBlock or MoEBlock driver), or a window of
+    blocks, on a cached set of calibration samples already resident on the
+    device.
 
     ``x_all`` is [n_samples * seq][hidden] bf16; batches are consecutive runs
     of ``block.cfg.batch`` samples.  The full-precision targets of every batch
@@ -63,10 +64,10 @@ class BlockCalibrator:
         self.n_batches = x_all.shape[0] // self.tok_per_batch
         self.n_epochs, self.gamma, self.s0, self.lr0 = n_epochs, gamma, s0, lr0
         self.total_steps = n_epochs * self.n_batches
-        A = block.arena
-        self.params = [A.d_mu, A.d_alpha, A.d_delta]
-        self.grads = [A.g_mu, A.g_alpha, A.g_delta]
-        self.bounds = [(-DMU_LIM, DMU_LIM), (POS_MIN, 1e30), (POS_MIN, 1e30)]
+        arenas = getattr(block, "arenas", None) or [block.arena]
+        self.params = [t for A in arenas for t in (A.d_mu, A.d_alpha, A.d_delta)]
+        self.grads = [t for A in arenas for t in (A.g_mu, A.g_alpha, A.g_delta)]
+        self.bounds = [(-DMU_LIM, DMU_LIM), (POS_MIN, 1e30), (POS_MIN, 1e30)] * len(arenas)
         self.m = [torch.zeros_like(p) for p in self.params]
         self.v = [torch.zeros_like(p) for p in self.params]
         self.step_no = 0          # optimiser steps taken
@@ -114,7 +115,7 @@ class BlockCalibrator:
 
     def load(self, path: str):
         with np.load(path, allow_pickle=False) as z:
-            for i in range(3):
+            for i in range(len(self.params)):
                 self.params[i].copy_(torch.from_numpy(z[f"p{i}"]))
                 self.m[i].copy_(torch.from_numpy(z[f"m{i}"]))
                 self.v[i].copy_(torch.from_numpy(z[f"v{i}"]))
@@ -122,7 +123,10 @@ class BlockCalibrator:
             self.step_no = int(z["step"])
             self.losses = [torch.from_numpy(z["losses"]).to(self.params[0].device)] \
                 if z["losses"].size else []
-        self.blk.stats_ready = False  # recomputed on the next step
+        if hasattr(self.blk, "invalidate_stats"):   # recomputed on the next step
+            self.blk.invalidate_stats()
+        else:
+            self.blk.stats_ready = False
 
     def finalize(self):
         """Final hard ternarisation and 2-bit packing of every weight."""

@@ -47,3 +47,19 @@ def test_dense_calibration_is_step_plus_adamw():
             p, _, _ = calib.adamw_step(fac0[n][i], r["fgrads"][n][i], np.zeros_like(fac0[n][i]),
                                        np.zeros_like(fac0[n][i]), 1, 1e-3, kind=kind)
             np.testing.assert_array_equal(out["factors"][n][i], p)
+
+
+@pytest.mark.parametrize("n,l,stride", [(1, 1, 1), (5, 2, 1), (5, 2, 2), (36, 4, 1), (36, 4, 3),
+                                        (7, 3, 3), (3, 8, 1)])
+def test_host_window_spans_match_oracle(n, l, stride):
+    """The sliding-window geometry the GPU driver walks is the oracle's."""
+    from oracle import window as ow
+    from paper_2606_26650_amd import window
+    assert window.window_spans(n, l, stride) == ow.window_spans(n, l, stride)
+
+
+def test_host_window_spans_reject_bad_geometry():
+    from paper_2606_26650_amd import window
+    for args in [(0, 2, 1), (4, 0, 1), (4, 2, 0), (6, 2, 3)]:
+        with pytest.raises(ValueError):
+            window.window_spans(*args)

@@ -1,0 +1,161 @@
+"""GPU parity of the sliding-window reconstruction (Eq. 7 over several
+blocks): the window step against the oracle's window step, the two-stream
+schedule against the one-stream one, and the window-by-window calibration
+against the oracle's own trajectory (the two sides follow their own
+trajectories; nothing the GPU computes is fed to the oracle)."""
+import numpy as np
+import pytest
+
+import synthgen as sg
+from helpers import f64, host, max_norm_err, median_rel, to_dev_bf16
+from oracle import calib, lmst, window
+
+pytestmark = pytest.mark.gpu
+
+LIN_ID = {"qkv": 0, "o": 1, "gu": 2, "d": 3}
+
+
+def _blocks(cfg, n, fac_seed0=None):
+    """n dense blocks with weights drawn from seeds 0..n-1; factors loaded
+    when fac_seed0 is given.  Returns GPU blocks, oracle weights, oracle
+    factors."""
+    from paper_2606_26650_amd.block import DenseBlock
+    blks, Wos, facs = [], [], []
+    for i in range(n):
+        W = sg.block_weights(cfg, i)
+        blk = DenseBlock(cfg, W)
+        fac = {}
+        if fac_seed0 is not None:
+            for name, L in blk.lin.items():
+                f = sg.perturbed_factors(fac_seed0 + i, L.n_groups, extra=(LIN_ID[name],))
+                L.set_factors(*f)
+                parts = [DenseBlock.split_fused(cfg, name, a) for a in f]
+                for k in parts[0]:
+                    fac[k] = [np.asarray(parts[j][k]).reshape(-1) for j in range(3)]
+        blks.append(blk)
+        Wos.append({k: f64(v) for k, v in W.items()})
+        facs.append(fac)
+    return blks, Wos, facs
+
+
+def _split(cfg, name, arrs):
+    from paper_2606_26650_amd.block import DenseBlock
+    parts = [DenseBlock.split_fused(cfg, name, host(a)) for a in arrs]
+    return {k: [np.asarray(parts[i][k]).reshape(-1) for i in range(3)] for k in parts[0]}
+
+
+@pytest.mark.parametrize("mode,s", [(lmst.SOFT, 15.0), (lmst.HARD, 0.0)])
+def test_window_step_parity(catq, mode, s):
+    import torch
+    from paper_2606_26650_amd.window import Window
+    cfg = sg.small_dense(batch=2, seq=136, hidden=256, n_q=4, n_kv=2, head_dim=64, ffn=384)
+    blks, Wos, facs = _blocks(cfg, 2, fac_seed0=1)
+    xb = sg.activations(cfg, 0)
+    x = to_dev_bf16(xb)
+    win = Window(blks)
+    y_fp = win.new_output()
+    win.target(x, y_fp)
+    loss = win.step(x, y_fp, mode=mode, s=s, s_bwd=30.0)
+    torch.cuda.synchronize()
+    print(f"[window] mode={mode} s={s} loss={loss.item():.6e}", flush=True)
+    ref = window.window_step(f64(xb), Wos, facs, cfg, mode, s=s if s else None, s_bwd=30.0)
+    tol = 2e-2
+    assert max_norm_err(host(y_fp), ref["y_fp"]) <= tol
+    assert max_norm_err(host(win.y), ref["y_q"]) <= tol
+    assert max_norm_err(host(blks[0].y), ref["inputs"][1]) <= tol
+    assert abs(loss.item() - ref["loss"]) <= tol * ref["loss"], (loss.item(), ref["loss"])
+    assert max_norm_err(host(win.dx), ref["dx"]) <= tol
+    assert max_norm_err(host(blks[1].dx), _inner_dy(ref, cfg)) <= tol
+    # The factor gradients of block b come through the backward of the
+    # n - b blocks from the loss down to it, each adding the bf16 rounding of
+    # its activations and gradients: the one-block bound scales with that
+    # depth.
+    n = len(blks)
+    for b, blk in enumerate(blks):
+        worst = 0.0
+        for name, L in blk.lin.items():
+            for k, v in _split(cfg, name, (L.g_mu, L.g_alpha, L.g_delta)).items():
+                for i in range(3):
+                    r = ref["fgrads"][b][k][i]
+                    err = max_norm_err(v[i], r)
+                    worst = max(worst, err)
+                    assert err <= tol * (n - b), (b, k, i, err, median_rel(v[i], r))
+        print(f"[window] block {b}: worst factor-gradient error {worst:.4f}", flush=True)
+
+
+def _inner_dy(ref, cfg):
+    """Gradient of the loss at the output of the first block: the input
+    gradient of the last block, from the oracle's own backward."""
+    from oracle import block
+    _, xs, caches = window.window_forward(ref["inputs"][0], ref["W_fake"], cfg)
+    d, _ = block.block_backward(ref["dy"], caches[1], ref["W_fake"][1], cfg)
+    return d
+
+
+def test_window_overlap_matches_serial(catq):
+    import torch
+    from paper_2606_26650_amd.window import Window
+    cfg = sg.small_dense(batch=2, seq=128, hidden=256, n_q=4, n_kv=2, head_dim=64, ffn=384)
+    blks, _, _ = _blocks(cfg, 3, fac_seed0=4)
+    x = to_dev_bf16(sg.activations(cfg, 0))
+    win = Window(blks)
+    y_fp = win.new_output()
+    win.target(x, y_fp)
+    out = []
+    for overlap in (False, True):
+        fin = win.finalize_buffers()
+        l = win.step(x, y_fp, mode=lmst.SOFT, s=15.0, overlap=overlap, finalize=fin).clone()
+        torch.cuda.synchronize()
+        out.append((l, win.dx.clone(), [t.clone() for b in blks for L in b.lin.values()
+                                        for t in (L.g_mu, L.g_alpha, L.g_delta)],
+                    [f["_flat"]["packed"].clone() for f in fin]))
+    a, b = out
+    assert torch.equal(a[0], b[0])
+    assert torch.equal(a[1].view(torch.int16), b[1].view(torch.int16))
+    for u, v in zip(a[2], b[2]):
+        assert torch.equal(u, v)
+    for u, v in zip(a[3], b[3]):
+        assert torch.equal(u, v)
+
+
+N_SAMPLES, N_EPOCHS = 4, 3
+
+
+def test_sliding_calibration_against_oracle(catq):
+    import torch
+    from paper_2606_26650_amd.block import DenseBlock
+    from paper_2606_26650_amd.window import SlidingCalibrator
+    cfg = sg.small_dense(batch=2, seq=64, hidden=256, n_q=4, n_kv=2, head_dim=64, ffn=384)
+    xcfg = sg.small_dense(batch=N_SAMPLES, seq=64, hidden=256, n_q=4, n_kv=2, head_dim=64,
+                          ffn=384)
+    blks, Wos, _ = _blocks(cfg, 3)
+    xb = sg.activations(xcfg, 0)
+    cal = SlidingCalibrator(blks, to_dev_bf16(xb), l=2, n_epochs=N_EPOCHS)
+    bufs = cal.run()
+    torch.cuda.synchronize()
+    ref = window.sliding_calibration(f64(xb), Wos, cfg, l=2, n_epochs=N_EPOCHS)
+    assert [sp for sp, _ in cal.history] == [h["span"] for h in ref["history"]] == [(0, 2), (1, 3)]
+    steps = N_EPOCHS * (N_SAMPLES // cfg.batch)
+    for (sp, got), h in zip(cal.history, ref["history"]):
+        assert len(got) == len(h["losses"]) == steps
+        for k, (a, b) in enumerate(zip(got, h["losses"])):
+            assert abs(a - b) <= 2e-2 * b, (sp, k, a, b)
+    per_window = 2.0 * sum(calib.linear_lr(k, steps) for k in range(steps))
+    flips = total_w = 0
+    for i, blk in enumerate(blks):
+        n_win = sum(1 for a, e in cal.spans if a <= i < e)
+        drift = n_win * per_window
+        for name, L in blk.lin.items():
+            gf = _split(cfg, name, (L.d_mu, L.d_alpha, L.d_delta))
+            for k, v in gf.items():
+                for j in range(3):
+                    d = np.abs(v[j] - ref["factors"][i][k][j])
+                    assert d.max() <= drift, (i, k, j, d.max(), drift)
+            codes = DenseBlock.split_fused(cfg, name, bufs[i][name]["codes"].cpu().numpy())
+            for k, c in codes.items():
+                rc = lmst.modulate_ternarize(Wos[i][k], 128, *ref["factors"][i][k],
+                                             lmst.HARD)["codes"]
+                flips += int((c != rc).sum())
+                total_w += c.size
+    assert sorted(bufs) == [0, 1, 2]
+    assert flips <= 1e-2 * total_w, (flips, total_w)
