@@ -52,6 +52,9 @@ def parse():
     ap.add_argument("--no-overlap", action="store_true",
                     help="run the step on one stream (no side stream for the weight-gradient "
                          "halves and the finalize)")
+    ap.add_argument("--ternary", type=int, default=0, metavar="M",
+                    help="only time the packed-ternary decode layers of a Qwen3-14B-shaped "
+                         "block at M tokens (deployment on the 2-bit storage)")
     ap.add_argument("--window", type=int, default=1,
                     help="calibrate this many consecutive blocks jointly (sliding-window "
                          "reconstruction; 1 = the single-block step)")
@@ -143,6 +146,95 @@ def cpu_baseline(cfg, W, xb, row_frac=8):
             "seconds_per_step": step}
 
 
+def ternary_bench(args):
+    """Deployment side: the four linears of a Qwen3-14B-shaped block (q|k|v
+    7168x5120, o 5120x5120, gate|up 34816x5120, down 5120x17408) as packed
+    ternary weights, applied to M tokens (decode).  Random codes and scales
+    (the product's cost does not depend on their values); inputs resident in
+    HBM.  Reports HBM bytes moved per second (2-bit codes + fp32 scales + X +
+    Y, each once) against the 8 TB/s peak, with torch's bf16 dense product
+    on the same shapes (hipBLASLt) as context."""
+    import numpy as np
+    import torch
+
+    import paper_2606_26650_amd as cq
+
+    torch.cuda.set_device(0)
+    M = args.ternary
+    shapes = [("qkv", 7168, 5120), ("o", 5120, 5120), ("gu", 34816, 5120), ("d", 5120, 17408)]
+    g = torch.Generator(device="cuda").manual_seed(0)
+    layers = []
+    for name, n, k in shapes:
+        packed = torch.randint(0, 256, (n, k // 4), dtype=torch.uint8, device="cuda", generator=g)
+        alpha = torch.rand(n, k // 128, device="cuda", generator=g) * 0.05 + 0.002
+        x = torch.randn(M, k, device="cuda", generator=g).to(torch.bfloat16)
+        y = torch.empty(M, n, dtype=torch.float32, device="cuda")
+        layers.append((name, n, k, packed, alpha, x, y))
+
+    def run():
+        for _, _, _, packed, alpha, x, y in layers:
+            cq.catq_ternary_linear(x, packed, alpha, y)
+
+    for _ in range(args.warmup):
+        run()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        run()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    # per-launch durations (HIP events on the launch stream)
+    cq.catq_trace_enable(8 * args.steps + 8)
+    for _ in range(args.steps):
+        run()
+    torch.cuda.synchronize()
+    recs = cq.trace_records()
+    cq.catq_trace_disable()
+    per = {}
+    for r, (name, n, k, *_rest) in zip(recs, [l for _ in range(args.steps) for l in layers]):
+        a = per.setdefault(name, {"ms": 0.0, "bytes": r["bytes"], "tag": r["tag"]})
+        a["ms"] += r["ms"] / args.steps
+    tot_bytes = sum(v["bytes"] for v in per.values())
+    tot_ms = sum(v["ms"] for v in per.values())
+    big = per["gu"]
+    # context: bf16 dense weights through torch (hipBLASLt), same shapes
+    dense = [(torch.randn(n, k, device="cuda", generator=g).to(torch.bfloat16), x)
+             for (_, n, k, _, _, x, _) in layers]
+    for _ in range(3):
+        for w, x in dense:
+            torch.nn.functional.linear(x, w)
+    torch.cuda.synchronize()
+    d0 = time.perf_counter()
+    for _ in range(args.steps):
+        for w, x in dense:
+            torch.nn.functional.linear(x, w)
+    torch.cuda.synchronize()
+    dense_ms = 1000.0 * (time.perf_counter() - d0) / args.steps
+    out = {
+        "metric": "packed-ternary decode: HBM GB/s of the 2-bit linear layers",
+        "value": tot_bytes / (tot_ms * 1e-3) / 1e9,
+        "unit": "GB/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": 1000.0 * elapsed / args.steps,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"qwen3-14b-shaped block linears (q|k|v, o, gate|up, down) as "
+                               f"2-bit ternary + fp32 group scales, {M} token(s)",
+                   "tokens": M, "weights": sum(n * k for _, n, k in shapes), "group_size": 128},
+        "roofline": {"bound": "hbm", "kernel": big["tag"] + " (gate|up 34816x5120)",
+                     "achieved": big["bytes"] / (big["ms"] * 1e-3) / 1e9, "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s",
+                     "frac": big["bytes"] / (big["ms"] * 1e-3) / 1e9 / PEAK_HBM_GBS,
+                     "avg_launch_us": 1000.0 * big["ms"], "bytes_per_launch": big["bytes"],
+                     "traffic": None},
+        "per_layer": {k: {"us": 1000.0 * v["ms"], "GB/s": v["bytes"] / (v["ms"] * 1e-3) / 1e9}
+                      for k, v in per.items()},
+        "bf16_dense_torch_ms_per_step": dense_ms,
+        "kernel_ms_per_step": tot_ms,
+    }
+    print(json.dumps(out))
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -167,6 +259,10 @@ def main():
             b.copy_(a)
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4}))
+        return
+
+    if args.ternary > 0:
+        ternary_bench(args)
         return
 
     cfg = sg.QWEN3_1P7B

@@ -212,6 +212,24 @@ catq_status catq_block_recon_loss(const void* Y_q, const void* Y_fp, catq_dtype 
 catq_status catq_pack_ternary(const int8_t* codes, int64_t d_out, int64_t d_in, uint8_t* packed,
                               hipStream_t stream);
 
+/* catq_ternary_linear -- deployment-side linear layer on that storage:
+ *   Y[m][n] = sum_k X[m][k] * alpha[n][k / g] * T[n][k]
+ * i.e. Y = X (alpha * T)^T with the ternary weights and group scales of the
+ * final ternarisation (App. B.2: T plus one scale per group, no zero point),
+ * reading 2 bits per weight.  Code 3 (invalid) contributes 0.
+ *   X       bf16 [M][ldx] (row-major; d_in <= ldx <= 2^24, ldx % 8 == 0)
+ *   packed  uint8 [d_out][d_in/4] in the layout above
+ *   alpha   fp32 [d_out][d_in/g]
+ *   Y       y_dtype (fp32 or bf16) [M][ldy], ldy >= d_out; written, not
+ *           accumulated
+ * g is the group size (128 times a power of two, dividing d_in); d_in <= 65536.
+ * M = 0 is a no-op.  Accumulation in fp32 in a fixed order (bitwise
+ * deterministic); built for decode-sized M (every 16 tokens re-read the
+ * weights).  X and alpha 16-byte aligned, packed 8-byte, Y 4-byte. */
+catq_status catq_ternary_linear(const void* X, int64_t M, int64_t ldx, const uint8_t* packed,
+                                const float* alpha, int64_t d_out, int64_t d_in, int32_t g,
+                                void* Y, catq_dtype y_dtype, int64_t ldy, hipStream_t stream);
+
 /* Workspace sizes, in bytes, for the calls that take a workspace. */
 enum { CATQ_WS_LINEAR_BWD = 0, CATQ_WS_LOSS = 1 };
 size_t catq_workspace_size(int32_t which_call, int64_t M, int64_t N, int64_t K, int32_t n_experts);

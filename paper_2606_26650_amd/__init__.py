@@ -14,7 +14,7 @@ from ._lib import (BF16, F32, HARD, IDENTITY, SOFT, WS_LINEAR_BWD, WS_LOSS, Attn
 
 __all__ = [
     "catq_modulate_ternarize", "catq_fakeq_linear_fwd", "catq_fakeq_linear_bwd",
-    "catq_block_recon_loss", "catq_pack_ternary", "catq_workspace_size",
+    "catq_block_recon_loss", "catq_pack_ternary", "catq_ternary_linear", "catq_workspace_size",
     "catq_aux_rmsnorm_fwd", "catq_aux_rmsnorm_bwd", "catq_aux_attention_fwd",
     "catq_aux_attention_bwd", "catq_attn_saved_bytes", "catq_attn_bwd_workspace_bytes",
     "catq_aux_swiglu_fwd", "catq_aux_swiglu_bwd", "catq_aux_moe_route",
@@ -120,6 +120,18 @@ def catq_pack_ternary(codes, packed, stream=None):
     rows = codes.numel() // d_in
     st = lib.catq_pack_ternary(_ptr(codes), rows, d_in, _ptr(packed), _stream(stream))
     _lib.check("catq_pack_ternary", st)
+
+
+def catq_ternary_linear(X, packed, alpha, Y, g=128, stream=None):
+    """Y = X (alpha * T)^T from the 2-bit storage: X bf16 [M][d_in] (rows may
+    be strided), packed uint8 [d_out][d_in/4], alpha fp32 [d_out][d_in/g],
+    Y fp32 or bf16 [M][d_out] (rows may be strided)."""
+    d_out, d_in = packed.shape[0], packed.shape[1] * 4
+    M = X.shape[0]
+    st = lib.catq_ternary_linear(_ptr(X), M, X.stride(0) if M else d_in, _ptr(packed),
+                                 _ptr(alpha), d_out, d_in, g, _ptr(Y), _dt(Y),
+                                 Y.stride(0) if M else d_out, _stream(stream))
+    _lib.check("catq_ternary_linear", st)
 
 
 def catq_workspace_size(which, M, N, K, n_experts=1):

@@ -19,7 +19,7 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libcatq.so")
 
 SOURCES = ["status.hip", "trace.hip", "lmst.hip", "gemm.hip", "linear.hip", "loss.hip", "glue.hip",
-           "attention.hip", "flash.hip"]
+           "attention.hip", "flash.hip", "ternary.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950",
@@ -27,9 +27,15 @@ FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950",
          "-I", INCLUDE, "-I", CSRC, "-Wall", "-Wno-unused-result"]
 
 
+# per-source code generation options: the packed-ternary product keeps its
+# matrix-core accumulators in ordinary VGPRs (it scales them after every
+# 128-code chunk, so accumulation registers would cost a copy each time)
+EXTRA = {"ternary.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC, *FLAGS, *EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     err = "\n".join(l for l in r.stderr.splitlines() if "packed-fp32-ops" not in l)
     if r.returncode != 0:

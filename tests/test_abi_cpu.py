@@ -147,3 +147,32 @@ def test_workspace_sizes_monotone(cq):
     assert 0 < a < b
     assert cq.catq_workspace_size(1, 1 << 20, 1, 1) > 0
     assert cq.catq_workspace_size(0, 0, 4, 4) == 0
+
+
+def test_ternary_linear_validation(cq):
+    """Packed-ternary linear: shape, group size, dtype and alignment checks
+    fail before any launch; M = 0 is a no-op that touches nothing."""
+    L = cq.lib
+    # (X, M, ldx, packed, alpha, d_out, d_in, g, Y, y_dtype, ldy, stream)
+    ok = dict(X=FAKE, M=4, ldx=256, P=FAKE, A=FAKE, d_out=32, d_in=256, g=128, Y=FAKE, dt=0,
+              ldy=32)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return L.catq_ternary_linear(a["X"], a["M"], a["ldx"], a["P"], a["A"], a["d_out"],
+                                     a["d_in"], a["g"], a["Y"], a["dt"], a["ldy"], None)
+
+    assert call(M=0, X=None, P=None) == 0          # no-op
+    assert call(M=-1) == 2
+    assert call(X=None) == 1 and call(P=None) == 1 and call(A=None) == 1 and call(Y=None) == 1
+    assert call(d_in=192) == 2                      # not a multiple of g
+    assert call(g=64) == 4 and call(g=0) == 4       # g must be 128 * 2^j
+    assert call(g=384, d_in=768, ldx=768) == 4
+    assert call(g=256, d_in=384) == 2
+    assert call(d_in=128 * 513, ldx=128 * 513) == 2  # longer than the staged scales
+    assert call(ldx=200) == 2 and call(ldx=260) == 2
+    assert call(ldy=16) == 2
+    assert call(dt=3) == 3
+    assert call(X=FAKE + 8) == 5 and call(A=FAKE + 4) == 5 and call(P=FAKE + 4) == 5
+    assert call(Y=FAKE + 2) == 5
+    assert call(d_out=0) == 2

@@ -1,0 +1,149 @@
+"""GPU parity of the packed-ternary linear layer (deployment on the 2-bit
+storage) against the oracle's product of the decoded weights.
+
+Bound (fp32 output): every product x * 2T is exact in fp32 and the kernel
+sums them in fp32 (128 per chunk inside the matrix core), scales each chunk
+once by alpha/2 and adds the chunks and the waves' partials: at most
+128 + 1 + n_chunks + 16 roundings on any path, so |y - ref| <=
+(145 + n_chunks) * 2^-24 * sum_k |x_k alpha_k T_k|.  bf16 output adds one
+rounding to 8 significant bits, at most 2^-8 |y|."""
+import numpy as np
+import pytest
+
+import synthgen as sg
+from helpers import f64, host, to_dev_bf16
+from oracle import lmst, ternary
+
+pytestmark = pytest.mark.gpu
+
+
+def _case(d_out, d_in, M, g, seed):
+    rng = np.random.default_rng([seed, d_out, d_in, M, g])
+    codes = rng.integers(0, 3, (d_out, d_in))
+    packed = lmst.pack_ternary((codes - 1).astype(np.int8))
+    alpha = rng.uniform(0.002, 0.05, (d_out, d_in // g)).astype(np.float32)
+    xb = sg.normal_bf16(seed, "X", (M, d_in))
+    return packed, alpha, xb
+
+
+def _run(catq, packed, alpha, xb, g, y_dtype, ldx_pad=0, ldy_pad=0):
+    import torch
+    M, d_in = xb.shape
+    d_out = packed.shape[0]
+    x = torch.zeros(M, d_in + ldx_pad, dtype=torch.bfloat16, device="cuda")
+    if M:
+        x[:, :d_in] = to_dev_bf16(xb)
+    y = torch.full((M, d_out + ldy_pad), float("nan"), dtype=y_dtype, device="cuda")
+    p = torch.from_numpy(packed).cuda()
+    a = torch.from_numpy(alpha).cuda()
+    catq.catq_ternary_linear(x[:, :d_in], p, a, y[:, :d_out], g=g)
+    torch.cuda.synchronize()
+    return y
+
+
+def _bound(xo, packed, alpha, d_in, g, n_chunks):
+    return (145 + n_chunks) * 2.0 ** -24 * ternary.abs_terms(xo, packed, alpha, d_in, g)
+
+
+@pytest.mark.parametrize("d_out,d_in,M,g", [
+    (48, 384, 1, 128), (40, 256, 3, 128), (64, 1024, 16, 128), (33, 128, 17, 128),
+    (128, 3072, 5, 128), (16, 8192, 2, 128), (80, 2048, 40, 256), (7, 512, 1, 512)])
+def test_ternary_linear_parity_fp32(catq, d_out, d_in, M, g):
+    import torch
+    packed, alpha, xb = _case(d_out, d_in, M, g, 1)
+    y = _run(catq, packed, alpha, xb, g, torch.float32, ldx_pad=8, ldy_pad=3)
+    xo = f64(xb)
+    ref = ternary.ternary_linear(xo, packed, alpha, d_in, g)
+    got = host(y)
+    assert np.isnan(got[:, d_out:]).all()        # padding untouched
+    err = np.abs(got[:, :d_out] - ref)
+    bound = _bound(xo, packed, alpha, d_in, g, d_in // 128)
+    assert np.all(err <= bound), (float((err / bound).max()), d_out, d_in, M)
+
+
+def test_ternary_linear_parity_bf16_output(catq):
+    import torch
+    packed, alpha, xb = _case(96, 1536, 4, 128, 2)
+    y = _run(catq, packed, alpha, xb, 128, torch.bfloat16)
+    xo = f64(xb)
+    ref = ternary.ternary_linear(xo, packed, alpha, 1536)
+    bound = _bound(xo, packed, alpha, 1536, 128, 12) * (1 + 2.0 ** -8) + 2.0 ** -8 * np.abs(ref)
+    assert np.all(np.abs(host(y) - ref) <= bound)
+
+
+def test_ternary_linear_invalid_codes_and_zero_tokens(catq):
+    import torch
+    packed, alpha, xb = _case(32, 256, 2, 128, 3)
+    packed[5] = 0xFF                                 # a row of invalid codes -> 0
+    y = _run(catq, packed, alpha, xb, 128, torch.float32)
+    assert not torch.any(y[:, 5])
+    ref = ternary.ternary_linear(f64(xb), packed, alpha, 256)
+    assert np.all(np.abs(host(y) - ref) <= _bound(f64(xb), packed, alpha, 256, 128, 2))
+    e = _run(catq, packed, alpha, xb[:0], 128, torch.float32)     # M = 0: no-op
+    assert e.shape == (0, 32)
+
+
+def test_ternary_linear_deterministic(catq):
+    import torch
+    packed, alpha, xb = _case(512, 5120, 8, 128, 4)
+    a = _run(catq, packed, alpha, xb, 128, torch.float32)
+    b = _run(catq, packed, alpha, xb, 128, torch.float32)
+    assert torch.equal(a, b)
+
+
+def test_ternary_linear_on_finalized_block(catq):
+    """Deployment after calibration: the GPU's packed codes and scales of a
+    block's linears are bit-identical to the oracle's hard ternarisation of
+    the same factors, and the packed product on them matches the oracle's
+    product on its own codes."""
+    import torch
+    from paper_2606_26650_amd.block import DenseBlock
+    cfg = sg.small_dense(batch=1, seq=64, hidden=256, n_q=4, n_kv=2, head_dim=64, ffn=384)
+    W = sg.block_weights(cfg, 0)
+    fused = {"qkv": np.concatenate([W["Wq"], W["Wk"], W["Wv"]]), "o": W["Wo"],
+             "gu": np.concatenate([W["Wg"], W["Wu"]]), "d": W["Wd"]}
+    blk = DenseBlock(cfg, W)
+    facs = {}
+    for i, (name, L) in enumerate(blk.lin.items()):
+        facs[name] = sg.perturbed_factors(7, L.n_groups, extra=(i,))
+        L.set_factors(*facs[name])
+    bufs = blk.finalize(blk.finalize_buffers())
+    xb = sg.normal_bf16(5, "X", (3, 384))
+    for name, L in blk.lin.items():
+        d_out, d_in = fused[name].shape
+        hard = lmst.modulate_ternarize(f64(fused[name]), 128, *facs[name], lmst.HARD)
+        packed_ref = lmst.pack_ternary(hard["codes"])
+        np.testing.assert_array_equal(bufs[name]["packed"].cpu().numpy(), packed_ref, err_msg=name)
+        np.testing.assert_array_equal(bufs[name]["alpha"].cpu().numpy().astype(np.float64),
+                                      hard["alpha"], err_msg=name)
+        x = f64(xb[:, :d_in])
+        y = torch.empty(3, d_out, dtype=torch.float32, device="cuda")
+        catq.catq_ternary_linear(to_dev_bf16(np.ascontiguousarray(xb[:, :d_in])),
+                                 bufs[name]["packed"], bufs[name]["alpha"].view(d_out, -1), y)
+        torch.cuda.synchronize()
+        alpha_ref = hard["alpha"].reshape(d_out, -1)
+        ref = ternary.ternary_linear(x, packed_ref, alpha_ref, d_in)
+        bound = _bound(x, packed_ref, alpha_ref, d_in, 128, d_in // 128)
+        assert np.all(np.abs(host(y) - ref) <= bound), name
+        np.testing.assert_allclose(ref, x @ hard["W_fake"].T, rtol=1e-12, atol=1e-15)
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("d_out,d_in,M", [(34816, 5120, 1), (5120, 17408, 1), (7168, 5120, 8),
+                                          (34816, 5120, 16)])
+def test_ternary_linear_full_size_sampled(catq, d_out, d_in, M):
+    """Qwen3-14B-shaped layers (gate|up, down, q|k|v) at decode sizes, in the
+    launch configuration the benchmark times: sampled output rows against
+    the oracle (computed for those rows only)."""
+    import torch
+    rng = np.random.default_rng([9, d_out, d_in, M])
+    packed = rng.integers(0, 256, (d_out, d_in // 4), dtype=np.uint8)   # code 3 -> 0 included
+    alpha = rng.uniform(0.002, 0.05, (d_out, d_in // 128)).astype(np.float32)
+    xb = sg.normal_bf16(6, "X", (M, d_in))
+    y = _run(catq, packed, alpha, xb, 128, torch.float32)
+    rows = np.sort(np.concatenate([rng.choice(d_out, 61, replace=False), [0, d_out - 1]]))
+    xo = f64(xb)
+    ref = ternary.ternary_linear(xo, packed[rows], alpha[rows], d_in)
+    got = host(y)[:, rows]
+    bound = _bound(xo, packed[rows], alpha[rows], d_in, 128, d_in // 128)
+    assert np.all(np.abs(got - ref) <= bound)
