@@ -17,7 +17,8 @@ gradients) and the hard finalize go to a side stream and overlap the
 input-gradient chain (--no-overlap: one stream).
 
 Prints one JSON line.  ``value`` and ``ms_per_step`` come from the timed pass
-(the production two-stream schedule, no per-launch instrumentation).  A
+(the production schedule: two streams, no per-launch instrumentation; --graph
+replays the step captured as a HIP graph instead).  A
 kernel pass then repeats the same steps on one stream with a HIP event pair
 recorded by the library around each of its launches, on the launch stream:
 the per-kernel durations behind ``roofline`` come from there, so a kernel's
@@ -52,6 +53,9 @@ def parse():
     ap.add_argument("--no-overlap", action="store_true",
                     help="run the step on one stream (no side stream for the weight-gradient "
                          "halves and the finalize)")
+    ap.add_argument("--graph", action="store_true",
+                    help="replay the step captured as a HIP graph in the timed pass (measured "
+                         "slower than issuing the launches on this step: it is not launch-bound)")
     ap.add_argument("--ternary", type=int, default=0, metavar="M",
                     help="only time the packed-ternary decode layers of a Qwen3-14B-shaped "
                          "block at M tokens (deployment on the 2-bit storage)")
@@ -283,13 +287,20 @@ def main():
         blk.step(x, y_fp, mode=cq.SOFT, s=15.0, s_bwd=30.0, recompute_stats=True,
                  overlap=overlap, finalize=fin)
 
-    # timed pass: the production schedule, no per-launch instrumentation
+    # timed pass: the production schedule (two streams; optionally the step
+    # replayed as a HIP graph), no per-launch instrumentation
+    run = lambda: step(not args.no_overlap)
+    if args.graph:
+        from paper_2606_26650_amd.block import StepGraph
+        graph = StepGraph(blk, x, y_fp, mode=cq.SOFT, s=15.0, s_bwd=30.0, recompute_stats=True,
+                          overlap=not args.no_overlap, finalize=fin)
+        run = graph.replay
     for _ in range(args.warmup):
-        step(not args.no_overlap)
+        run()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        step(not args.no_overlap)
+        run()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     elapsed = t1 - t0
@@ -363,6 +374,8 @@ def main():
             "flops_per_launch": dom["flops"] / dom["n"],
             "traffic": counted_traffic(dom_tag),
         },
+        "schedule": ("two streams" if not args.no_overlap else "one stream") +
+                    (", step replayed as a HIP graph" if args.graph else ", launches issued per step"),
         "kernel_pass": {"ms_per_step": kernel_pass_ms, "streams": 1, "steps": args.steps,
                         "instrumented": "HIP event pair per launch"},
         "gemm_tflops_all": all_gemm_flops / (all_gemm_ms * 1e-3) / 1e12,

@@ -181,6 +181,7 @@ class DenseBlock:
         self.loss = torch.zeros(1, dtype=torch.float32, device=DEV)
         self.stats_ready = False
         self.side = None
+        self._events = {}
 
     def side_stream(self):
         """Second stream (default priority) for the weight-gradient halves and
@@ -188,6 +189,16 @@ class DenseBlock:
         if self.side is None:
             self.side = torch.cuda.Stream(device=DEV)
         return self.side
+
+    def order(self, key, before, after):
+        """Make stream ``after`` wait for the work issued so far on ``before``,
+        through an event kept per ``key`` (created on first use, then
+        re-recorded: a step captured into a graph creates no events)."""
+        ev = self._events.get(key)
+        if ev is None:
+            ev = self._events[key] = torch.cuda.Event()
+        ev.record(before)
+        after.wait_event(ev)
 
     # ------------------------------------------------------------------ LM+ST
     def params(self, mode, s=15.0, s_bwd=30.0, strides=(1, 1, 1)):
@@ -254,9 +265,7 @@ class DenseBlock:
                                       L.d_alpha, L.d_delta, p, L.g_mu, L.g_alpha, L.g_delta, ws,
                                       dX=dX)
                 return
-            ready = torch.cuda.Event()
-            ready.record(main)
-            side.wait_event(ready)
+            self.order(name, main, side)
             with torch.cuda.stream(side):
                 catq_fakeq_linear_bwd(dY, X, L.W_fake, M, L.d_out, L.d_in, L.W, L.stats, L.d_mu,
                                       L.d_alpha, L.d_delta, p, L.g_mu, L.g_alpha, L.g_delta, ws)
@@ -274,7 +283,7 @@ class DenseBlock:
         lbwd("qkv", self.dqkv, self.xn1, self.dxn1)
         catq_aux_rmsnorm_bwd(x, self.rstd1, self.dxn1, self.dx, dres=self.dh1)
         if side is not None and join:
-            main.wait_stream(side)
+            self.order("join", side, main)
 
     # ------------------------------------------------------------------- step
     def step(self, x, y_fp, mode=SOFT, s=15.0, s_bwd=30.0, recompute_stats=False, overlap=True,
@@ -288,16 +297,15 @@ class DenseBlock:
         if finalize is not None:
             main = torch.cuda.current_stream()
             side = self.side_stream() if overlap else main
-            ready = torch.cuda.Event()
-            ready.record(main)
-            side.wait_event(ready)
+            if side is not main:
+                self.order("finalize", main, side)
             with torch.cuda.stream(side):
                 self.finalize(finalize)
         self.forward(x)
         catq_block_recon_loss(self.y, y_fp, self.loss, self.dy, self.loss_ws)
         self.backward(x, p, overlap)
         if finalize is not None and overlap:
-            torch.cuda.current_stream().wait_stream(self.side_stream())
+            self.order("finalize_join", self.side_stream(), torch.cuda.current_stream())
         return self.loss
 
     def finalize_buffers(self):
@@ -409,9 +417,11 @@ class MoEBlock:
         self.loss = torch.zeros(1, dtype=torch.float32, device=DEV)
         self.stats_ready = False
         self.side = None
+        self._events = {}
 
     params = DenseBlock.params
     side_stream = DenseBlock.side_stream
+    order = DenseBlock.order
     modulate_all = DenseBlock.modulate_all
     new_output = DenseBlock.new_output
     finalize_buffers = DenseBlock.finalize_buffers
@@ -460,9 +470,7 @@ class MoEBlock:
                                       L.d_alpha, L.d_delta, p, L.g_mu, L.g_alpha, L.g_delta, ws,
                                       dX=dX, n_experts=E_, row_offsets=offs)
                 return
-            ready = torch.cuda.Event()
-            ready.record(main)
-            side.wait_event(ready)
+            self.order(name, main, side)
             with torch.cuda.stream(side):
                 catq_fakeq_linear_bwd(dY, X, L.W_fake, rows, L.d_out, L.d_in, L.W, L.stats, L.d_mu,
                                       L.d_alpha, L.d_delta, p, L.g_mu, L.g_alpha, L.g_delta, ws,
@@ -484,7 +492,7 @@ class MoEBlock:
         lbwd("qkv", self.dqkv, self.xn1, self.dxn1, M)
         catq_aux_rmsnorm_bwd(x, self.rstd1, self.dxn1, self.dx, dres=self.dh1)
         if side is not None and join:
-            main.wait_stream(side)
+            self.order("join", side, main)
 
     step = DenseBlock.step
 
@@ -503,6 +511,27 @@ class MoEBlock:
             per = arr.reshape(E, 2 * F, -1)
             return {"Wg": per[:, :F].reshape(E * F, -1), "Wu": per[:, F:].reshape(E * F, -1)}
         return {"Wd": arr}
+
+
+class StepGraph:
+    """One calibration step (both streams) captured as a HIP graph and
+    replayed: the step's ~35 launches then cost one graph launch.  Inputs
+    and outputs are the captured buffers: change them in place between
+    replays (the factors are updated in place by the optimiser).  The step
+    is run once eagerly first, so the side stream, the events and the
+    cached statistics exist before capture."""
+
+    def __init__(self, blk, x, y_fp, **step_kw):
+        blk.step(x, y_fp, **step_kw)
+        torch.cuda.synchronize()
+        self.graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(self.graph):
+            self.loss = blk.step(x, y_fp, **step_kw)
+        torch.cuda.synchronize()
+
+    def replay(self):
+        self.graph.replay()
+        return self.loss
 
 
 def _split_rows(arr, sizes, names):

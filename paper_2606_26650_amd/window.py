@@ -113,11 +113,11 @@ class Window:
         p = self.params(mode, s, s_bwd)
         self.modulate_all(p, recompute_stats)
         main = torch.cuda.current_stream()
+        b0 = self.blocks[0]
         if finalize is not None:
-            side = self.blocks[0].side_stream() if overlap else main
-            ready = torch.cuda.Event()
-            ready.record(main)
-            side.wait_event(ready)
+            side = b0.side_stream() if overlap else main
+            if side is not main:
+                b0.order("window_finalize", main, side)
             with torch.cuda.stream(side):
                 self.finalize(finalize)
         last = self.blocks[-1]
@@ -129,7 +129,7 @@ class Window:
             dy = None if i == n - 1 else self.blocks[i + 1].dx
             self.blocks[i].backward(ins[i], p, overlap, dy=dy, join=(i == 0))
         if finalize is not None and overlap:
-            main.wait_stream(self.blocks[0].side_stream())
+            b0.order("window_finalize_join", b0.side_stream(), main)
         return last.loss
 
 
