@@ -19,6 +19,8 @@ from __future__ import annotations
 
 import numpy as np
 
+from . import actquant
+
 EPS = 1e-6
 LINEARS = ("Wq", "Wk", "Wv", "Wo", "Wg", "Wu", "Wd")
 
@@ -111,12 +113,24 @@ def causal_attention_bwd(q, k, v, P, dO):
 
 # ---------------------------------------------------------- attention half
 
-def attn_forward(x, W, cfg):
-    """x [M][h] -> h1 = x + o_proj(attention(...)).  W maps names to [d_out][d_in]."""
+def _aq(x, group):
+    """W1.58A8 activation fake quantization of a stored (bf16) activation:
+    the quantizer of oracle/actquant.py applied to the bf16 value."""
+    x32 = np.asarray(x, np.float64).astype(np.float32)
+    return actquant.quantize(actquant.bf16_round(x32), group)[0]
+
+
+def attn_forward(x, W, cfg, a8=False):
+    """x [M][h] -> h1 = x + o_proj(attention(...)).  W maps names to [d_out][d_in].
+    a8: the inputs of q|k|v and o, and Q, K, V of the attention products, are
+    fake-quantized to 8 bits (per token; per token and head for Q, K, V) and
+    the cache holds the quantized values (the backward is straight-through)."""
     B, S = cfg.batch, cfg.seq
     Hq, Hkv, hd = cfg.n_q, cfg.n_kv, cfg.head_dim
     c = {"x": x}
     xn1, r1 = rmsnorm(x)
+    if a8:
+        xn1 = _aq(xn1, xn1.shape[-1])
     c.update(xn1=xn1, r1=r1)
     q = (xn1 @ W["Wq"].T).reshape(B, S, Hq, hd)
     k = (xn1 @ W["Wk"].T).reshape(B, S, Hkv, hd)
@@ -129,10 +143,15 @@ def attn_forward(x, W, cfg):
     cos, sin = rope_tables(S, hd, cfg.rope_theta)
     c.update(cos=cos, sin=sin, q_n=q, k_n=k)
     qr, kr = rope(q, cos, sin), rope(k, cos, sin)
+    if a8:
+        qr, kr, v = _aq(qr, hd), _aq(kr, hd), _aq(v, hd)
+        c["v"] = v
     c.update(qr=qr, kr=kr)
     O, P = causal_attention(qr, kr, v)
     c["P"] = P
     attn = O.reshape(B * S, Hq * hd)
+    if a8:
+        attn = _aq(attn, attn.shape[-1])
     c["attn"] = attn
     h1 = x + attn @ W["Wo"].T
     return h1, c
@@ -163,11 +182,15 @@ def attn_backward(dh1, c, W, cfg):
 
 # ---------------------------------------------------------------- MLP half
 
-def mlp_forward(h1, W):
+def mlp_forward(h1, W, a8=False):
     xn2, r2 = rmsnorm(h1)
+    if a8:
+        xn2 = _aq(xn2, xn2.shape[-1])
     gt = xn2 @ W["Wg"].T
     up = xn2 @ W["Wu"].T
     a = silu(gt) * up
+    if a8:
+        a = _aq(a, a.shape[-1])
     y = h1 + a @ W["Wd"].T
     return y, dict(h1=h1, xn2=xn2, r2=r2, gt=gt, up=up, a=a)
 
@@ -187,9 +210,9 @@ def mlp_backward(dy, c, W):
 
 # ------------------------------------------------------------------ block
 
-def block_forward(x, W, cfg):
-    h1, ca = attn_forward(x, W, cfg)
-    y, cm = mlp_forward(h1, W)
+def block_forward(x, W, cfg, a8=False):
+    h1, ca = attn_forward(x, W, cfg, a8)
+    y, cm = mlp_forward(h1, W, a8)
     return y, (ca, cm)
 
 

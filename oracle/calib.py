@@ -74,14 +74,16 @@ def factor_grads_all(dW, Wd, factors, g, mode, s, s_bwd, strides=(1, 1, 1), delt
     return out
 
 
-def dense_step(x, Wd, factors, cfg, mode, s=None, s_bwd=0.0, g=128, y_fp=None):
+def dense_step(x, Wd, factors, cfg, mode, s=None, s_bwd=0.0, g=128, y_fp=None, a8=False):
     """LM+ST of all seven linears -> block forward with alpha*T -> loss
     against the full-precision block output on the same x -> backward to the
-    input and to every linear's factors."""
+    input and to every linear's factors.  a8: the quantized block also
+    fake-quantizes its activations (W1.58A8); the target stays the
+    full-precision block."""
     Wf = fake_weights(Wd, factors, g, mode, s)
     if y_fp is None:
         y_fp, _ = block.block_forward(x, Wd, cfg)
-    y_q, cache = block.block_forward(x, Wf, cfg)
+    y_q, cache = block.block_forward(x, Wf, cfg, a8)
     loss, dy = block.recon_loss(y_q, y_fp)
     dx, dW = block.block_backward(dy, cache, Wf, cfg)
     fg = factor_grads_all(dW, Wd, factors, g, mode, s, s_bwd)
