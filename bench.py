@@ -59,6 +59,8 @@ def parse():
     ap.add_argument("--ternary", type=int, default=0, metavar="M",
                     help="only time the packed-ternary decode layers of a Qwen3-14B-shaped "
                          "block at M tokens (deployment on the 2-bit storage)")
+    ap.add_argument("--a8", action="store_true",
+                    help="the W1.58A8 setting: activations fake-quantized to 8 bits in the step")
     ap.add_argument("--window", type=int, default=1,
                     help="calibrate this many consecutive blocks jointly (sliding-window "
                          "reconstruction; 1 = the single-block step)")
@@ -274,10 +276,11 @@ def main():
     xb = sg.activations(cfg, 0)
     if args.window > 1:
         from paper_2606_26650_amd.window import Window
-        blk = Window([DenseBlock(cfg, W)] +
-                     [DenseBlock(cfg, sg.block_weights(cfg, i)) for i in range(1, args.window)])
+        blk = Window([DenseBlock(cfg, W, a8=args.a8)] +
+                     [DenseBlock(cfg, sg.block_weights(cfg, i), a8=args.a8)
+                      for i in range(1, args.window)])
     else:
-        blk = DenseBlock(cfg, W)
+        blk = DenseBlock(cfg, W, a8=args.a8)
     x = bf16_tensor(xb)
     y_fp = blk.new_output()
     blk.target(x, y_fp)
@@ -359,7 +362,8 @@ def main():
         "config": {"workload": ("qwen3-1.7b-shaped decoder block" if args.window == 1 else
                                 f"window of {args.window} qwen3-1.7b-shaped decoder blocks") +
                                ", 4 x 2048 tokens, one CAT-Q calibration step (LM+ST s=15, fwd, "
-                               "loss, bwd to factors, ternarise+pack)",
+                               "loss, bwd to factors, ternarise+pack)" +
+                               (", W1.58A8 (8-bit activations)" if args.a8 else ""),
                    "hidden": cfg.hidden, "heads": [cfg.n_q, cfg.n_kv, cfg.head_dim],
                    "ffn": cfg.ffn, "tokens": cfg.tokens, "group_size": 128,
                    "weights": cfg.n_weights()},
@@ -386,7 +390,7 @@ def main():
         "lmst_bwd_gbs": lmb["bytes"] / (lmb["ms"] * 1e-3) / 1e9 if lmb["ms"] else None,
         "loss": loss,
     }
-    if not args.no_cpu_baseline and args.window == 1:
+    if not args.no_cpu_baseline and args.window == 1 and not args.a8:
         out["cpu_baseline"] = cpu_baseline(cfg, W, xb)
     if args.breakdown:
         shp = {}

@@ -254,12 +254,26 @@ catq_status catq_aux_rmsnorm_bwd(const void* x, catq_dtype x_dtype, const float*
                                  const void* dy, const void* dres, int64_t rows, int64_t n,
                                  void* dx, hipStream_t stream);
 
+/* W1.58A8 activation fake quantization (Sec. 3: all intermediate
+ * activations but the softmax output are quantized to 8 bits; the quantizer
+ * is not specified -- this is symmetric absmax per group): for each group of
+ * `group` consecutive values of a row, s = max|x|/127, q = round-half-even
+ * (x/s) clamped to [-127, 127] (0 when s = 0), y = bf16(q*s), all in IEEE
+ * fp32.  x [rows][n] of x_dtype (bf16 or fp32), y bf16 [rows][n]; y may be x
+ * when x is bf16.  group divides n and is a multiple of 8.  rows = 0 is a
+ * no-op.  The backward is straight-through (no call needed). */
+catq_status catq_aux_act_quant(const void* x, catq_dtype x_dtype, int64_t rows, int64_t n,
+                               int64_t group, void* y, hipStream_t stream);
+
 /* Attention geometry for the q/k/v buffer produced by the fused q|k|v linear. */
 typedef struct {
   int32_t batch, seq, n_q, n_kv, head_dim;
   int32_t qk_norm;     /* per-head RMSNorm on q and k before the rotary embedding */
   float rope_theta;    /* rotary base; pairs (i, i + d/2) rotate by pos*theta^(-2i/d) */
   float eps;           /* RMSNorm epsilon of the q/k norms */
+  int32_t act_quant;   /* 1: Q, K, V of the attention products fake-quantized to 8 bits
+                          per (token, head) as in catq_aux_act_quant (W1.58A8; the softmax
+                          output is not); needs head_dim 64 or 128.  0: off */
 } catq_attn_desc;
 
 /*

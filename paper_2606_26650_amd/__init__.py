@@ -15,7 +15,7 @@ from ._lib import (BF16, F32, HARD, IDENTITY, SOFT, WS_LINEAR_BWD, WS_LOSS, Attn
 __all__ = [
     "catq_modulate_ternarize", "catq_fakeq_linear_fwd", "catq_fakeq_linear_bwd",
     "catq_block_recon_loss", "catq_pack_ternary", "catq_ternary_linear", "catq_workspace_size",
-    "catq_aux_rmsnorm_fwd", "catq_aux_rmsnorm_bwd", "catq_aux_attention_fwd",
+    "catq_aux_act_quant", "catq_aux_rmsnorm_fwd", "catq_aux_rmsnorm_bwd", "catq_aux_attention_fwd",
     "catq_aux_attention_bwd", "catq_attn_saved_bytes", "catq_attn_bwd_workspace_bytes",
     "catq_aux_swiglu_fwd", "catq_aux_swiglu_bwd", "catq_aux_moe_route",
     "catq_aux_moe_route_workspace_bytes", "catq_aux_moe_gather", "catq_aux_moe_combine",
@@ -65,12 +65,13 @@ def lmst_params(group_size=128, mode=SOFT, delta0=0.5, s=15.0, s_bwd=30.0, strid
     return p
 
 
-def attn_desc(batch, seq, n_q, n_kv, head_dim, qk_norm, rope_theta, eps=1e-6):
+def attn_desc(batch, seq, n_q, n_kv, head_dim, qk_norm, rope_theta, eps=1e-6, act_quant=False):
     a = AttnDesc()
     a.batch, a.seq, a.n_q, a.n_kv, a.head_dim = batch, seq, n_q, n_kv, head_dim
     a.qk_norm = int(bool(qk_norm))
     a.rope_theta = rope_theta
     a.eps = eps
+    a.act_quant = int(bool(act_quant))
     return a
 
 
@@ -136,6 +137,15 @@ def catq_ternary_linear(X, packed, alpha, Y, g=128, stream=None):
 
 def catq_workspace_size(which, M, N, K, n_experts=1):
     return int(lib.catq_workspace_size(which, M, N, K, n_experts))
+
+
+def catq_aux_act_quant(x, y, group=None, stream=None):
+    """8-bit absmax fake quantization of each group of `group` consecutive
+    values of every row of x (default: the whole row) into bf16 y (may be x)."""
+    n = x.shape[-1]
+    st = lib.catq_aux_act_quant(_ptr(x), _dt(x), x.numel() // n if n else 0, n,
+                                group or n, _ptr(y), _stream(stream))
+    _lib.check("catq_aux_act_quant", st)
 
 
 def catq_aux_rmsnorm_fwd(x, y, rstd, eps=1e-6, stream=None):

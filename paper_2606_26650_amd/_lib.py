@@ -27,7 +27,7 @@ class LmstParams(C.Structure):
 class AttnDesc(C.Structure):
     _fields_ = [("batch", C.c_int32), ("seq", C.c_int32), ("n_q", C.c_int32),
                 ("n_kv", C.c_int32), ("head_dim", C.c_int32), ("qk_norm", C.c_int32),
-                ("rope_theta", C.c_float), ("eps", C.c_float)]
+                ("rope_theta", C.c_float), ("eps", C.c_float), ("act_quant", C.c_int32)]
 
 
 class TraceRec(C.Structure):
@@ -56,6 +56,7 @@ SIGNATURES = {
     "catq_workspace_size": [I32, I64, I64, I64, I32],
     "catq_status_string": [I32],
     "catq_last_error_message": [],
+    "catq_aux_act_quant": [P, I32, I64, I64, I64, P, P],
     "catq_aux_rmsnorm_fwd": [P, I32, I64, I64, F, P, P, P],
     "catq_aux_rmsnorm_bwd": [P, I32, P, P, P, I64, I64, P, P],
     "catq_attn_saved_bytes": [PA],

@@ -19,7 +19,7 @@ from __future__ import annotations
 import numpy as np
 import torch
 
-from . import (BF16, HARD, IDENTITY, SOFT, attn_desc, catq_aux_attention_bwd,
+from . import (BF16, HARD, IDENTITY, SOFT, attn_desc, catq_aux_act_quant, catq_aux_attention_bwd,
                catq_aux_attention_fwd, catq_aux_moe_combine, catq_aux_moe_combine_bwd,
                catq_aux_moe_gather, catq_aux_moe_route, catq_aux_moe_route_workspace_bytes,
                catq_aux_moe_scatter_add, catq_aux_rmsnorm_bwd, catq_aux_rmsnorm_fwd,
@@ -134,10 +134,16 @@ class DenseBlock:
     """Pre-norm decoder block (RMSNorm, fused q|k|v, QK-norm, RoPE, causal GQA
     attention, o, residual, RMSNorm, fused gate|up, SwiGLU, down, residual)."""
 
-    def __init__(self, cfg, weights: dict, g: int = 128):
+    def __init__(self, cfg, weights: dict, g: int = 128, a8: bool = False):
+        """a8: the W1.58A8 setting -- the inputs of the four linears and Q, K,
+        V of the attention products are fake-quantized to 8 bits in the
+        step's forward (straight-through backward); the full-precision
+        target is not."""
         self.cfg = cfg
         c = cfg
         hd, h = c.head_dim, c.hidden
+        self.a8 = a8
+        self._act = a8
         self.Nqkv = (c.n_q + 2 * c.n_kv) * hd
         self.M = c.batch * c.seq
         self.g = g
@@ -152,10 +158,14 @@ class DenseBlock:
         del dev_w
         M = self.M
         self.desc = attn_desc(c.batch, c.seq, c.n_q, c.n_kv, hd, c.qk_norm, c.rope_theta)
+        self.desc_a8 = attn_desc(c.batch, c.seq, c.n_q, c.n_kv, hd, c.qk_norm, c.rope_theta,
+                                 act_quant=True) if a8 else None
+        self.fwd_desc = self.desc
         # activations
         self.xn1, self.rstd1 = empty((M, h)), empty((M,), torch.float32)
         self.qkv = empty((M, self.Nqkv))
         self.attn = empty((M, c.n_q * hd))
+        self.attn_q = empty((M, c.n_q * hd)) if a8 else None   # quantized o input
         self.h1 = empty((M, h), torch.float32)      # residual stream kept in fp32
         self.xn2, self.rstd2 = empty((M, h)), empty((M,), torch.float32)
         self.gu = empty((M, 2 * c.ffn))
@@ -221,16 +231,28 @@ class DenseBlock:
         c, M = self.cfg, self.M
         h = c.hidden
         y = self.y if out is None else out
+        act = self._act
         catq_aux_rmsnorm_fwd(x, self.xn1, self.rstd1)
+        if act:
+            catq_aux_act_quant(self.xn1, self.xn1)
         L = self.lin["qkv"]
         catq_fakeq_linear_fwd(self.xn1, L.W_fake, self.qkv, M, self.Nqkv, h)
-        catq_aux_attention_fwd(self.desc, self.qkv, self.attn, self.saved)
+        self.fwd_desc = self.desc_a8 if act else self.desc
+        catq_aux_attention_fwd(self.fwd_desc, self.qkv, self.attn, self.saved)
+        self.o_in = self.attn
+        if act:
+            catq_aux_act_quant(self.attn, self.attn_q)
+            self.o_in = self.attn_q
         L = self.lin["o"]
-        catq_fakeq_linear_fwd(self.attn, L.W_fake, self.h1, M, h, c.n_q * c.head_dim, residual=x)
+        catq_fakeq_linear_fwd(self.o_in, L.W_fake, self.h1, M, h, c.n_q * c.head_dim, residual=x)
         catq_aux_rmsnorm_fwd(self.h1, self.xn2, self.rstd2)
+        if act:
+            catq_aux_act_quant(self.xn2, self.xn2)
         L = self.lin["gu"]
         catq_fakeq_linear_fwd(self.xn2, L.W_fake, self.gu, M, 2 * c.ffn, h)
         catq_aux_swiglu_fwd(self.gu, self.a)
+        if act:
+            catq_aux_act_quant(self.a, self.a)
         L = self.lin["d"]
         catq_fakeq_linear_fwd(self.a, L.W_fake, y, M, h, c.ffn, residual=self.h1)
         return y
@@ -239,9 +261,14 @@ class DenseBlock:
         return empty((self.M, self.cfg.hidden), torch.float32)
 
     def target(self, x, out):
-        """Full-precision block output on the same input (IDENTITY branch)."""
+        """Full-precision block output on the same input (IDENTITY branch,
+        activations not quantized)."""
         self.modulate_all(self.params(IDENTITY))
-        return self.forward(x, out)
+        self._act = False
+        try:
+            return self.forward(x, out)
+        finally:
+            self._act = self.a8
 
     # --------------------------------------------------------------- backward
     def backward(self, x, p, overlap=True, dy=None, join=True):
@@ -277,9 +304,9 @@ class DenseBlock:
         catq_aux_swiglu_bwd(self.gu, self.da, self.dgu)
         lbwd("gu", self.dgu, self.xn2, self.dxn2)
         catq_aux_rmsnorm_bwd(self.h1, self.rstd2, self.dxn2, self.dh1, dres=dy)
-        lbwd("o", self.dh1, self.attn, self.dattn)
-        catq_aux_attention_bwd(self.desc, self.qkv, self.attn, self.saved, self.dattn, self.dqkv,
-                               self.attn_ws)
+        lbwd("o", self.dh1, self.o_in, self.dattn)
+        catq_aux_attention_bwd(self.fwd_desc, self.qkv, self.attn, self.saved, self.dattn,
+                               self.dqkv, self.attn_ws)
         lbwd("qkv", self.dqkv, self.xn1, self.dxn1)
         catq_aux_rmsnorm_bwd(x, self.rstd1, self.dxn1, self.dx, dres=self.dh1)
         if side is not None and join:

@@ -91,6 +91,8 @@ static catq_status check_desc(const catq_attn_desc* a) {
   CATQ_REQUIRE(a->seq % 8 == 0 && a->seq <= 8192, CATQ_ERR_SHAPE,
                "seq must be a multiple of 8 and <= 8192");
   CATQ_REQUIRE(a->rope_theta > 1.0f && a->eps >= 0.0f, CATQ_ERR_VALUE, "bad rope_theta or eps");
+  CATQ_REQUIRE(a->act_quant == 0 || (a->act_quant == 1 && a->head_dim <= 128), CATQ_ERR_VALUE,
+               "act_quant must be 0 or 1, and 1 needs head_dim 64 or 128 (fused attention)");
   return CATQ_OK;
 }
 
@@ -160,13 +162,34 @@ __global__ __launch_bounds__(256) void qk_prep_fwd_kernel(const bf16* qkv, int64
   }
 }
 
+// W1.58A8 fake quantization of one (token, head) vector held by LPH lanes
+// (16 values each, as stored: bf16): s = max|x|/127, x = bf16(rne(x/s)*s),
+// clamped to +-127 codes; the same fp32 steps as catq_aux_act_quant.
+__device__ __forceinline__ void head_act_quant(float (&x1)[8], float (&x2)[8], int LPH) {
+  float m = 0.f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    x1[j] = (float)(bf16)x1[j];
+    x2[j] = (float)(bf16)x2[j];
+    m = fmaxf(m, fmaxf(fabsf(x1[j]), fabsf(x2[j])));
+  }
+  for (int k = LPH >> 1; k >= 1; k >>= 1) m = fmaxf(m, __shfl_xor(m, k, 64));
+  const float s = m / 127.0f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    x1[j] = s > 0.f ? fminf(fmaxf(rintf(x1[j] / s), -127.f), 127.f) * s : 0.f;
+    x2[j] = s > 0.f ? fminf(fmaxf(rintf(x2[j] / s), -127.f), 127.f) * s : 0.f;
+  }
+}
+
 // Vectorised q/k preparation for head sizes with half % 8 == 0 and half/8 a
 // power of two: LPH = half/8 lanes per (token, head), each lane owning
 // elements i0..i0+7 of both rotation halves (two 16-byte loads and stores).
+// a8: the stored Q, K and V heads are fake-quantized (W1.58A8).
 __global__ __launch_bounds__(256) void qk_prep_fwd_vec_kernel(
     const bf16* qkv, int64_t B, int64_t S, int Hq, int Hkv, int d, int ld, int lph_log2,
     int qk_norm, float eps, const float* cs, const float* sn, bf16* Qh, bf16* Kh, bf16* Vh,
-    float* rstd) {
+    float* rstd, int a8) {
   const int H = Hq + Hkv;
   const int Hall = Vh ? H + Hkv : H;
   const int LPH = 1 << lph_log2;
@@ -182,6 +205,15 @@ __global__ __launch_bounds__(256) void qk_prep_fwd_vec_kernel(
   const bf16* src = qkv + t * ld + (int64_t)h * d;
   if (h >= H) {  // v head: head-major copy
     bf16* dst = Vh + ((b * Hkv + (h - H)) * S + s) * d;
+    if (a8) {
+      float v1[8], v2[8];
+      load8<bf16>(src + i0, v1);
+      load8<bf16>(src + half + i0, v2);
+      head_act_quant(v1, v2, LPH);
+      store8<bf16>(dst + i0, v1);
+      store8<bf16>(dst + half + i0, v2);
+      return;
+    }
     *reinterpret_cast<u32x4*>(dst + i0) = *reinterpret_cast<const u32x4*>(src + i0);
     *reinterpret_cast<u32x4*>(dst + half + i0) = *reinterpret_cast<const u32x4*>(src + half + i0);
     return;
@@ -209,6 +241,7 @@ __global__ __launch_bounds__(256) void qk_prep_fwd_vec_kernel(
     o2[j] = bb * c[j] + a * sv[j];
   }
   bf16* dst = h < Hq ? Qh + ((b * Hq + h) * S + s) * d : Kh + ((b * Hkv + (h - Hq)) * S + s) * d;
+  if (a8) head_act_quant(o1, o2, LPH);
   store8<bf16>(dst + i0, o1);
   store8<bf16>(dst + half + i0, o2);
 }
@@ -542,8 +575,11 @@ extern "C" catq_status catq_aux_attention_fwd(const catq_attn_desc* a, const voi
                 hipLaunchKernelGGL(qk_prep_fwd_vec_kernel, dim3((unsigned)((nt + 255) / 256)),
                                    dim3(256), 0, stream, (const bf16*)qkv, L.B, L.S, (int)L.Hq,
                                    (int)L.Hkv, (int)L.d, (int)L.ld, lph, a->qk_norm, a->eps, cs,
-                                   sn, Qh, Kh, Vh, rstd));
+                                   sn, Qh, Kh, Vh, rstd, a->act_quant));
   } else {
+    CATQ_REQUIRE(!a->act_quant, CATQ_ERR_VALUE,
+                 "activation quantization needs the vectorised q/k path (head_dim 64 or 128, "
+                 "16-byte aligned rows)");
     hipLaunchKernelGGL(qk_prep_fwd_kernel, dim3((unsigned)((nw + 3) / 4)), dim3(256), 0, stream,
                        (const bf16*)qkv, L.B, L.S, (int)L.Hq, (int)L.Hkv, (int)L.d, (int)L.ld,
                        a->qk_norm, a->eps, cs, sn, Qh, Kh, Vh, rstd);

@@ -22,6 +22,55 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
   return s;
 }
 
+template <int NT>
+__device__ __forceinline__ float block_max(float v, float* red) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m, 64));
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  if (l == 0) red[w] = v;
+  __syncthreads();
+  float r = 0.f;
+#pragma unroll
+  for (int i = 0; i < NT / 64; ++i) r = fmaxf(r, red[i]);
+  __syncthreads();
+  return r;
+}
+
+// -------------------------------------------------- activation quantization
+// Symmetric 8-bit absmax fake quantization (the W1.58A8 setting) of each
+// group of `group` consecutive values of a row: s = max|x| / 127,
+// q = round-half-even(x / s) clamped to [-127, 127] (0 when s = 0),
+// y = bf16(q * s); every step in IEEE fp32.  One workgroup per (row, group):
+// a pass for the maximum, a second (from L2) for the codes.  y may alias x.
+template <typename XT>
+__global__ __launch_bounds__(256) void act_quant_kernel(const XT* x, int64_t n, int64_t group,
+                                                        bf16* y) {
+  __shared__ float red[4];
+  const int64_t off = (int64_t)blockIdx.x * n + (int64_t)blockIdx.y * group;
+  const XT* xr = x + off;
+  bf16* yr = y + off;
+  const int64_t nc = group / 8;
+  float m = 0.f;
+  for (int64_t c = threadIdx.x; c < nc; c += 256) {
+    float v[8];
+    load8<XT>(xr + c * 8, v);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) m = fmaxf(m, fabsf(v[j]));
+  }
+  m = block_max<256>(m, red);
+  const float s = m / 127.0f;
+  for (int64_t c = threadIdx.x; c < nc; c += 256) {
+    float v[8];
+    load8<XT>(xr + c * 8, v);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float q = s > 0.f ? fminf(fmaxf(rintf(v[j] / s), -127.f), 127.f) : 0.f;
+      v[j] = q * s;
+    }
+    store8<bf16>(yr + c * 8, v);
+  }
+}
+
 // ---------------------------------------------------------------- RMSNorm
 
 template <typename XT>
@@ -344,6 +393,34 @@ extern "C" catq_status catq_aux_rmsnorm_bwd(const void* x, catq_dtype x_dtype, c
                                    stream, (const float*)x, rstd, (const bf16*)dy,
                                    (const bf16*)dres, n, (bf16*)dx));
   CATQ_CHECK_LAUNCH("rmsnorm bwd");
+  return CATQ_OK;
+}
+
+extern "C" catq_status catq_aux_act_quant(const void* x, catq_dtype x_dtype, int64_t rows,
+                                          int64_t n, int64_t group, void* y,
+                                          hipStream_t stream) {
+  clear_error();
+  CATQ_REQUIRE(rows >= 0, CATQ_ERR_SHAPE, "rows must be >= 0");
+  if (rows == 0) return CATQ_OK;
+  CATQ_REQUIRE(x && y, CATQ_ERR_NULL, "NULL argument");
+  CATQ_REQUIRE(dtype_ok(x_dtype), CATQ_ERR_DTYPE, "x must be bf16 or fp32");
+  CATQ_REQUIRE(n > 0 && group > 0 && n % group == 0 && group % 8 == 0, CATQ_ERR_SHAPE,
+               "group must be a multiple of 8 dividing n");
+  CATQ_REQUIRE(rows <= INT32_MAX && n / group <= 65535, CATQ_ERR_SHAPE, "too many rows or groups");
+  CATQ_REQUIRE(aligned16(x) && aligned16(y), CATQ_ERR_ALIGN, "misaligned");
+  CATQ_REQUIRE(x_dtype == CATQ_BF16 || x != y, CATQ_ERR_VALUE,
+               "an fp32 input cannot be quantized in place (y is bf16)");
+  const dim3 grid((unsigned)rows, (unsigned)(n / group));
+  const double bytes = (double)rows * (double)n * (2.0 * dtype_size(x_dtype) + 2.0);
+  if (x_dtype == CATQ_BF16)
+    CATQ_TRACED(stream, "act_quant_kernel<bf16>", 0.0, bytes, rows, n, group,
+                hipLaunchKernelGGL(act_quant_kernel<bf16>, grid, dim3(256), 0, stream,
+                                   (const bf16*)x, n, group, (bf16*)y));
+  else
+    CATQ_TRACED(stream, "act_quant_kernel<float>", 0.0, bytes, rows, n, group,
+                hipLaunchKernelGGL(act_quant_kernel<float>, grid, dim3(256), 0, stream,
+                                   (const float*)x, n, group, (bf16*)y));
+  CATQ_CHECK_LAUNCH("act quant");
   return CATQ_OK;
 }
 

@@ -176,3 +176,20 @@ def test_ternary_linear_validation(cq):
     assert call(X=FAKE + 8) == 5 and call(A=FAKE + 4) == 5 and call(P=FAKE + 4) == 5
     assert call(Y=FAKE + 2) == 5
     assert call(d_out=0) == 2
+
+
+def test_act_quant_validation(cq):
+    L = cq.lib
+    # (x, dtype, rows, n, group, y, stream)
+    assert L.catq_aux_act_quant(None, 1, 0, 64, 64, None, None) == 0      # rows = 0: no-op
+    assert L.catq_aux_act_quant(FAKE, 1, 4, 64, 24, FAKE, None) == 2      # group does not divide n
+    assert L.catq_aux_act_quant(FAKE, 1, 4, 60, 60, FAKE, None) == 2      # group % 8
+    assert L.catq_aux_act_quant(FAKE, 3, 4, 64, 64, FAKE, None) == 3
+    assert L.catq_aux_act_quant(FAKE + 8, 1, 4, 64, 64, FAKE, None) == 5
+    assert L.catq_aux_act_quant(FAKE, 0, 4, 64, 64, FAKE, None) == 4      # fp32 in place
+    assert L.catq_aux_act_quant(None, 1, 4, 64, 64, FAKE, None) == 1
+    d = cq.attn_desc(1, 16, 2, 1, 256, True, 1e6, act_quant=True)       # needs fused attention
+    assert L.catq_aux_attention_fwd(C.byref(d), FAKE, FAKE, FAKE, 1 << 30, None) == 4
+    d = cq.attn_desc(1, 16, 2, 1, 64, True, 1e6)
+    d.act_quant = 2
+    assert L.catq_aux_attention_fwd(C.byref(d), FAKE, FAKE, FAKE, 1 << 30, None) == 4
