@@ -230,6 +230,26 @@ catq_status catq_ternary_linear(const void* X, int64_t M, int64_t ldx, const uin
                                 const float* alpha, int64_t d_out, int64_t d_in, int32_t g,
                                 void* Y, catq_dtype y_dtype, int64_t ldy, hipStream_t stream);
 
+/* Fused variants for the SwiGLU MLP of a decoder block (a4 and a8 with the
+ * SwiGLU of a5 / a7 in the GEMM epilogue; same results as the unfused calls).
+ *
+ * catq_fakeq_gateup_swiglu_fwd -- the fused gate|up projection and its SwiGLU:
+ *   gu = X W_fake^T, a = silu(gate) * up
+ *   X bf16 [M][K], W_fake bf16 [2F][K] (gate rows, then up rows), gu bf16
+ *   [M][2F] ([gate | up]), a bf16 [M][F]; F % 8 == 0.
+ * catq_fakeq_down_swiglu_bwd -- input gradient of the down projection with
+ * the SwiGLU backward:  d a = dY W_fake, then d gate = d a * up * silu'(gate),
+ * d up = d a * silu(gate), written as d[gate | up]:
+ *   dY bf16 [M][N], W_fake bf16 [N][F], gu bf16 [M][2F] (the forward's),
+ *   dgu bf16 [M][2F] out; da bf16 [M][F] is scratch used only for shapes the
+ *   fused epilogue does not take (may be NULL otherwise; then such a shape is
+ *   CATQ_ERR_NULL).  F % 8 == 0.  16-byte aligned pointers. */
+catq_status catq_fakeq_gateup_swiglu_fwd(const void* X, const void* W_fake, int64_t M, int64_t F,
+                                         int64_t K, void* gu, void* a, hipStream_t stream);
+catq_status catq_fakeq_down_swiglu_bwd(const void* dY, const void* W_fake, int64_t M, int64_t N,
+                                       int64_t F, const void* gu, void* dgu, void* da,
+                                       hipStream_t stream);
+
 /* Workspace sizes, in bytes, for the calls that take a workspace. */
 enum { CATQ_WS_LINEAR_BWD = 0, CATQ_WS_LOSS = 1 };
 size_t catq_workspace_size(int32_t which_call, int64_t M, int64_t N, int64_t K, int32_t n_experts);

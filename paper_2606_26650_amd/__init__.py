@@ -14,7 +14,8 @@ from ._lib import (BF16, F32, HARD, IDENTITY, SOFT, WS_LINEAR_BWD, WS_LOSS, Attn
 
 __all__ = [
     "catq_modulate_ternarize", "catq_fakeq_linear_fwd", "catq_fakeq_linear_bwd",
-    "catq_block_recon_loss", "catq_pack_ternary", "catq_ternary_linear", "catq_workspace_size",
+    "catq_block_recon_loss", "catq_pack_ternary", "catq_fakeq_gateup_swiglu_fwd",
+    "catq_fakeq_down_swiglu_bwd", "catq_ternary_linear", "catq_workspace_size",
     "catq_aux_act_quant", "catq_aux_rmsnorm_fwd", "catq_aux_rmsnorm_bwd", "catq_aux_attention_fwd",
     "catq_aux_attention_bwd", "catq_attn_saved_bytes", "catq_attn_bwd_workspace_bytes",
     "catq_aux_swiglu_fwd", "catq_aux_swiglu_bwd", "catq_aux_moe_route",
@@ -133,6 +134,18 @@ def catq_ternary_linear(X, packed, alpha, Y, g=128, stream=None):
                                  _ptr(alpha), d_out, d_in, g, _ptr(Y), _dt(Y),
                                  Y.stride(0) if M else d_out, _stream(stream))
     _lib.check("catq_ternary_linear", st)
+
+
+def catq_fakeq_gateup_swiglu_fwd(X, W_fake, gu, a, M, F, K, stream=None):
+    st = lib.catq_fakeq_gateup_swiglu_fwd(_ptr(X), _ptr(W_fake), M, F, K, _ptr(gu), _ptr(a),
+                                          _stream(stream))
+    _lib.check("catq_fakeq_gateup_swiglu_fwd", st)
+
+
+def catq_fakeq_down_swiglu_bwd(dY, W_fake, gu, dgu, M, N, F, da=None, stream=None):
+    st = lib.catq_fakeq_down_swiglu_bwd(_ptr(dY), _ptr(W_fake), M, N, F, _ptr(gu), _ptr(dgu),
+                                        _ptr(da), _stream(stream))
+    _lib.check("catq_fakeq_down_swiglu_bwd", st)
 
 
 def catq_workspace_size(which, M, N, K, n_experts=1):

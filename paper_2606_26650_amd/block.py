@@ -25,7 +25,8 @@ from . import (BF16, HARD, IDENTITY, SOFT, attn_desc, catq_aux_act_quant, catq_a
                catq_aux_moe_scatter_add, catq_aux_rmsnorm_bwd, catq_aux_rmsnorm_fwd,
                catq_aux_swiglu_bwd, catq_aux_swiglu_fwd, catq_attn_bwd_workspace_bytes,
                catq_attn_saved_bytes, catq_block_recon_loss, catq_fakeq_linear_bwd,
-               catq_fakeq_linear_fwd, catq_modulate_ternarize, catq_pack_ternary,
+               catq_fakeq_down_swiglu_bwd, catq_fakeq_gateup_swiglu_fwd, catq_fakeq_linear_fwd,
+               catq_modulate_ternarize, catq_pack_ternary,
                catq_workspace_size, lmst_params, WS_LINEAR_BWD, WS_LOSS)
 
 DEV = "cuda"
@@ -144,6 +145,9 @@ class DenseBlock:
         hd, h = c.head_dim, c.hidden
         self.a8 = a8
         self._act = a8
+        # SwiGLU forward and backward inside the gate|up and down GEMM
+        # epilogues (same bits as the separate kernels; off: separate kernels)
+        self.fuse_swiglu = True
         self.Nqkv = (c.n_q + 2 * c.n_kv) * hd
         self.M = c.batch * c.seq
         self.g = g
@@ -249,8 +253,11 @@ class DenseBlock:
         if act:
             catq_aux_act_quant(self.xn2, self.xn2)
         L = self.lin["gu"]
-        catq_fakeq_linear_fwd(self.xn2, L.W_fake, self.gu, M, 2 * c.ffn, h)
-        catq_aux_swiglu_fwd(self.gu, self.a)
+        if self.fuse_swiglu:
+            catq_fakeq_gateup_swiglu_fwd(self.xn2, L.W_fake, self.gu, self.a, M, c.ffn, h)
+        else:
+            catq_fakeq_linear_fwd(self.xn2, L.W_fake, self.gu, M, 2 * c.ffn, h)
+            catq_aux_swiglu_fwd(self.gu, self.a)
         if act:
             catq_aux_act_quant(self.a, self.a)
         L = self.lin["d"]
@@ -300,8 +307,20 @@ class DenseBlock:
                                   L.d_alpha, L.d_delta, p, None, None, None, None, dX=dX)
 
         dy = self.dy if dy is None else dy
-        lbwd("d", dy, self.a, self.da)
-        catq_aux_swiglu_bwd(self.gu, self.da, self.dgu)
+        if self.fuse_swiglu:
+            # the down projection's weight-gradient half as usual; its input
+            # gradient with the SwiGLU backward in the GEMM epilogue
+            L = self.lin["d"]
+            if side is not None:
+                self.order("d", main, side)
+            with torch.cuda.stream(side if side is not None else main):
+                catq_fakeq_linear_bwd(dy, self.a, L.W_fake, M, L.d_out, L.d_in, L.W, L.stats,
+                                      L.d_mu, L.d_alpha, L.d_delta, p, L.g_mu, L.g_alpha,
+                                      L.g_delta, ws)
+            catq_fakeq_down_swiglu_bwd(dy, L.W_fake, self.gu, self.dgu, M, h, c.ffn, da=self.da)
+        else:
+            lbwd("d", dy, self.a, self.da)
+            catq_aux_swiglu_bwd(self.gu, self.da, self.dgu)
         lbwd("gu", self.dgu, self.xn2, self.dxn2)
         catq_aux_rmsnorm_bwd(self.h1, self.rstd2, self.dxn2, self.dh1, dres=dy)
         lbwd("o", self.dh1, self.o_in, self.dattn)

@@ -86,6 +86,18 @@ __device__ __forceinline__ void load8<float>(const float* p, float (&v)[8]) {
   }
 }
 
+// SwiGLU of one (gate, up) pair and its backward; shared by the SwiGLU
+// kernels and the GEMM epilogues that fuse them (identical results).
+__device__ __forceinline__ float sigmoid_f(float g) { return 1.0f / (1.0f + __expf(-g)); }
+__device__ __forceinline__ float swiglu1(float g, float u) { return g * sigmoid_f(g) * u; }
+__device__ __forceinline__ void swiglu1_bwd(float g, float u, float d, float& dg, float& du) {
+  const float sg = sigmoid_f(g);
+  const float silu = g * sg;
+  du = d * silu;
+  dg = d * u * sg * (1.0f + g * (1.0f - sg));
+}
+__device__ __forceinline__ float bf16_round_f(float x) { return (float)(bf16)x; }
+
 template <typename T>
 __device__ __forceinline__ void store8(T* p, const float (&v)[8]);
 template <>

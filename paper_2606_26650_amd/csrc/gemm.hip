@@ -37,6 +37,9 @@ GemmArgs gemm_args_default() {
   a.causal = 0;
   a.group_off = nullptr;
   a.group_mode = 0;
+  a.epi = 0;
+  a.aux0 = a.aux1 = nullptr;
+  a.ld_aux = 0;
   a.n_groups = 1;
   a.b_gs = a.c_gs = 0;
   a.max_rows_per_group = 0;
@@ -384,6 +387,20 @@ struct DmaOpNT {
       g[i] = base + min(row0 + blk * 8 + rl, rows - 1) * ld + c * 8;
     }
   }
+  // tile row r holds matrix row half*(r & 1) + (row0 + r)/2 (row0 even):
+  // gate and up rows of a fused [gate | up] weight taken in pairs
+  __device__ __forceinline__ void init_pairs(const bf16* base, int64_t ld, int64_t row0,
+                                             int64_t half, int wave, int lane) {
+    const int rl = lane >> 3;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int blk = wave * NI + i;
+      const int c = (lane & 7) ^ (((blk & 1) << 2) | (rl >> 1));
+      const int r = blk * 8 + rl;
+      const int64_t mr = (r & 1) * half + min((row0 + r) >> 1, half - 1);
+      g[i] = base + mr * ld + c * 8;
+    }
+  }
   __device__ __forceinline__ void issue(uint4* lds, int64_t ld, int64_t k0, int wave) const {
 #pragma unroll
     for (int i = 0; i < NI; ++i) dma16(g[i] + k0, &lds[(wave * NI + i) * 64]);
@@ -438,7 +455,7 @@ struct DmaOpKM {
 };
 
 template <int BM, int BN, int WGM, int WGN, bool AKM, bool BKM, typename OutT, typename RT,
-          bool HAS_R>
+          bool HAS_R, int EPI = 0>
 __global__ __launch_bounds__(WGM* WGN * 64, 1)
     __attribute__((amdgpu_waves_per_eu(1, (WGM * WGN + 3) / 4))) void gemm_dma_kernel(GemmLaunch L) {
 #if defined(__HIP_DEVICE_COMPILE__)
@@ -466,7 +483,10 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
   OA oa;
   OB ob;
   oa.init(reinterpret_cast<const bf16*>(g.A), g.lda, m0, g.M, wave, lane);
-  ob.init(reinterpret_cast<const bf16*>(g.B), g.ldb, n0, g.N, wave, lane);
+  if constexpr (EPI == 1)
+    ob.init_pairs(reinterpret_cast<const bf16*>(g.B), g.ldb, n0, g.N / 2, wave, lane);
+  else
+    ob.init(reinterpret_cast<const bf16*>(g.B), g.ldb, n0, g.N, wave, lane);
   bf16x8 fa[2][FM], fb[2][FN];
   auto ldfrag = [&](int buf, int kk, int slot) {
 #pragma unroll
@@ -564,12 +584,43 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
         f32x4 v = *reinterpret_cast<const f32x4*>(st + rr * EP + cc);
         if (m < g.M && n < g.N) {
           v *= g.alpha;
-          if (HAS_R) v += load4f(R + m * g.ldr + n);
-          store4f(C + m * g.ldc + n, v);
+          if constexpr (EPI == 1) {
+            // columns n..n+3 = gate_p, up_p, gate_p+1, up_p+1 (p = n/2), each
+            // rounded as stored; gate|up back to [gate | up], a = SwiGLU
+            const int64_t p = n >> 1, half = g.N >> 1;
+            const float g0 = bf16_round_f(v[0]), u0 = bf16_round_f(v[1]);
+            const float g1 = bf16_round_f(v[2]), u1 = bf16_round_f(v[3]);
+            bf16* gu = reinterpret_cast<bf16*>(C) + m * g.ldc;
+            *reinterpret_cast<unsigned*>(gu + p) = pack_bf16x2(g0, g1);
+            *reinterpret_cast<unsigned*>(gu + half + p) = pack_bf16x2(u0, u1);
+            bf16* ar = reinterpret_cast<bf16*>(g.aux0) + m * g.ld_aux;
+            *reinterpret_cast<unsigned*>(ar + p) = pack_bf16x2(swiglu1(g0, u0), swiglu1(g1, u1));
+          } else if constexpr (EPI == 2) {
+            // v = d a[m][n..n+3] (rounded as stored); gate|up of the forward
+            // from aux0, d[gate | up] to aux1
+            const int64_t Fh = g.N;
+            const bf16* gu = reinterpret_cast<const bf16*>(g.aux0) + m * g.ld_aux;
+            bf16* dgu = reinterpret_cast<bf16*>(g.aux1) + m * g.ld_aux;
+            const f32x4 gg = load4f(gu + n), uu = load4f(gu + Fh + n);
+            f32x4 dg, du;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              float a_, b_;
+              swiglu1_bwd(gg[e], uu[e], bf16_round_f(v[e]), a_, b_);
+              dg[e] = a_;
+              du[e] = b_;
+            }
+            store4f(dgu + n, dg);
+            store4f(dgu + Fh + n, du);
+          } else {
+            if (HAS_R) v += load4f(R + m * g.ldr + n);
+            store4f(C + m * g.ldc + n, v);
+          }
         }
       }
     }
-  } else {
+  } else if constexpr (EPI == 0) {
+    // (the fused epilogues run only where the host checked the vector path)
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
 #pragma unroll
@@ -700,26 +751,29 @@ static void launch_cfg(GemmLaunch& L, hipStream_t stream) {
                                    grid, block, 0, stream, L));
 }
 
-template <int BM, int BN, int WGM, int WGN, bool AKM, bool BKM, typename OutT, typename RT>
+template <int BM, int BN, int WGM, int WGN, bool AKM, bool BKM, typename OutT, typename RT,
+          int EPI = 0>
 static void launch_dma(GemmLaunch& L, hipStream_t stream) {
   const GemmArgs& g = L.g;
   L.tiles_m = (int)((g.M + BM - 1) / BM);
   L.tiles_n = (int)((g.N + BN - 1) / BN);
   dim3 grid((unsigned)(L.tiles_m * L.tiles_n), 1, (unsigned)L.ksplit);
   dim3 block(WGM * WGN * 64);
-  char tag[96];
-  std::snprintf(tag, sizeof(tag), "gemm_dma_kernel<%d, %d, %d, %d, %s%s, %s, %s, %s>", BM, BN, WGM,
-                WGN, AKM ? "k" : "n", BKM ? "k" : "t", tname<OutT>(), tname<RT>(),
-                g.R ? "true" : "false");
+  char tag[112];
+  std::snprintf(tag, sizeof(tag), "gemm_dma_kernel<%d, %d, %d, %d, %s%s, %s, %s, %s%s>", BM, BN,
+                WGM, WGN, AKM ? "k" : "n", BKM ? "k" : "t", tname<OutT>(), tname<RT>(),
+                g.R ? "true" : "false", EPI == 1 ? ", swiglu" : (EPI == 2 ? ", swiglu_bwd" : ""));
   double flops, bytes;
   gemm_work(L, (int)sizeof(OutT), flops, bytes);
+  if (EPI == 1) bytes += (double)g.M * (double)(g.N / 2) * 2.0;          // a written
+  if (EPI == 2) bytes += (double)g.M * (double)g.N * 2.0 * 4.0 - (double)g.M * g.N * sizeof(OutT);
   if (g.R)
     CATQ_TRACED(stream, tag, flops, bytes, g.M, g.N, g.K,
-                hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WGM, WGN, AKM, BKM, OutT, RT, true>),
+                hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WGM, WGN, AKM, BKM, OutT, RT, true, EPI>),
                                    grid, block, 0, stream, L));
   else
     CATQ_TRACED(stream, tag, flops, bytes, g.M, g.N, g.K,
-                hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WGM, WGN, AKM, BKM, OutT, RT, false>),
+                hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WGM, WGN, AKM, BKM, OutT, RT, false, EPI>),
                                    grid, block, 0, stream, L));
 }
 
@@ -813,6 +867,38 @@ catq_status gemm_run_split(const GemmArgs& a, int a_t, int b_t, catq_dtype in_dt
 catq_status gemm_run(const GemmArgs& a, int a_t, int b_t, catq_dtype in_dtype, catq_dtype c_dtype,
                      hipStream_t stream, catq_dtype r_dtype) {
   return gemm_run_split(a, a_t, b_t, in_dtype, c_dtype, 1, 0, stream, r_dtype);
+}
+
+catq_status gemm_run_epi(const GemmArgs& a, int a_t, int b_t, hipStream_t stream) {
+  CATQ_REQUIRE(a.epi == 1 || a.epi == 2, CATQ_ERR_VALUE, "unknown fused epilogue");
+  GemmLaunch L;
+  L.g = a;
+  L.ksplit = 1;
+  L.kchunk = a.K;
+  L.c_split_stride = 0;
+  L.tiles_m = L.tiles_n = 0;
+  if (a.M <= 0 || a.N <= 0 || a.K <= 0) return CATQ_OK;
+  // the vector epilogue: 4 consecutive columns per lane, 4-byte (EPI 1) or
+  // 8-byte (EPI 2) aligned rows of every output; and the shapes on which the
+  // plain GEMM takes the same 256 x 256 kernel, so fused and unfused results
+  // are the same bits
+  const int64_t t256 = ((a.M + 255) / 256) * ((a.N + 255) / 256);
+  const bool shape = t256 >= 256 && a.R == nullptr && a.alpha == 1.0f && a.N % 4 == 0 &&
+                     a.ldc % 4 == 0 && a.ld_aux % 4 == 0 && aligned16(a.C) && aligned16(a.aux0) &&
+                     (a.epi == 1 || aligned16(a.aux1));
+  if (a.epi == 1) {
+    // A [M][K] tokens (K-contiguous), B the fused weight [N][K]
+    if (!(shape && a_t == 0 && b_t == 0 && a.M >= 256 && a.N >= 256 && dma_ok(L, 0, 0, 256, 256)))
+      return CATQ_ERR_VALUE;
+    launch_dma<256, 256, 2, 4, false, false, bf16, bf16, 1>(L, stream);
+  } else {
+    // dX-shaped: A = dY [M][K] (K-contiguous), B = W_fake [K][N] (K-major)
+    if (!(shape && a_t == 0 && b_t == 1 && a.M >= 256 && a.N >= 256 && dma_ok(L, 0, 1, 256, 256)))
+      return CATQ_ERR_VALUE;
+    launch_dma<256, 256, 2, 4, false, true, bf16, bf16, 2>(L, stream);
+  }
+  CATQ_CHECK_LAUNCH("gemm fused epilogue");
+  return CATQ_OK;
 }
 
 int gemm_split_count(const GemmArgs& a, int ksplit) {

@@ -134,7 +134,6 @@ __global__ __launch_bounds__(256) void rmsnorm_bwd_kernel(const XT* x, const flo
 
 // ---------------------------------------------------------------- SwiGLU
 
-__device__ __forceinline__ float sigmoid_f(float g) { return 1.0f / (1.0f + __expf(-g)); }
 
 __global__ __launch_bounds__(256) void swiglu_fwd_kernel(const bf16* gu, int64_t rows, int64_t F,
                                                          bf16* a) {
@@ -146,7 +145,7 @@ __global__ __launch_bounds__(256) void swiglu_fwd_kernel(const bf16* gu, int64_t
   load8<bf16>(gu + r * 2 * F + c * 8, g);
   load8<bf16>(gu + r * 2 * F + F + c * 8, u);
 #pragma unroll
-  for (int j = 0; j < 8; ++j) g[j] = g[j] * sigmoid_f(g[j]) * u[j];
+  for (int j = 0; j < 8; ++j) g[j] = swiglu1(g[j], u[j]);
   store8<bf16>(a + r * F + c * 8, g);
 }
 
@@ -161,12 +160,7 @@ __global__ __launch_bounds__(256) void swiglu_bwd_kernel(const bf16* gu, const b
   load8<bf16>(gu + r * 2 * F + F + c * 8, u);
   load8<bf16>(da + r * F + c * 8, d);
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const float sg = sigmoid_f(g[j]);
-    const float silu = g[j] * sg;
-    du[j] = d[j] * silu;
-    dg[j] = d[j] * u[j] * sg * (1.0f + g[j] * (1.0f - sg));
-  }
+  for (int j = 0; j < 8; ++j) swiglu1_bwd(g[j], u[j], d[j], dg[j], du[j]);
   store8<bf16>(dgu + r * 2 * F + c * 8, dg);
   store8<bf16>(dgu + r * 2 * F + F + c * 8, du);
 }

@@ -64,6 +64,18 @@ struct GemmArgs {
   int32_t n_groups;
   int64_t b_gs, c_gs;
   int64_t max_rows_per_group;  // group_mode 1: bound used to size the grid
+  // fused epilogues of the direct-to-LDS kernel (gemm_run_epi):
+  //  1 (SwiGLU forward): B rows are the gate rows [0, N/2) and up rows
+  //    [N/2, N) of a fused gate|up weight taken in (gate_j, up_j) pairs, so
+  //    output columns 2j, 2j+1 hold gate_j, up_j; C receives them as
+  //    [gate | up] (ldc) and aux0 the SwiGLU a [M][N/2] (ld_aux)
+  //  2 (SwiGLU backward): C is the gradient of a [M][N]; aux0 holds the
+  //    forward's [gate | up] [M][2N] and aux1 receives d[gate | up] (ld_aux);
+  //    C itself is not written
+  int32_t epi;
+  void* aux0;
+  void* aux1;
+  int64_t ld_aux;
 };
 
 GemmArgs gemm_args_default();
@@ -78,6 +90,11 @@ catq_status gemm_run_split(const GemmArgs& a, int a_t, int b_t, catq_dtype in_dt
                            catq_dtype c_dtype, int ksplit, int64_t c_split_stride,
                            hipStream_t stream, catq_dtype r_dtype = CATQ_BF16);
 int gemm_split_count(const GemmArgs& a, int ksplit);
+// A dense bf16 GEMM with one of the fused epilogues above (a.epi).  Returns
+// CATQ_ERR_VALUE without launching when the shape or layout does not fit
+// the direct-to-LDS kernel's vector epilogue (the caller then runs the
+// unfused pair of kernels).
+catq_status gemm_run_epi(const GemmArgs& a, int a_t, int b_t, hipStream_t stream);
 
 // ---------------------------------------------------------- fused attention
 struct FaArgs {

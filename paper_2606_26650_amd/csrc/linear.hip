@@ -109,6 +109,76 @@ extern "C" catq_status catq_fakeq_linear_fwd(const void* X, const void* W_fake, 
   return gemm_run(a, 0, 0, dtype, y_dtype, stream, r_dtype);
 }
 
+extern "C" catq_status catq_fakeq_gateup_swiglu_fwd(const void* X, const void* W_fake, int64_t M,
+                                                    int64_t F, int64_t K, void* gu, void* a,
+                                                    hipStream_t stream) {
+  clear_error();
+  CATQ_REQUIRE(X && W_fake && gu && a, CATQ_ERR_NULL, "NULL argument");
+  CATQ_REQUIRE(M > 0 && F > 0 && K > 0 && F % 8 == 0, CATQ_ERR_SHAPE,
+               "M, K must be > 0 and F a positive multiple of 8");
+  CATQ_REQUIRE(aligned16(X) && aligned16(W_fake) && aligned16(gu) && aligned16(a),
+               CATQ_ERR_ALIGN, "pointers must be 16-byte aligned");
+  GemmArgs g = gemm_args_default();
+  g.A = X;
+  g.B = W_fake;
+  g.C = gu;
+  g.M = M;
+  g.N = 2 * F;
+  g.K = K;
+  g.lda = K;
+  g.ldb = K;
+  g.ldc = 2 * F;
+  g.epi = 1;
+  g.aux0 = a;
+  g.ld_aux = F;
+  const catq_status st = gemm_run_epi(g, 0, 0, stream);
+  if (st != CATQ_ERR_VALUE) return st;
+  // not eligible for the fused epilogue: the GEMM, then the SwiGLU kernel
+  clear_error();
+  g.epi = 0;
+  g.aux0 = nullptr;
+  CATQ_TRY(gemm_run(g, 0, 0, CATQ_BF16, CATQ_BF16, stream));
+  return catq_aux_swiglu_fwd(gu, M, F, a, stream);
+}
+
+extern "C" catq_status catq_fakeq_down_swiglu_bwd(const void* dY, const void* W_fake, int64_t M,
+                                                  int64_t N, int64_t F, const void* gu, void* dgu,
+                                                  void* da, hipStream_t stream) {
+  clear_error();
+  CATQ_REQUIRE(dY && W_fake && gu && dgu, CATQ_ERR_NULL, "NULL argument");
+  CATQ_REQUIRE(M > 0 && N > 0 && F > 0 && F % 8 == 0, CATQ_ERR_SHAPE,
+               "M, N must be > 0 and F a positive multiple of 8");
+  CATQ_REQUIRE(aligned16(dY) && aligned16(W_fake) && aligned16(gu) && aligned16(dgu) &&
+                   aligned16(da),
+               CATQ_ERR_ALIGN, "pointers must be 16-byte aligned");
+  // d a = dY . W_fake (contraction over the N outputs; W_fake K-major)
+  GemmArgs g = gemm_args_default();
+  g.A = dY;
+  g.B = W_fake;
+  g.C = dgu;   // not written by the fused epilogue
+  g.M = M;
+  g.N = F;
+  g.K = N;
+  g.lda = N;
+  g.ldb = F;
+  g.ldc = F;
+  g.epi = 2;
+  g.aux0 = const_cast<void*>(gu);
+  g.aux1 = dgu;
+  g.ld_aux = 2 * F;
+  const catq_status st = gemm_run_epi(g, 0, 1, stream);
+  if (st != CATQ_ERR_VALUE) return st;
+  // not eligible: d a into the caller's scratch, then the SwiGLU backward
+  clear_error();
+  CATQ_REQUIRE(da != nullptr, CATQ_ERR_NULL,
+               "this shape needs the d a scratch buffer (bf16 [M][F])");
+  g.epi = 0;
+  g.C = da;
+  g.aux0 = g.aux1 = nullptr;
+  CATQ_TRY(gemm_run(g, 0, 1, CATQ_BF16, CATQ_BF16, stream));
+  return catq_aux_swiglu_bwd(gu, da, M, F, dgu, stream);
+}
+
 extern "C" catq_status catq_fakeq_linear_bwd(
     const void* dY, const void* X, const void* W_fake, catq_dtype dtype, int64_t M, int64_t N,
     int64_t K, int32_t n_experts, const int64_t* row_offsets, const void* W, catq_dtype w_dtype,

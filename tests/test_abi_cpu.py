@@ -127,6 +127,11 @@ def test_aux_validation(cq):
     assert L.catq_aux_rmsnorm_fwd(FAKE, 1, 4, 12, 1e-6, FAKE, None, None) == 2
     assert L.catq_aux_rmsnorm_fwd(FAKE, 3, 4, 16, 1e-6, FAKE, None, None) == 3
     assert L.catq_aux_swiglu_fwd(FAKE, 4, 12, FAKE, None) == 2
+    assert L.catq_fakeq_gateup_swiglu_fwd(FAKE, FAKE, 4, 12, 64, FAKE, FAKE, None) == 2
+    assert L.catq_fakeq_gateup_swiglu_fwd(FAKE, None, 4, 16, 64, FAKE, FAKE, None) == 1
+    assert L.catq_fakeq_gateup_swiglu_fwd(FAKE, FAKE, 4, 16, 64, FAKE, FAKE + 2, None) == 5
+    assert L.catq_fakeq_down_swiglu_bwd(FAKE, FAKE, 4, 64, 12, FAKE, FAKE, FAKE, None) == 2
+    assert L.catq_fakeq_down_swiglu_bwd(FAKE, FAKE, 4, 64, 16, None, FAKE, FAKE, None) == 1
     d = cq.attn_desc(1, 16, 3, 2, 64, True, 1e6)          # n_q not a multiple of n_kv
     assert L.catq_aux_attention_fwd(C.byref(d), FAKE, FAKE, FAKE, 1 << 30, None) == 2
     d = cq.attn_desc(1, 16, 2, 1, 96, True, 1e6)          # head_dim
