@@ -164,10 +164,9 @@ __device__ __forceinline__ void store_out<bf16>(bf16* p, float v) {
   *p = (bf16)v;
 }
 
-__device__ __forceinline__ void tile_coords(int pid, int tiles_m, int tiles_n, int& pm, int& pn) {
-  const int num = tiles_m * tiles_n;
-  // keep neighbouring tiles on one XCD (round-robin dispatch over 8 XCDs)
-  if ((num & 7) == 0) pid = (pid & 7) * (num >> 3) + (pid >> 3);
+// tile id -> (tile row, tile column), walking bands of 8 tile rows column by
+// column (the A panels of a band stay in L2 while its B panels stream)
+__device__ __forceinline__ void band_coords(int pid, int tiles_m, int tiles_n, int& pm, int& pn) {
   constexpr int GROUP_M = 8;
   const int in_group = GROUP_M * tiles_n;
   const int gid = pid / in_group;
@@ -176,6 +175,25 @@ __device__ __forceinline__ void tile_coords(int pid, int tiles_m, int tiles_n, i
   const int r = pid % in_group;
   pm = first + r % gsz;
   pn = r / gsz;
+}
+
+__device__ __forceinline__ void tile_coords(int pid, int tiles_m, int tiles_n, int& pm, int& pn) {
+  const int num = tiles_m * tiles_n;
+  // keep neighbouring tiles on one XCD (round-robin dispatch over 8 XCDs)
+  if ((num & 7) == 0) pid = (pid & 7) * (num >> 3) + (pid >> 3);
+  band_coords(pid, tiles_m, tiles_n, pm, pn);
+}
+
+// One-dimensional grid over (K split, tile).  Workgroups are dealt to the 8
+// XCDs round-robin; each XCD gets a contiguous range of (split, tile) ids, so
+// with splits an XCD works through one K range (its operand panels are read
+// by that XCD alone) and neighbouring tiles share its L2.
+__device__ __forceinline__ void split_tile_coords(int lin, int tiles_m, int tiles_n, int ksplit,
+                                                  int& pm, int& pn, int& z) {
+  const int T = tiles_m * tiles_n, num = T * ksplit;
+  const int v = (num & 7) == 0 ? (lin & 7) * (num >> 3) + (lin >> 3) : lin;
+  z = v / T;
+  band_coords(v - z * T, tiles_m, tiles_n, pm, pn);
 }
 
 template <int BM, int BN, int BK, int WGM, int WGN, int A_T, int B_T, typename OutT, typename RT,
@@ -333,6 +351,18 @@ __device__ __forceinline__ f32x4 load4f(const bf16* p) {
   v[3] = __uint_as_float(u.y & 0xffff0000u);
   return v;
 }
+// 4 consecutive values kept as loaded (fp32: 16 B, bf16: 8 B), widened later
+__device__ __forceinline__ f32x4 raw4(const float* p) { return *reinterpret_cast<const f32x4*>(p); }
+__device__ __forceinline__ uint2 raw4(const bf16* p) { return *reinterpret_cast<const uint2*>(p); }
+__device__ __forceinline__ f32x4 widen4(f32x4 v) { return v; }
+__device__ __forceinline__ f32x4 widen4(uint2 u) {
+  f32x4 v;
+  v[0] = __uint_as_float(u.x << 16);
+  v[1] = __uint_as_float(u.x & 0xffff0000u);
+  v[2] = __uint_as_float(u.y << 16);
+  v[3] = __uint_as_float(u.y & 0xffff0000u);
+  return v;
+}
 __device__ __forceinline__ void store4f(float* p, f32x4 v) { *reinterpret_cast<f32x4*>(p) = v; }
 __device__ __forceinline__ void store4f(bf16* p, f32x4 v) {
   uint2 u;
@@ -471,14 +501,14 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WGN, wn = wave % WGN;
-  int pm, pn;
-  tile_coords(blockIdx.x, L.tiles_m, L.tiles_n, pm, pn);
+  int pm, pn, z;
+  split_tile_coords(blockIdx.x, L.tiles_m, L.tiles_n, L.ksplit, pm, pn, z);
   const int64_t m0 = (int64_t)pm * BM, n0 = (int64_t)pn * BN;
   int64_t kb = 0, ke = g.K, c_off = 0;
   if (L.ksplit > 1) {
-    kb = (int64_t)blockIdx.z * L.kchunk;
+    kb = (int64_t)z * L.kchunk;
     ke = min(g.K, kb + L.kchunk);
-    c_off = (int64_t)blockIdx.z * L.c_split_stride;
+    c_off = (int64_t)z * L.c_split_stride;
   }
   OA oa;
   OB ob;
@@ -568,19 +598,41 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
   if (vec) {
     constexpr int EP = WTN + 8;
     constexpr int LPR = WTN / 4, RPP = 64 / LPR;  // lanes per row, rows per pass
+    constexpr int NP = 32 / RPP;                  // passes per 32-row slab
     static_assert(NW * 32 * EP * 4 <= (int)sizeof(sA) + (int)sizeof(sB), "epilogue staging");
     float* st = reinterpret_cast<float*>(&sA[0][0]) + wave * (32 * EP);
+    const int cc = (lane % LPR) * 4;
+    const int64_t n = n0 + wn * WTN + cc;
+    const int64_t n_c = min(n, g.N - 4);   // clamped column for the early loads
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
+      // The slab's other inputs (residual, or gate and up of the forward) are
+      // loaded for all its passes before the LDS round trip, so their latency
+      // is paid once per slab; rows clamped into the matrix, the values of
+      // lanes outside it unused.
+      using RawR = decltype(raw4((const RT*)nullptr));
+      [[maybe_unused]] RawR rv[NP];
+      [[maybe_unused]] uint2 gv[NP], uv[NP];
+#pragma unroll
+      for (int q = 0; q < NP; ++q) {
+        const int64_t m_c = min(m0 + wm * WTM + i * 32 + q * RPP + lane / LPR, g.M - 1);
+        if constexpr (EPI == 2) {
+          const bf16* gu = reinterpret_cast<const bf16*>(g.aux0) + m_c * g.ld_aux;
+          gv[q] = raw4(gu + n_c);
+          uv[q] = raw4(gu + g.N + n_c);
+        } else if constexpr (EPI == 0 && HAS_R) {
+          rv[q] = raw4(R + m_c * g.ldr + n_c);
+        }
+      }
 #pragma unroll
       for (int j = 0; j < FN; ++j)
 #pragma unroll
         for (int r = 0; r < 16; ++r)
           st[(8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * EP + j * 32 + (lane & 31)] = acc[i][j][r];
 #pragma unroll
-      for (int rr0 = 0; rr0 < 32; rr0 += RPP) {
-        const int rr = rr0 + lane / LPR, cc = (lane % LPR) * 4;
-        const int64_t m = m0 + wm * WTM + i * 32 + rr, n = n0 + wn * WTN + cc;
+      for (int q = 0; q < NP; ++q) {
+        const int rr = q * RPP + lane / LPR;
+        const int64_t m = m0 + wm * WTM + i * 32 + rr;
         f32x4 v = *reinterpret_cast<const f32x4*>(st + rr * EP + cc);
         if (m < g.M && n < g.N) {
           v *= g.alpha;
@@ -599,9 +651,8 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
             // v = d a[m][n..n+3] (rounded as stored); gate|up of the forward
             // from aux0, d[gate | up] to aux1
             const int64_t Fh = g.N;
-            const bf16* gu = reinterpret_cast<const bf16*>(g.aux0) + m * g.ld_aux;
             bf16* dgu = reinterpret_cast<bf16*>(g.aux1) + m * g.ld_aux;
-            const f32x4 gg = load4f(gu + n), uu = load4f(gu + Fh + n);
+            const f32x4 gg = widen4(gv[q]), uu = widen4(uv[q]);
             f32x4 dg, du;
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
@@ -613,7 +664,7 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
             store4f(dgu + n, dg);
             store4f(dgu + Fh + n, du);
           } else {
-            if (HAS_R) v += load4f(R + m * g.ldr + n);
+            if constexpr (HAS_R) v += widen4(rv[q]);
             store4f(C + m * g.ldc + n, v);
           }
         }
@@ -757,7 +808,7 @@ static void launch_dma(GemmLaunch& L, hipStream_t stream) {
   const GemmArgs& g = L.g;
   L.tiles_m = (int)((g.M + BM - 1) / BM);
   L.tiles_n = (int)((g.N + BN - 1) / BN);
-  dim3 grid((unsigned)(L.tiles_m * L.tiles_n), 1, (unsigned)L.ksplit);
+  dim3 grid((unsigned)(L.tiles_m * L.tiles_n * L.ksplit));
   dim3 block(WGM * WGN * 64);
   char tag[112];
   std::snprintf(tag, sizeof(tag), "gemm_dma_kernel<%d, %d, %d, %d, %s%s, %s, %s, %s%s>", BM, BN,
