@@ -150,6 +150,35 @@ __device__ __forceinline__ void dma16(const void* g, const void* lds_base) {
                : "memory", "m0");
 #endif
 }
+
+typedef int i32x4_rsrc __attribute__((ext_vector_type(4)));
+
+// Buffer resource (uniform, SGPRs) for raw loads of `bytes` bytes from p:
+// offsets at or past the end read as zero without touching memory.
+__device__ __forceinline__ i32x4_rsrc buf_rsrc(const void* p, uint32_t bytes) {
+  const uint64_t a = (uint64_t)(uintptr_t)p;
+  i32x4_rsrc r;
+  r[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+  r[1] = __builtin_amdgcn_readfirstlane((int)((uint32_t)(a >> 32) & 0xffffu));
+  r[2] = __builtin_amdgcn_readfirstlane((int)bytes);
+  r[3] = 0x00020000;
+  return r;
+}
+
+// 16-byte buffer -> LDS copy (lane l landing at lds_base + 16*l) from byte
+// offset voff (per lane) + soff (uniform) of the resource.  One VGPR per
+// lane instead of a 64-bit address; waits as for dma16.
+__device__ __forceinline__ void dma16_buf(i32x4_rsrc rsrc, uint32_t voff, uint32_t soff,
+                                          const void* lds_base) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  const unsigned l = __builtin_amdgcn_readfirstlane(
+      (unsigned)(uintptr_t)(__attribute__((address_space(3))) const void*)lds_base);
+  const unsigned so = __builtin_amdgcn_readfirstlane(soff);
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds" ::"s"(l), "v"(voff),
+               "s"(rsrc), "s"(so)
+               : "memory", "m0");
+#endif
+}
 #pragma clang diagnostic pop
 
 __device__ __forceinline__ void wait_vmem() {

@@ -373,16 +373,16 @@ __device__ __forceinline__ void store4f(bf16* p, f32x4 v) {
 
 // ------------------------------------------- dense GEMM, direct to LDS
 //
-// Tiles move from global memory straight into LDS with global_load_lds_dwordx4
-// (no register staging): each wave instruction fills 1 KB of LDS, lane l
+// Tiles move from global memory straight into LDS with buffer_load_dwordx4 ...
+// lds (no register staging): each wave instruction fills 1 KB of LDS, lane l
 // landing at base + 16 l.  Each operand is in one of two layouts:
 //
 // * K-contiguous ("nt", stored [rows][K]): a tile is ROWS x 64 bf16 =
 //   ROWS*8 chunks of 16 B; chunk c of row r sits in slot r*8 + (c ^ ((r >> 1)
 //   & 7)).  A 128-bit LDS read is served 16 lanes at a time over 64 four-byte
 //   banks; the MFMA fragment read (16 consecutive rows at one chunk) then
-//   covers all 16 bank groups once.  Rows past the matrix are clamped to the
-//   last row (their results are never stored).
+//   covers all 16 bank groups once.  Rows past the matrix read as zero
+//   (their results are never stored).
 // * K-major ("km", stored [K][cols]): a tile is 64 rows of k x COLS bf16;
 //   chunk c of row k sits in slot k*(COLS/8) + (c ^ (4*(k & 3))).  Fragments
 //   come from two ds_read_b64_tr_b16 each: within a block of 16 lanes, lane i
@@ -400,40 +400,56 @@ __device__ __forceinline__ void store4f(bf16* p, f32x4 v) {
 // sub-step after the barrier.
 
 
-// K-contiguous operand tile, ROWS x 64, for NW waves.
+// K-contiguous operand tile, ROWS x 64, for NW waves.  Buffer loads from the
+// tile's first row: instructions i and i+2 differ only by 16 rows (a uniform
+// offset), so a lane keeps two 32-bit offsets; rows past the matrix read as
+// zero (their results are never stored).
 template <int ROWS, int NW>
 struct DmaOpNT {
   static constexpr int NI = ROWS / 8 / NW;  // 1 KB instructions per wave
   static constexpr int READS = 1;           // LDS reads per fragment
-  static_assert(NI >= 1, "tile too small for the wave count");
-  const bf16* g[NI];
+  static_assert(NI >= 2 && NI % 2 == 0, "tile too small for the wave count");
+  const char* panel;     // byte address of the tile's first row (uniform)
+  uint64_t bytes;        // bytes from panel to the end of the matrix
+  uint32_t step;         // bytes between instructions i and i+2 (uniform)
+  uint32_t voff[2];      // per lane, instructions of parity 0 and 1
   __device__ __forceinline__ void init(const bf16* base, int64_t ld, int64_t row0, int64_t rows,
                                        int wave, int lane) {
+    panel = reinterpret_cast<const char*>(base + row0 * ld);
+    bytes = (uint64_t)(rows - row0) * (uint64_t)ld * 2;
+    step = (uint32_t)(16 * ld * 2);
     const int rl = lane >> 3;
 #pragma unroll
-    for (int i = 0; i < NI; ++i) {
-      const int blk = wave * NI + i;
+    for (int p = 0; p < 2; ++p) {
+      const int blk = wave * NI + p;
       const int c = (lane & 7) ^ (((blk & 1) << 2) | (rl >> 1));
-      g[i] = base + min(row0 + blk * 8 + rl, rows - 1) * ld + c * 8;
+      voff[p] = (uint32_t)((blk * 8 + rl) * ld * 2 + c * 16);
     }
   }
   // tile row r holds matrix row half*(r & 1) + (row0 + r)/2 (row0 even):
-  // gate and up rows of a fused [gate | up] weight taken in pairs
+  // gate and up rows of a fused [gate | up] weight taken in pairs (gate rows
+  // past the end read up rows, up rows past the end read zero; neither is
+  // stored)
   __device__ __forceinline__ void init_pairs(const bf16* base, int64_t ld, int64_t row0,
                                              int64_t half, int wave, int lane) {
+    panel = reinterpret_cast<const char*>(base + (row0 >> 1) * ld);
+    bytes = (uint64_t)(2 * half - (row0 >> 1)) * (uint64_t)ld * 2;
+    step = (uint32_t)(8 * ld * 2);
     const int rl = lane >> 3;
 #pragma unroll
-    for (int i = 0; i < NI; ++i) {
-      const int blk = wave * NI + i;
+    for (int p = 0; p < 2; ++p) {
+      const int blk = wave * NI + p;
       const int c = (lane & 7) ^ (((blk & 1) << 2) | (rl >> 1));
-      const int r = blk * 8 + rl;
-      const int64_t mr = (r & 1) * half + min((row0 + r) >> 1, half - 1);
-      g[i] = base + mr * ld + c * 8;
+      const int64_t mr = (rl & 1) * half + blk * 4 + (rl >> 1);
+      voff[p] = (uint32_t)(mr * ld * 2 + c * 16);
     }
   }
-  __device__ __forceinline__ void issue(uint4* lds, int64_t ld, int64_t k0, int wave) const {
+  __device__ __forceinline__ void issue(uint4* lds, int64_t, int64_t k0, int wave) const {
+    const uint64_t kb = (uint64_t)k0 * 2;
+    const i32x4_rsrc r = buf_rsrc(panel + kb, (uint32_t)min(bytes - kb, (uint64_t)0xFFFFFFFFu));
 #pragma unroll
-    for (int i = 0; i < NI; ++i) dma16(g[i] + k0, &lds[(wave * NI + i) * 64]);
+    for (int i = 0; i < NI; ++i)
+      dma16_buf(r, voff[i & 1], (uint32_t)(i >> 1) * step, &lds[(wave * NI + i) * 64]);
   }
   // rows row0 .. row0+31 (lane: row row0 + lane%32), k = 16 kk + 8 (lane/32) .. +7
   __device__ __forceinline__ bf16x8 frag(const uint4* lds, int row0, int kk, int lane) const {
@@ -442,28 +458,36 @@ struct DmaOpNT {
   }
 };
 
-// K-major operand tile, 64 x COLS, for NW waves.
+// K-major operand tile, 64 x COLS, for NW waves.  Buffer loads from the
+// tile's 64-row k slab; the swizzle repeats every P instructions, so a lane
+// keeps P 32-bit offsets and the rest is a uniform offset.
 template <int COLS, int NW>
 struct DmaOpKM {
   static constexpr int CPR = COLS / 8;             // 16-byte chunks per row
   static constexpr int RPI = 64 / CPR;             // rows per 1 KB instruction
   static constexpr int NI = 64 * CPR / 64 / NW;    // instructions per wave
+  static constexpr int P = RPI >= 4 ? 1 : 4 / RPI; // period of the swizzle in i
   static constexpr int READS = 2;
-  static_assert(NI >= 1 && RPI >= 1, "tile too small for the wave count");
-  const bf16* g[NI];
+  static_assert(NI >= 1 && RPI >= 1 && NI % P == 0, "tile too small for the wave count");
+  const char* panel;     // byte address of the tile's first column, row 0 (uniform)
+  uint32_t ld2;          // row pitch in bytes
+  uint32_t voff[P];      // per lane
   __device__ __forceinline__ void init(const bf16* base, int64_t ld, int64_t col0, int64_t,
                                        int wave, int lane) {
+    panel = reinterpret_cast<const char*>(base + col0);
+    ld2 = (uint32_t)(ld * 2);
 #pragma unroll
-    for (int i = 0; i < NI; ++i) {
-      const int row = (wave * NI + i) * RPI + lane / CPR;
+    for (int p = 0; p < P; ++p) {
+      const int row = (wave * NI + p) * RPI + lane / CPR;
       const int c = (lane % CPR) ^ (4 * (row & 3));
-      g[i] = base + (int64_t)row * ld + col0 + c * 8;
+      voff[p] = (uint32_t)(row * ld * 2 + c * 16);
     }
   }
   __device__ __forceinline__ void issue(uint4* lds, int64_t ld, int64_t k0, int wave) const {
-    const int64_t off = k0 * ld;
+    const i32x4_rsrc r = buf_rsrc(panel + (uint64_t)k0 * ld * 2, 64u * ld2);
 #pragma unroll
-    for (int i = 0; i < NI; ++i) dma16(g[i] + off, &lds[(wave * NI + i) * 64]);
+    for (int i = 0; i < NI; ++i)
+      dma16_buf(r, voff[i % P], (uint32_t)((i / P) * P * RPI) * ld2, &lds[(wave * NI + i) * 64]);
   }
   // columns col0 .. col0+31 (lane: column col0 + lane%32), k = 16 kk + 8 (lane/32) .. +7
   __device__ __forceinline__ bf16x8 frag(const uint4* lds, int col0, int kk, int lane) const {
@@ -829,12 +853,13 @@ static void launch_dma(GemmLaunch& L, hipStream_t stream) {
 }
 
 // The direct-to-LDS kernel serves dense bf16 problems with K (per split) a
-// multiple of 64; a K-major operand also needs its tile extent to divide the
-// matrix extent.
+// multiple of 64 and row pitches below 4M elements; a K-major operand also
+// needs its tile extent to divide the matrix extent.
 static bool dma_ok(const GemmLaunch& L, int a_t, int b_t, int bm, int bn) {
   const GemmArgs& g = L.g;
   return g.group_mode == 0 && g.causal == 0 && g.batch == 1 && g.K % 64 == 0 &&
          (L.ksplit <= 1 || L.kchunk % 64 == 0) && g.lda % 8 == 0 && g.ldb % 8 == 0 &&
+         g.lda < (1 << 22) && g.ldb < (1 << 22) &&  // 32-bit buffer offsets within a tile
          aligned16(g.A) && aligned16(g.B) && (a_t == 0 || g.M % bm == 0) &&
          (b_t == 0 || g.N % bn == 0);
 }
