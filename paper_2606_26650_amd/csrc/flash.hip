@@ -453,10 +453,11 @@ __global__ __launch_bounds__(fa::NT, 1) void flash_bwd_dkdv_kernel(FaArgs a) {
 template <int D>
 __global__ __launch_bounds__(fa::NT, 2) void flash_bwd_dq_kernel(FaArgs a) {
   using C = fa::Cfg<D>;
-  __shared__ u16 sK[fa::BK * C::KP];
-  __shared__ u16 sKt[D * fa::TP];
-  __shared__ u16 sV[fa::BK * C::KP];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 5, l32 = lane & 31;
+  constexpr int TW = 64 * D / 8;  // 16-byte slots of one 64 x D tile
+  __shared__ uint4 sK[2][TW];
+  __shared__ uint4 sV[2][TW];
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   // grid (B*Hq, query tiles): the longest causal rows are dispatched first
   const int qt = (int)gridDim.y - 1 - (int)blockIdx.y;
   const int h = blockIdx.x % a.Hq, b = blockIdx.x / a.Hq;
@@ -486,48 +487,52 @@ __global__ __launch_bounds__(fa::NT, 2) void flash_bwd_dq_kernel(FaArgs a) {
   const int q_last = min(q0 + 127, a.S - 1);
   const int nkt = q_last / fa::BK + 1;
   const int wave_last = q0 + 32 * w + 31;
-  fa::Tile<D> tk, tv;
-  tk.load(Kb, D, 0, a.S, tid);
-  tv.load(Vb, D, 0, a.S, tid);
+  // K and V tiles of 64 keys stream into swizzled row-major LDS tiles by
+  // direct copies (rows past the sequence read the last row; their P is 0);
+  // K^T fragments come from transpose reads of the same K tile
+  auto issue = [&](int buf, int k0) {
+    fa::dma_tile<D>(Kb, D, k0, a.S, sK[buf], w, lane);
+    fa::dma_tile<D>(Vb, D, k0, a.S, sV[buf], w, lane);
+  };
+  issue(0, 0);
+  wait_vmem();
+  __syncthreads();
   for (int kt = 0; kt < nkt; ++kt) {
-    const int k0 = kt * fa::BK;
-    __syncthreads();
-    tk.store_rows(sK);
-    tk.store_transposed(sKt);
-    tv.store_rows(sV);
-    __syncthreads();
-    if (kt + 1 < nkt) {
-      tk.load(Kb, D, k0 + fa::BK, a.S, tid);
-      tv.load(Vb, D, k0 + fa::BK, a.S, tid);
-    }
-    if (k0 > wave_last) continue;
+    const int k0 = kt * fa::BK, buf = kt & 1;
+    // the next tile lands in the buffer every wave finished reading before
+    // the previous barrier
+    if (kt + 1 < nkt) issue(buf ^ 1, k0 + fa::BK);
+    if (k0 <= wave_last) {
 #pragma unroll
-    for (int sb = 0; sb < 2; ++sb) {
-      f32x16 s = fa::zero16(), dp = fa::zero16();
+      for (int sb = 0; sb < 2; ++sb) {
+        f32x16 s = fa::zero16(), dp = fa::zero16();
 #pragma unroll
-      for (int t = 0; t < C::KS; ++t) {
-        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            fa::frag_rows(sK, sb * 32 + l32, 16 * t + 8 * g, C::KP), qf[t], s, 0, 0, 0);
-        dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            fa::frag_rows(sV, sb * 32 + l32, 16 * t + 8 * g, C::KP), of[t], dp, 0, 0, 0);
-      }
+        for (int t = 0; t < C::KS; ++t) {
+          s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              fa::tfrag_row<D>(sK[buf], sb * 32 + l32, 2 * t + g), qf[t], s, 0, 0, 0);
+          dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              fa::tfrag_row<D>(sV[buf], sb * 32 + l32, 2 * t + g), of[t], dp, 0, 0, 0);
+        }
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = k0 + sb * 32 + fa::acc_row(r, g);
-        float p = __builtin_amdgcn_exp2f(fmaf(s[r], a.c, -lse));
-        if (key > qme || key >= a.S || qme >= a.S) p = 0.f;
-        dp[r] = p * (dp[r] - dsum);
-      }
-      // dQ^T[d][q] += K^T dS  (contraction over keys)
+        for (int r = 0; r < 16; ++r) {
+          const int key = k0 + sb * 32 + fa::acc_row(r, g);
+          float p = __builtin_amdgcn_exp2f(fmaf(s[r], a.c, -lse));
+          if (key > qme || key >= a.S || qme >= a.S) p = 0.f;
+          dp[r] = p * (dp[r] - dsum);
+        }
+        // dQ^T[d][q] += K^T dS  (contraction over keys)
 #pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        const bf16x8 df = fa::pack8(dp, hh);
+        for (int hh = 0; hh < 2; ++hh) {
+          const bf16x8 df = fa::pack8(dp, hh);
 #pragma unroll
-        for (int i = 0; i < C::DB; ++i)
-          dq[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              fa::frag_tr(sKt, i * 32 + l32, 2 * sb + hh, g), df, dq[i], 0, 0, 0);
+          for (int i = 0; i < C::DB; ++i)
+            dq[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                fa::tfrag_tr<D>(sK[buf], i * 32, 2 * sb + hh, lane), df, dq[i], 0, 0, 0);
+        }
       }
     }
+    wait_vmem();
+    __syncthreads();
   }
   if (qme < a.S) {
     float* dQb = a.dQ + ((int64_t)(b * a.Hq + h) * a.S + qme) * D;
