@@ -622,74 +622,83 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
   if (vec) {
     constexpr int EP = WTN + 8;
     constexpr int LPR = WTN / 4, RPP = 64 / LPR;  // lanes per row, rows per pass
-    constexpr int NP = 32 / RPP;                  // passes per 32-row slab
-    static_assert(NW * 32 * EP * 4 <= (int)sizeof(sA) + (int)sizeof(sB), "epilogue staging");
-    float* st = reinterpret_cast<float*>(&sA[0][0]) + wave * (32 * EP);
+    // rows staged per LDS round trip: the whole 32-row slab when every wave's
+    // share fits in the operand buffers, else half of it (16 waves)
+    constexpr int SR = (NW * 32 * EP * 4 <= (int)sizeof(sA) + (int)sizeof(sB)) ? 32 : 16;
+    constexpr int NP = SR / RPP;                  // passes per staged part
+    static_assert(NW * SR * EP * 4 <= (int)sizeof(sA) + (int)sizeof(sB), "epilogue staging");
+    float* st = reinterpret_cast<float*>(&sA[0][0]) + wave * (SR * EP);
     const int cc = (lane % LPR) * 4;
     const int64_t n = n0 + wn * WTN + cc;
     const int64_t n_c = min(n, g.N - 4);   // clamped column for the early loads
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
-      // The slab's other inputs (residual, or gate and up of the forward) are
-      // loaded for all its passes before the LDS round trip, so their latency
-      // is paid once per slab; rows clamped into the matrix, the values of
-      // lanes outside it unused.
-      using RawR = decltype(raw4((const RT*)nullptr));
-      [[maybe_unused]] RawR rv[NP];
-      [[maybe_unused]] uint2 gv[NP], uv[NP];
 #pragma unroll
-      for (int q = 0; q < NP; ++q) {
-        const int64_t m_c = min(m0 + wm * WTM + i * 32 + q * RPP + lane / LPR, g.M - 1);
-        if constexpr (EPI == 2) {
-          const bf16* gu = reinterpret_cast<const bf16*>(g.aux0) + m_c * g.ld_aux;
-          gv[q] = raw4(gu + n_c);
-          uv[q] = raw4(gu + g.N + n_c);
-        } else if constexpr (EPI == 0 && HAS_R) {
-          rv[q] = raw4(R + m_c * g.ldr + n_c);
+      for (int h = 0; h < 32 / SR; ++h) {
+        const int64_t mrow = m0 + wm * WTM + i * 32 + h * SR;
+        // The part's other inputs (residual, or gate and up of the forward)
+        // are loaded for all its passes before the LDS round trip, so their
+        // latency is paid once; rows clamped into the matrix, the values of
+        // lanes outside it unused.
+        using RawR = decltype(raw4((const RT*)nullptr));
+        [[maybe_unused]] RawR rv[NP];
+        [[maybe_unused]] uint2 gv[NP], uv[NP];
+#pragma unroll
+        for (int q = 0; q < NP; ++q) {
+          const int64_t m_c = min(mrow + q * RPP + lane / LPR, g.M - 1);
+          if constexpr (EPI == 2) {
+            const bf16* gu = reinterpret_cast<const bf16*>(g.aux0) + m_c * g.ld_aux;
+            gv[q] = raw4(gu + n_c);
+            uv[q] = raw4(gu + g.N + n_c);
+          } else if constexpr (EPI == 0 && HAS_R) {
+            rv[q] = raw4(R + m_c * g.ldr + n_c);
+          }
         }
-      }
 #pragma unroll
-      for (int j = 0; j < FN; ++j)
+        for (int j = 0; j < FN; ++j)
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-          st[(8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * EP + j * 32 + (lane & 31)] = acc[i][j][r];
+          for (int r = 0; r < 16; ++r) {
+            const int row = 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+            if (row / SR == h) st[(row - h * SR) * EP + j * 32 + (lane & 31)] = acc[i][j][r];
+          }
 #pragma unroll
-      for (int q = 0; q < NP; ++q) {
-        const int rr = q * RPP + lane / LPR;
-        const int64_t m = m0 + wm * WTM + i * 32 + rr;
-        f32x4 v = *reinterpret_cast<const f32x4*>(st + rr * EP + cc);
-        if (m < g.M && n < g.N) {
-          v *= g.alpha;
-          if constexpr (EPI == 1) {
-            // columns n..n+3 = gate_p, up_p, gate_p+1, up_p+1 (p = n/2), each
-            // rounded as stored; gate|up back to [gate | up], a = SwiGLU
-            const int64_t p = n >> 1, half = g.N >> 1;
-            const float g0 = bf16_round_f(v[0]), u0 = bf16_round_f(v[1]);
-            const float g1 = bf16_round_f(v[2]), u1 = bf16_round_f(v[3]);
-            bf16* gu = reinterpret_cast<bf16*>(C) + m * g.ldc;
-            *reinterpret_cast<unsigned*>(gu + p) = pack_bf16x2(g0, g1);
-            *reinterpret_cast<unsigned*>(gu + half + p) = pack_bf16x2(u0, u1);
-            bf16* ar = reinterpret_cast<bf16*>(g.aux0) + m * g.ld_aux;
-            *reinterpret_cast<unsigned*>(ar + p) = pack_bf16x2(swiglu1(g0, u0), swiglu1(g1, u1));
-          } else if constexpr (EPI == 2) {
-            // v = d a[m][n..n+3] (rounded as stored); gate|up of the forward
-            // from aux0, d[gate | up] to aux1
-            const int64_t Fh = g.N;
-            bf16* dgu = reinterpret_cast<bf16*>(g.aux1) + m * g.ld_aux;
-            const f32x4 gg = widen4(gv[q]), uu = widen4(uv[q]);
-            f32x4 dg, du;
+        for (int q = 0; q < NP; ++q) {
+          const int rr = q * RPP + lane / LPR;
+          const int64_t m = mrow + rr;
+          f32x4 v = *reinterpret_cast<const f32x4*>(st + rr * EP + cc);
+          if (m < g.M && n < g.N) {
+            v *= g.alpha;
+            if constexpr (EPI == 1) {
+              // columns n..n+3 = gate_p, up_p, gate_p+1, up_p+1 (p = n/2), each
+              // rounded as stored; gate|up back to [gate | up], a = SwiGLU
+              const int64_t p = n >> 1, half = g.N >> 1;
+              const float g0 = bf16_round_f(v[0]), u0 = bf16_round_f(v[1]);
+              const float g1 = bf16_round_f(v[2]), u1 = bf16_round_f(v[3]);
+              bf16* gu = reinterpret_cast<bf16*>(C) + m * g.ldc;
+              *reinterpret_cast<unsigned*>(gu + p) = pack_bf16x2(g0, g1);
+              *reinterpret_cast<unsigned*>(gu + half + p) = pack_bf16x2(u0, u1);
+              bf16* ar = reinterpret_cast<bf16*>(g.aux0) + m * g.ld_aux;
+              *reinterpret_cast<unsigned*>(ar + p) = pack_bf16x2(swiglu1(g0, u0), swiglu1(g1, u1));
+            } else if constexpr (EPI == 2) {
+              // v = d a[m][n..n+3] (rounded as stored); gate|up of the forward
+              // from aux0, d[gate | up] to aux1
+              const int64_t Fh = g.N;
+              bf16* dgu = reinterpret_cast<bf16*>(g.aux1) + m * g.ld_aux;
+              const f32x4 gg = widen4(gv[q]), uu = widen4(uv[q]);
+              f32x4 dg, du;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              float a_, b_;
-              swiglu1_bwd(gg[e], uu[e], bf16_round_f(v[e]), a_, b_);
-              dg[e] = a_;
-              du[e] = b_;
+              for (int e = 0; e < 4; ++e) {
+                float a_, b_;
+                swiglu1_bwd(gg[e], uu[e], bf16_round_f(v[e]), a_, b_);
+                dg[e] = a_;
+                du[e] = b_;
+              }
+              store4f(dgu + n, dg);
+              store4f(dgu + Fh + n, du);
+            } else {
+              if constexpr (HAS_R) v += widen4(rv[q]);
+              store4f(C + m * g.ldc + n, v);
             }
-            store4f(dgu + n, dg);
-            store4f(dgu + Fh + n, du);
-          } else {
-            if constexpr (HAS_R) v += widen4(rv[q]);
-            store4f(C + m * g.ldc + n, v);
           }
         }
       }
@@ -869,7 +878,7 @@ static void launch_bf16(GemmLaunch& L, hipStream_t stream) {
   const GemmArgs& g = L.g;
   const int64_t t256 = ((g.M + 255) / 256) * ((g.N + 255) / 256) * L.ksplit;
   if (g.M >= 256 && g.N >= 256 && t256 >= 256 && dma_ok(L, A_T, B_T, 256, 256)) {
-    launch_dma<256, 256, 2, 4, A_T == 1, B_T == 1, OutT, RT>(L, stream);
+    launch_dma<256, 256, 4, 4, A_T == 1, B_T == 1, OutT, RT>(L, stream);
     return;
   }
   if (dma_ok(L, A_T, B_T, 128, 128)) {
@@ -966,12 +975,12 @@ catq_status gemm_run_epi(const GemmArgs& a, int a_t, int b_t, hipStream_t stream
     // A [M][K] tokens (K-contiguous), B the fused weight [N][K]
     if (!(shape && a_t == 0 && b_t == 0 && a.M >= 256 && a.N >= 256 && dma_ok(L, 0, 0, 256, 256)))
       return CATQ_ERR_VALUE;
-    launch_dma<256, 256, 2, 4, false, false, bf16, bf16, 1>(L, stream);
+    launch_dma<256, 256, 4, 4, false, false, bf16, bf16, 1>(L, stream);
   } else {
     // dX-shaped: A = dY [M][K] (K-contiguous), B = W_fake [K][N] (K-major)
     if (!(shape && a_t == 0 && b_t == 1 && a.M >= 256 && a.N >= 256 && dma_ok(L, 0, 1, 256, 256)))
       return CATQ_ERR_VALUE;
-    launch_dma<256, 256, 2, 4, false, true, bf16, bf16, 2>(L, stream);
+    launch_dma<256, 256, 4, 4, false, true, bf16, bf16, 2>(L, stream);
   }
   CATQ_CHECK_LAUNCH("gemm fused epilogue");
   return CATQ_OK;
