@@ -61,6 +61,11 @@ def parse():
                          "block at M tokens (deployment on the 2-bit storage)")
     ap.add_argument("--a8", action="store_true",
                     help="the W1.58A8 setting: activations fake-quantized to 8 bits in the step")
+    ap.add_argument("--block", default="qwen3-1.7b",
+                    choices=["qwen3-1.7b", "llama3-8b", "qwen3-14b", "qwen3-235b-moe",
+                             "qwen3-235b-moe-skew"],
+                    help="block shape of the step (the default is the headline workload; the "
+                         "others are reported without a CPU baseline)")
     ap.add_argument("--window", type=int, default=1,
                     help="calibrate this many consecutive blocks jointly (sliding-window "
                          "reconstruction; 1 = the single-block step)")
@@ -94,6 +99,31 @@ def counted_traffic(kernel_tag):
             return None
         return float(fields["traffic_bytes_per_launch"])
     return None
+
+
+def workload_config(args, cfg):
+    """The JSON `config` object: the workload named by what it is, its sizes."""
+    moe = hasattr(cfg, "n_experts")
+    shape = {"qwen3-1.7b": "qwen3-1.7b", "llama3-8b": "llama3-8b", "qwen3-14b": "qwen3-14b",
+             "qwen3-235b-moe": "qwen3-235b-a22b routed-expert",
+             "qwen3-235b-moe-skew": "qwen3-235b-a22b routed-expert (skewed expert loads)"}
+    name = shape[args.block] + "-shaped decoder block"
+    if args.window > 1:
+        name = f"window of {args.window} {name}s"
+    name += (f", {cfg.batch} x {cfg.seq} tokens, one CAT-Q calibration step (LM+ST s=15, fwd, "
+             "loss, bwd to factors, ternarise+pack)")
+    if args.a8:
+        name += ", W1.58A8 (8-bit activations)"
+    conf = {"workload": name, "hidden": cfg.hidden, "heads": [cfg.n_q, cfg.n_kv, cfg.head_dim],
+            "tokens": cfg.tokens, "group_size": 128}
+    if moe:
+        n_w = sum(a * b for a, b in cfg.attn_shapes().values())
+        n_w += sum(e * a * b for e, a, b in cfg.expert_shapes().values())
+        conf.update({"experts": cfg.n_experts, "top_k": cfg.top_k, "expert_ffn": cfg.expert_ffn,
+                     "weights": n_w})
+    else:
+        conf.update({"ffn": cfg.ffn, "weights": cfg.n_weights()})
+    return conf
 
 
 def cpu_baseline(cfg, W, xb, row_frac=8):
@@ -271,16 +301,25 @@ def main():
         ternary_bench(args)
         return
 
-    cfg = sg.QWEN3_1P7B
+    cfg = {"qwen3-1.7b": sg.QWEN3_1P7B, "llama3-8b": sg.LLAMA3_8B, "qwen3-14b": sg.QWEN3_14B,
+           "qwen3-235b-moe": sg.QWEN3_235B_MOE,
+           "qwen3-235b-moe-skew": sg.QWEN3_235B_MOE_SKEW}[args.block]
+    moe = hasattr(cfg, "n_experts")
+    if (moe or args.block != "qwen3-1.7b") and (args.window > 1 or args.a8):
+        sys.exit("--window and --a8 run on the qwen3-1.7b-shaped dense block only")
     W = sg.block_weights(cfg, 0)
     xb = sg.activations(cfg, 0)
-    if args.window > 1:
+    if moe:
+        from paper_2606_26650_amd.block import MoEBlock
+        blk = MoEBlock(cfg, W, sg.router_logits(cfg, 0))
+    elif args.window > 1:
         from paper_2606_26650_amd.window import Window
         blk = Window([DenseBlock(cfg, W, a8=args.a8)] +
                      [DenseBlock(cfg, sg.block_weights(cfg, i), a8=args.a8)
                       for i in range(1, args.window)])
     else:
         blk = DenseBlock(cfg, W, a8=args.a8)
+    del W
     x = bf16_tensor(xb)
     y_fp = blk.new_output()
     blk.target(x, y_fp)
@@ -359,14 +398,7 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": ("qwen3-1.7b-shaped decoder block" if args.window == 1 else
-                                f"window of {args.window} qwen3-1.7b-shaped decoder blocks") +
-                               ", 4 x 2048 tokens, one CAT-Q calibration step (LM+ST s=15, fwd, "
-                               "loss, bwd to factors, ternarise+pack)" +
-                               (", W1.58A8 (8-bit activations)" if args.a8 else ""),
-                   "hidden": cfg.hidden, "heads": [cfg.n_q, cfg.n_kv, cfg.head_dim],
-                   "ffn": cfg.ffn, "tokens": cfg.tokens, "group_size": 128,
-                   "weights": cfg.n_weights()},
+        "config": workload_config(args, cfg),
         "roofline": {
             "bound": "mfma",
             "kernel": dom_tag,
@@ -390,8 +422,8 @@ def main():
         "lmst_bwd_gbs": lmb["bytes"] / (lmb["ms"] * 1e-3) / 1e9 if lmb["ms"] else None,
         "loss": loss,
     }
-    if not args.no_cpu_baseline and args.window == 1 and not args.a8:
-        out["cpu_baseline"] = cpu_baseline(cfg, W, xb)
+    if not args.no_cpu_baseline and args.window == 1 and not args.a8 and args.block == "qwen3-1.7b":
+        out["cpu_baseline"] = cpu_baseline(cfg, sg.block_weights(cfg, 0), xb)
     if args.breakdown:
         shp = {}
         for r in recs:

@@ -23,6 +23,7 @@ namespace catq {
 struct AttnLayout {
   int64_t B, S, Hq, Hkv, d, G, ld;  // ld = (Hq + 2 Hkv) d
   bool flash;                        // fused kernels (head_dim 64 or 128)
+  int hs;                            // flash dK/dV: q heads of a group split over hs blocks
   // saved buffer (byte offsets)
   size_t o_qh, o_kh, o_vh, o_lse, o_p, o_rstd, o_cos, o_sin, o_sc, saved_total;
   // backward workspace
@@ -39,6 +40,20 @@ static AttnLayout attn_layout(const catq_attn_desc* a) {
   L.G = L.Hq / (L.Hkv > 0 ? L.Hkv : 1);
   L.ld = (L.Hq + 2 * L.Hkv) * L.d;
   L.flash = (L.d == 64 || L.d == 128);
+  // The dK/dV kernel runs one block per (batch, kv head, 128 keys) and loops
+  // over the group's q heads; with few kv heads (a high q:kv ratio) that is
+  // too few blocks for the chip, so the group's heads are split over hs
+  // blocks (the smallest divisor of G giving >= 512 blocks), each writing
+  // its own partial dK/dV, summed in chunk order by the q/k backward.
+  L.hs = 1;
+  if (L.flash) {
+    const int64_t nb = L.B * L.Hkv * ((L.S + 127) / 128);
+    for (int h = 1; h <= L.G; ++h)
+      if (L.G % h == 0) {
+        L.hs = h;
+        if (nb * h >= 512) break;
+      }
+  }
   size_t off = 0;
   auto take = [&](size_t bytes) {
     size_t o = off;
@@ -66,8 +81,8 @@ static AttnLayout attn_layout(const catq_attn_desc* a) {
   if (L.flash) {
     L.o_dsum = take(BHq * L.S * 4);
     L.o_dq = take(BHq * L.S * L.d * 4);
-    L.o_dk = take(BHk * L.S * L.d * 4);
-    L.o_dv = take(BHk * L.S * L.d * 4);
+    L.o_dk = take((size_t)L.hs * BHk * L.S * L.d * 4);
+    L.o_dv = take((size_t)L.hs * BHk * L.S * L.d * 4);
     L.o_dp = L.o_ds = 0;
   } else {
     L.o_dp = take(BHq * SS * 4);
@@ -350,7 +365,7 @@ __global__ __launch_bounds__(256) void qk_prep_bwd_kernel(
     for (int i = lane; i < d; i += 64) {
       float acc = 0.f;
       if (per_kv)
-        acc = dVp[((b * Hkv + kv) * S + s) * d + i];
+        for (int c = 0; c < per_kv; ++c) acc += dVp[(((c * B + b) * Hkv + kv) * S + s) * d + i];
       else
         for (int gq = 0; gq < G; ++gq) acc += dVp[((b * Hq + kv * G + gq) * S + s) * d + i];
       dst[i] = (bf16)acc;
@@ -367,9 +382,11 @@ __global__ __launch_bounds__(256) void qk_prep_bwd_kernel(
       g1[p] = src[i];
       g2[p] = src[i + half];
     } else if (per_kv) {
-      const float* src = dKp + ((b * Hkv + (h - Hq)) * S + s) * d;
-      g1[p] = src[i];
-      g2[p] = src[i + half];
+      for (int c = 0; c < per_kv; ++c) {
+        const float* src = dKp + (((c * B + b) * Hkv + (h - Hq)) * S + s) * d;
+        g1[p] += src[i];
+        g2[p] += src[i + half];
+      }
     } else {
       const int kv = h - Hq;
       for (int gq = 0; gq < G; ++gq) {
@@ -450,7 +467,7 @@ __global__ __launch_bounds__(256) void qk_prep_bwd_vec_kernel(
   if (h >= Hq + Hkv) {  // v heads: sum over the q heads of the group
     const int kv = h - Hq - Hkv;
     if (per_kv)
-      gather(dVp + ((b * Hkv + kv) * S + s) * d, 0, 1);
+      gather(dVp + ((b * Hkv + kv) * S + s) * d, B * Hkv * S * d, per_kv);
     else
       gather(dVp + ((b * Hq + kv * G) * S + s) * d, S * d, G);
     store8<bf16>(dst + i0, g1);
@@ -460,7 +477,7 @@ __global__ __launch_bounds__(256) void qk_prep_bwd_vec_kernel(
   if (h < Hq)
     gather(dQ + ((b * Hq + h) * S + s) * d, 0, 1);
   else if (per_kv)
-    gather(dKp + ((b * Hkv + (h - Hq)) * S + s) * d, 0, 1);
+    gather(dKp + ((b * Hkv + (h - Hq)) * S + s) * d, B * Hkv * S * d, per_kv);
   else
     gather(dKp + ((b * Hq + (h - Hq) * G) * S + s) * d, S * d, G);
   {
@@ -694,6 +711,7 @@ extern "C" catq_status catq_aux_attention_bwd(const catq_attn_desc* a, const voi
     f.dQ = dQ;
     f.dK = dKp;
     f.dV = dVp;
+    f.hsplit = L.hs;
     f.B = (int)L.B;
     f.S = (int)L.S;
     f.Hq = (int)L.Hq;
@@ -797,12 +815,12 @@ extern "C" catq_status catq_aux_attention_bwd(const catq_attn_desc* a, const voi
                                    dim3(256), 0, stream, (const bf16*)qkv, rstd, cs, sn,
                                    (const float*)dQ, (const float*)dKp, (const float*)dVp, L.B,
                                    L.S, (int)L.Hq, (int)L.Hkv, (int)L.d, (int)L.ld, lph,
-                                   a->qk_norm, L.flash ? 1 : 0, (bf16*)dqkv));
+                                   a->qk_norm, L.flash ? L.hs : 0, (bf16*)dqkv));
   } else {
     hipLaunchKernelGGL(qk_prep_bwd_kernel, dim3((unsigned)((nw + 3) / 4)), dim3(256), 0, stream,
                        (const bf16*)qkv, rstd, cs, sn, (const float*)dQ, (const float*)dKp,
                        (const float*)dVp, L.B, L.S, (int)L.Hq, (int)L.Hkv, (int)L.d, (int)L.ld,
-                       a->qk_norm, L.flash ? 1 : 0, (bf16*)dqkv);
+                       a->qk_norm, L.flash ? L.hs : 0, (bf16*)dqkv);
   }
   CATQ_CHECK_LAUNCH("qk prep bwd");
   return CATQ_OK;

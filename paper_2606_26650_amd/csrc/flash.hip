@@ -341,10 +341,12 @@ __global__ __launch_bounds__(fa::NT, 1) void flash_bwd_dkdv_kernel(FaArgs a) {
   __shared__ u16 sOt[D * fa::TP];      // dO transposed
   __shared__ float sL[fa::BK], sD[fa::BK];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 5, l32 = lane & 31;
-  // grid (B*Hkv, key tiles): the low key tiles see the most queries and are
-  // dispatched first
-  const int kt = blockIdx.y, kvh = blockIdx.x % a.Hkv, b = blockIdx.x / a.Hkv;
-  const int G = a.Hq / a.Hkv;
+  // grid (B*Hkv*hsplit, key tiles): the low key tiles see the most queries
+  // and are dispatched first; block chunk of a kv head takes its share of the
+  // group's q heads and writes its own partial dK/dV
+  const int chunk = blockIdx.x % a.hsplit, bk = blockIdx.x / a.hsplit;
+  const int kt = blockIdx.y, kvh = bk % a.Hkv, b = bk / a.Hkv;
+  const int G = a.Hq / a.Hkv, Gc = G / a.hsplit;
   const int k0 = kt * 128;
   const int kme = k0 + 32 * w + l32;  // this lane's key (column of S^T[q][key])
   const bf16* Kb = a.K + ((int64_t)(b * a.Hkv + kvh) * a.S) * D;
@@ -370,7 +372,7 @@ __global__ __launch_bounds__(fa::NT, 1) void flash_bwd_dkdv_kernel(FaArgs a) {
   const int wave_first = k0 + 32 * w;  // queries below this see none of the wave's keys
   const int qt0 = k0 / fa::BK;
   const int nqt = (a.S + fa::BK - 1) / fa::BK;
-  for (int gq = 0; gq < G; ++gq) {
+  for (int gq = chunk * Gc; gq < (chunk + 1) * Gc; ++gq) {
     const int h = kvh * G + gq;
     const bf16* Qb = a.Q + ((int64_t)(b * a.Hq + h) * a.S) * D;
     const float* Lb = a.lse + (int64_t)(b * a.Hq + h) * a.S;
@@ -434,8 +436,9 @@ __global__ __launch_bounds__(fa::NT, 1) void flash_bwd_dkdv_kernel(FaArgs a) {
     }
   }
   // dv[i][r]: key row = 32w + acc_row(r, g) within the block, d column = 32i + l32
-  float* dKb = a.dK + ((int64_t)(b * a.Hkv + kvh) * a.S) * D;
-  float* dVb = a.dV + ((int64_t)(b * a.Hkv + kvh) * a.S) * D;
+  const int64_t part = (int64_t)chunk * a.B * a.Hkv * a.S * D;
+  float* dKb = a.dK + part + ((int64_t)(b * a.Hkv + kvh) * a.S) * D;
+  float* dVb = a.dV + part + ((int64_t)(b * a.Hkv + kvh) * a.S) * D;
 #pragma unroll
   for (int i = 0; i < C::DB; ++i)
 #pragma unroll
@@ -560,6 +563,8 @@ catq_status flash_forward(int D, FaArgs& a, hipStream_t stream) {
 }
 
 catq_status flash_backward(int D, FaArgs& a, hipStream_t stream) {
+  CATQ_REQUIRE(a.Hkv > 0 && a.Hq % a.Hkv == 0 && a.hsplit >= 1 && (a.Hq / a.Hkv) % a.hsplit == 0,
+               CATQ_ERR_VALUE, "the q-head split must divide the group size");
   const int64_t rows = (int64_t)a.B * a.S * a.Hq;
   dim3 gs((unsigned)((rows * (D / 8) + 255) / 256));
   const double dby = (double)rows * (4.0 * D + 4.0);
@@ -571,7 +576,7 @@ catq_status flash_backward(int D, FaArgs& a, hipStream_t stream) {
                 hipLaunchKernelGGL(flash_dsum_kernel<64>, gs, dim3(256), 0, stream, a));
   CATQ_CHECK_LAUNCH("flash dsum");
   const double half = 0.5 * 2.0 * (double)a.B * a.Hq * (double)a.S * a.S * D;
-  dim3 gkv((unsigned)(a.B * a.Hkv), (unsigned)((a.S + 127) / 128)), block(fa::NT);
+  dim3 gkv((unsigned)(a.B * a.Hkv * a.hsplit), (unsigned)((a.S + 127) / 128)), block(fa::NT);
   if (D == 128)
     CATQ_TRACED(stream, "flash_bwd_dkdv_kernel<128>", 4.0 * half, 0.0, a.S, a.Hkv, D,
                 hipLaunchKernelGGL(flash_bwd_dkdv_kernel<128>, gkv, block, 0, stream, a));

@@ -796,7 +796,10 @@ static const char* tname() {
 // causal attention products), each operand read once and C written once.
 static void gemm_work(const GemmLaunch& L, int out_bytes, double& flops, double& bytes) {
   const GemmArgs& g = L.g;
-  double nb = g.group_mode == 2 ? g.n_groups : (g.group_mode == 1 ? 1 : g.batch);
+  // grouped problems: rows split among the groups (mode 1), or the
+  // contraction split among them (mode 2, K = all groups' rows): either way
+  // 2 M N K in total
+  double nb = g.group_mode != 0 ? 1 : g.batch;
   double f = 2.0 * (double)g.M * (double)g.N * (double)g.K * nb;
   if (g.causal) f *= 0.5;
   flops = f;

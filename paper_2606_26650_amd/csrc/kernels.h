@@ -106,9 +106,10 @@ struct FaArgs {
   const bf16* dO;     // token-major [B*S][Hq*D]
   float* Dsum;        // [B][Hq][S]
   float* dQ;          // [B][Hq][S][D]
-  float* dK;          // [B][Hkv][S][D]
-  float* dV;          // [B][Hkv][S][D]
+  float* dK;          // [hsplit][B][Hkv][S][D]: partial sums over hsplit chunks of q heads
+  float* dV;          // [hsplit][B][Hkv][S][D]
   int B, S, Hq, Hkv;
+  int hsplit;         // blocks a kv head's q heads are split over (divides Hq/Hkv)
   float c;            // softmax scale * log2(e)
   float scale;        // softmax scale
 };

@@ -99,6 +99,8 @@ def test_grouped_experts(catq):
     X, W, dY = to_dev_bf16(xb), to_dev_bf16(wb), to_dev_bf16(dyb)
     offs = torch.from_numpy(off).cuda()
     Y = torch.empty(M, N, dtype=torch.bfloat16, device="cuda")
+    torch.cuda.synchronize()
+    catq.catq_trace_enable(64)
     catq.catq_fakeq_linear_fwd(X, W, Y, M, N, K, n_experts=E, row_offsets=offs)
     ng = E * N * K // 128
     fac = sg.perturbed_factors(6, ng)
@@ -114,6 +116,13 @@ def test_grouped_experts(catq):
     catq.catq_fakeq_linear_bwd(dY, X, wf, M, N, K, W, stats, dm, da, dd, p, *g, ws, dX=dX,
                                dW_fake=dW, n_experts=E, row_offsets=offs)
     torch.cuda.synchronize()
+    recs = [r for r in catq.trace_records() if r["tag"].startswith("gemm")]
+    catq.catq_trace_disable()
+    # forward, dX and G of the routed experts: each is 2 M N K flops in total
+    # over the experts (the rows, or the contraction, split among them)
+    assert len(recs) == 3
+    for r in recs:
+        assert r["flops"] == 2.0 * M * N * K, r
     Xo, Wo, dYo = f64(xb), f64(wb), f64(dyb)
     wfo = lmst.modulate_ternarize(Wo.reshape(E * N, K), 128, *fac, lmst.SOFT,
                                   s=7.0)["W_fake"].reshape(E, N, K)
