@@ -444,7 +444,8 @@ struct DmaOpNT {
       voff[p] = (uint32_t)(mr * ld * 2 + c * 16);
     }
   }
-  __device__ __forceinline__ void issue(uint4* lds, int64_t, int64_t k0, int wave) const {
+  // (K-contiguous rows are whole: the contraction extent is a multiple of 64)
+  __device__ __forceinline__ void issue(uint4* lds, int64_t, int64_t k0, int64_t, int wave) const {
     const uint64_t kb = (uint64_t)k0 * 2;
     const i32x4_rsrc r = buf_rsrc(panel + kb, (uint32_t)min(bytes - kb, (uint64_t)0xFFFFFFFFu));
 #pragma unroll
@@ -483,8 +484,11 @@ struct DmaOpKM {
       voff[p] = (uint32_t)(row * ld * 2 + c * 16);
     }
   }
-  __device__ __forceinline__ void issue(uint4* lds, int64_t ld, int64_t k0, int wave) const {
-    const i32x4_rsrc r = buf_rsrc(panel + (uint64_t)k0 * ld * 2, 64u * ld2);
+  // rows k0 .. min(k0 + 64, kend) - 1 (rows of the slab at or past kend read as zero)
+  __device__ __forceinline__ void issue(uint4* lds, int64_t ld, int64_t k0, int64_t kend,
+                                        int wave) const {
+    const uint32_t rows = (uint32_t)min((int64_t)64, kend - k0);
+    const i32x4_rsrc r = buf_rsrc(panel + (uint64_t)k0 * ld * 2, rows * ld2);
 #pragma unroll
     for (int i = 0; i < NI; ++i)
       dma16_buf(r, voff[i % P], (uint32_t)((i / P) * P * RPI) * ld2, &lds[(wave * NI + i) * 64]);
@@ -508,6 +512,38 @@ struct DmaOpKM {
   }
 };
 
+// Rows grouped by expert (row range off[e] .. off[e+1]): the m-tiles of all
+// experts concatenated.  Each wave finds, with a prefix sum of the experts'
+// tile counts over its lanes (64 experts at a time), the expert and m-tile of
+// concatenated tile t, and the total tile count.  Uniform across the wave.
+__device__ __forceinline__ bool group_tile(const int64_t* off, int E, int t, int bm, int lane,
+                                           int& e_out, int& pm_out, int& total_out) {
+  int base = 0;
+  bool found = false;
+  for (int c0 = 0; c0 < E; c0 += 64) {
+    const int e = c0 + lane;
+    int nt = 0;
+    if (e < E) nt = (int)((off[e + 1] - off[e] + bm - 1) / bm);
+    int incl = nt;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const int y = __shfl_up(incl, d, 64);
+      if (lane >= d) incl += y;
+    }
+    const int chunk = __shfl(incl, 63, 64);
+    if (!found && t < base + chunk) {
+      const unsigned long long m = __ballot(base + incl > t);
+      const int l = __builtin_ctzll(m);
+      e_out = c0 + l;
+      pm_out = t - base - __shfl(incl - nt, l, 64);
+      found = true;
+    }
+    base += chunk;
+  }
+  total_out = base;
+  return found;
+}
+
 template <int BM, int BN, int WGM, int WGN, bool AKM, bool BKM, typename OutT, typename RT,
           bool HAS_R, int EPI = 0>
 __global__ __launch_bounds__(WGM* WGN * 64, 1)
@@ -519,38 +555,77 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
   static_assert(FM >= 1 && FN >= 1 && FM * FN >= FM + FN, "bad tile");
   using OA = std::conditional_t<AKM, DmaOpKM<BM, NW>, DmaOpNT<BM, NW>>;
   using OB = std::conditional_t<BKM, DmaOpKM<BN, NW>, DmaOpNT<BN, NW>>;
-  __shared__ uint4 sA[2][BM * 8];
-  __shared__ uint4 sB[2][BN * 8];
+  // one LDS allocation: the two stages of A, then the two of B (the
+  // epilogue stages the output through all of it)
+  constexpr int LDS_SLOTS = 2 * (BM + BN) * 8;
+  __shared__ uint4 smem[LDS_SLOTS];
+  auto sA = [&](int buf) { return smem + buf * (BM * 8); };
+  auto sB = [&](int buf) { return smem + 2 * BM * 8 + buf * (BN * 8); };
   const GemmArgs& g = L.g;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WGN, wn = wave % WGN;
-  int pm, pn, z;
-  split_tile_coords(blockIdx.x, L.tiles_m, L.tiles_n, L.ksplit, pm, pn, z);
-  const int64_t m0 = (int64_t)pm * BM, n0 = (int64_t)pn * BN;
+  int pm = 0, pn = 0, z = 0;
+  int64_t m0, m_lim = g.M;   // first row of A (rows) and C of the tile; rows below m_lim valid
   int64_t kb = 0, ke = g.K, c_off = 0;
-  if (L.ksplit > 1) {
-    kb = (int64_t)z * L.kchunk;
-    ke = min(g.K, kb + L.kchunk);
-    c_off = (int64_t)z * L.c_split_stride;
+  const bf16* Bb = reinterpret_cast<const bf16*>(g.B);
+  if (g.group_mode == 1) {
+    // rows grouped by expert; blocks past the experts' tiles leave at once
+    // (uniformly: every wave computes the same search)
+    const int t0 = (int)(blockIdx.x / L.tiles_n);
+    int e = 0, pt = 0, tiles = 0;
+    group_tile(g.group_off, g.n_groups, t0, BM, lane, e, pt, tiles);
+    const int n_real = tiles * L.tiles_n;
+    const int lin = blockIdx.x;
+    if (lin >= n_real) return;
+    // Each XCD (round-robin dispatch) takes a contiguous range of the real
+    // tile ids, ordered expert by expert, then n-tile, then m-tile: the few
+    // m-tiles of an expert that share one of its weight panels run back to
+    // back on one L2, so each expert's weight is fetched about once.
+    const int x = lin & 7, q = n_real >> 3, r = n_real & 7;
+    const int v = x * q + min(x, r) + (lin >> 3);
+    group_tile(g.group_off, g.n_groups, v / L.tiles_n, BM, lane, e, pt, tiles);
+    const int64_t r0 = g.group_off[e];
+    m_lim = g.group_off[e + 1];
+    const int te = (int)((m_lim - r0 + BM - 1) / BM);              // the expert's m-tiles
+    const int local = v - (v / L.tiles_n - pt) * L.tiles_n;        // id within the expert
+    pn = local / te;
+    m0 = r0 + (int64_t)(local - pn * te) * BM;
+    Bb += (int64_t)e * g.b_gs;
+  } else {
+    split_tile_coords(blockIdx.x, L.tiles_m, L.tiles_n,
+                      g.group_mode == 2 ? g.n_groups : L.ksplit, pm, pn, z);
+    m0 = (int64_t)pm * BM;
+    if (g.group_mode == 2) {
+      // contraction grouped by expert (ragged): rows past the group's end
+      // read as zero; an empty group writes a zero tile
+      kb = g.group_off[z];
+      ke = g.group_off[z + 1];
+      c_off = (int64_t)z * g.c_gs;
+    } else if (L.ksplit > 1) {
+      kb = (int64_t)z * L.kchunk;
+      ke = min(g.K, kb + L.kchunk);
+      c_off = (int64_t)z * L.c_split_stride;
+    }
   }
+  const int64_t n0 = (int64_t)pn * BN;
   OA oa;
   OB ob;
-  oa.init(reinterpret_cast<const bf16*>(g.A), g.lda, m0, g.M, wave, lane);
+  oa.init(reinterpret_cast<const bf16*>(g.A), g.lda, m0, m_lim, wave, lane);
   if constexpr (EPI == 1)
-    ob.init_pairs(reinterpret_cast<const bf16*>(g.B), g.ldb, n0, g.N / 2, wave, lane);
+    ob.init_pairs(Bb, g.ldb, n0, g.N / 2, wave, lane);
   else
-    ob.init(reinterpret_cast<const bf16*>(g.B), g.ldb, n0, g.N, wave, lane);
+    ob.init(Bb, g.ldb, n0, g.N, wave, lane);
   bf16x8 fa[2][FM], fb[2][FN];
   auto ldfrag = [&](int buf, int kk, int slot) {
 #pragma unroll
-    for (int i = 0; i < FM; ++i) fa[slot][i] = oa.frag(sA[buf], wm * WTM + 32 * i, kk, lane);
+    for (int i = 0; i < FM; ++i) fa[slot][i] = oa.frag(sA(buf), wm * WTM + 32 * i, kk, lane);
 #pragma unroll
-    for (int j = 0; j < FN; ++j) fb[slot][j] = ob.frag(sB[buf], wn * WTN + 32 * j, kk, lane);
+    for (int j = 0; j < FN; ++j) fb[slot][j] = ob.frag(sB(buf), wn * WTN + 32 * j, kk, lane);
   };
   auto issue = [&](int buf, int64_t k0) {
-    oa.issue(sA[buf], g.lda, k0, wave);
-    ob.issue(sB[buf], g.ldb, k0, wave);
+    oa.issue(sA(buf), g.lda, k0, ke, wave);
+    ob.issue(sB(buf), g.ldb, k0, ke, wave);
   };
   f32x16 acc[FM][FN];
 #pragma unroll
@@ -600,7 +675,7 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
     mfmas(1);
     if (MORE) interleave();
   };
-  const int nk = (int)((ke - kb) / 64);
+  const int nk = (int)((ke - kb + 63) / 64);
   if (nk > 0) {
     issue(0, kb);
     wait_vmem();
@@ -624,10 +699,10 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
     constexpr int LPR = WTN / 4, RPP = 64 / LPR;  // lanes per row, rows per pass
     // rows staged per LDS round trip: the whole 32-row slab when every wave's
     // share fits in the operand buffers, else half of it (16 waves)
-    constexpr int SR = (NW * 32 * EP * 4 <= (int)sizeof(sA) + (int)sizeof(sB)) ? 32 : 16;
+    constexpr int SR = (NW * 32 * EP * 4 <= LDS_SLOTS * 16) ? 32 : 16;
     constexpr int NP = SR / RPP;                  // passes per staged part
-    static_assert(NW * SR * EP * 4 <= (int)sizeof(sA) + (int)sizeof(sB), "epilogue staging");
-    float* st = reinterpret_cast<float*>(&sA[0][0]) + wave * (SR * EP);
+    static_assert(NW * SR * EP * 4 <= LDS_SLOTS * 16, "epilogue staging");
+    float* st = reinterpret_cast<float*>(smem) + wave * (SR * EP);
     const int cc = (lane % LPR) * 4;
     const int64_t n = n0 + wn * WTN + cc;
     const int64_t n_c = min(n, g.N - 4);   // clamped column for the early loads
@@ -645,7 +720,7 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
         [[maybe_unused]] uint2 gv[NP], uv[NP];
 #pragma unroll
         for (int q = 0; q < NP; ++q) {
-          const int64_t m_c = min(mrow + q * RPP + lane / LPR, g.M - 1);
+          const int64_t m_c = min(mrow + q * RPP + lane / LPR, m_lim - 1);
           if constexpr (EPI == 2) {
             const bf16* gu = reinterpret_cast<const bf16*>(g.aux0) + m_c * g.ld_aux;
             gv[q] = raw4(gu + n_c);
@@ -666,7 +741,7 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
           const int rr = q * RPP + lane / LPR;
           const int64_t m = mrow + rr;
           f32x4 v = *reinterpret_cast<const f32x4*>(st + rr * EP + cc);
-          if (m < g.M && n < g.N) {
+          if (m < m_lim && n < g.N) {
             v *= g.alpha;
             if constexpr (EPI == 1) {
               // columns n..n+3 = gate_p, up_p, gate_p+1, up_p+1 (p = n/2), each
@@ -714,7 +789,7 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int64_t m = m0 + wm * WTM + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-          if (m >= g.M) continue;
+          if (m >= m_lim) continue;
           float v = acc[i][j][r] * g.alpha;
           if (HAS_R) v += to_f(R[m * g.ldr + n]);
           store_out<OutT>(C + m * g.ldc + n, v);
@@ -842,14 +917,16 @@ template <int BM, int BN, int WGM, int WGN, bool AKM, bool BKM, typename OutT, t
           int EPI = 0>
 static void launch_dma(GemmLaunch& L, hipStream_t stream) {
   const GemmArgs& g = L.g;
-  L.tiles_m = (int)((g.M + BM - 1) / BM);
+  // grouped rows: at most ceil(M/BM) + E m-tiles over all experts together
+  L.tiles_m = (int)((g.M + BM - 1) / BM) + (g.group_mode == 1 ? g.n_groups : 0);
   L.tiles_n = (int)((g.N + BN - 1) / BN);
-  dim3 grid((unsigned)(L.tiles_m * L.tiles_n * L.ksplit));
+  dim3 grid((unsigned)(L.tiles_m * L.tiles_n * (g.group_mode == 2 ? g.n_groups : L.ksplit)));
   dim3 block(WGM * WGN * 64);
   char tag[112];
-  std::snprintf(tag, sizeof(tag), "gemm_dma_kernel<%d, %d, %d, %d, %s%s, %s, %s, %s%s>", BM, BN,
+  std::snprintf(tag, sizeof(tag), "gemm_dma_kernel<%d, %d, %d, %d, %s%s, %s, %s, %s%s%s>", BM, BN,
                 WGM, WGN, AKM ? "k" : "n", BKM ? "k" : "t", tname<OutT>(), tname<RT>(),
-                g.R ? "true" : "false", EPI == 1 ? ", swiglu" : (EPI == 2 ? ", swiglu_bwd" : ""));
+                g.R ? "true" : "false", EPI == 1 ? ", swiglu" : (EPI == 2 ? ", swiglu_bwd" : ""),
+                g.group_mode ? ", experts" : "");
   double flops, bytes;
   gemm_work(L, (int)sizeof(OutT), flops, bytes);
   if (EPI == 1) bytes += (double)g.M * (double)(g.N / 2) * 2.0;          // a written
@@ -869,7 +946,11 @@ static void launch_dma(GemmLaunch& L, hipStream_t stream) {
 // needs its tile extent to divide the matrix extent.
 static bool dma_ok(const GemmLaunch& L, int a_t, int b_t, int bm, int bn) {
   const GemmArgs& g = L.g;
-  return g.group_mode == 0 && g.causal == 0 && g.batch == 1 && g.K % 64 == 0 &&
+  // grouped: rows by expert with A K-contiguous, or the contraction by
+  // expert with both operands K-major (ragged groups read zero past their end)
+  const bool grouping = g.group_mode == 0 || (g.group_mode == 1 && a_t == 0) ||
+                        (g.group_mode == 2 && a_t == 1 && b_t == 1);
+  return grouping && g.causal == 0 && g.batch == 1 && (g.group_mode == 2 || g.K % 64 == 0) &&
          (L.ksplit <= 1 || L.kchunk % 64 == 0) && g.lda % 8 == 0 && g.ldb % 8 == 0 &&
          g.lda < (1 << 22) && g.ldb < (1 << 22) &&  // 32-bit buffer offsets within a tile
          aligned16(g.A) && aligned16(g.B) && (a_t == 0 || g.M % bm == 0) &&
@@ -879,12 +960,22 @@ static bool dma_ok(const GemmLaunch& L, int a_t, int b_t, int bm, int bn) {
 template <int A_T, int B_T, typename OutT, typename RT>
 static void launch_bf16(GemmLaunch& L, hipStream_t stream) {
   const GemmArgs& g = L.g;
-  const int64_t t256 = ((g.M + 255) / 256) * ((g.N + 255) / 256) * L.ksplit;
-  if (g.M >= 256 && g.N >= 256 && t256 >= 256 && dma_ok(L, A_T, B_T, 256, 256)) {
+  if (g.group_mode == 1 && g.N >= 256 && dma_ok(L, A_T, B_T, 128, 256)) {
+    // routed experts' rows: 128-row tiles waste less on each expert's last tile
+    launch_dma<128, 256, 2, 4, A_T == 1, B_T == 1, OutT, RT>(L, stream);
+    return;
+  }
+  if (g.group_mode == 2 && dma_ok(L, A_T, B_T, 256, 256)) {
     launch_dma<256, 256, 4, 4, A_T == 1, B_T == 1, OutT, RT>(L, stream);
     return;
   }
-  if (dma_ok(L, A_T, B_T, 128, 128)) {
+  const int64_t t256 = ((g.M + 255) / 256) * ((g.N + 255) / 256) * L.ksplit;
+  if (g.group_mode == 0 && g.M >= 256 && g.N >= 256 && t256 >= 256 &&
+      dma_ok(L, A_T, B_T, 256, 256)) {
+    launch_dma<256, 256, 4, 4, A_T == 1, B_T == 1, OutT, RT>(L, stream);
+    return;
+  }
+  if (g.group_mode == 0 && dma_ok(L, A_T, B_T, 128, 128)) {
     launch_dma<128, 128, 2, 2, A_T == 1, B_T == 1, OutT, RT>(L, stream);
     return;
   }

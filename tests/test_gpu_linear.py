@@ -86,11 +86,16 @@ def test_bwd_hard_and_identity(catq):
     _bwd_case(catq, 300, 256, 256, catq.IDENTITY)
 
 
-def test_grouped_experts(catq):
+@pytest.mark.parametrize("E,N,K,counts", [
+    (5, 256, 384, [130, 0, 7, 300, 64]),
+    # extents that the direct-to-LDS kernels take for all three products
+    # (rows by expert, and the contraction by expert with ragged ends)
+    (4, 512, 768, [300, 0, 77, 650]),
+    (3, 256, 256, [1, 513, 64])])
+def test_grouped_experts(catq, E, N, K, counts):
     """Routed experts with uneven row counts, one expert empty."""
     import torch
-    E, N, K = 5, 256, 384
-    counts = np.array([130, 0, 7, 300, 64])
+    counts = np.array(counts)
     off = np.concatenate([[0], np.cumsum(counts)]).astype(np.int64)
     M = int(off[-1])
     xb = sg.normal_bf16(5, "X", (M, K))
@@ -137,7 +142,8 @@ def test_grouped_experts(catq):
     assert max_norm_err(host(Y), Yref) <= 4e-3
     assert max_norm_err(host(dX), dXref) <= 2e-2
     assert max_norm_err(host(dW), Gref) <= 1e-4
-    assert np.all(host(dW)[1] == 0)             # the empty expert
+    for e in np.flatnonzero(counts == 0):       # an empty expert
+        assert np.all(host(dW)[e] == 0)
     ref = lmst.factor_grads(Gref.reshape(E * N, K), Wo.reshape(E * N, K), 128, *fac, lmst.SOFT,
                             s=7.0)
     for a, b in zip(g, ref):
