@@ -969,8 +969,11 @@ static void launch_bf16(GemmLaunch& L, hipStream_t stream) {
     launch_dma<256, 256, 4, 4, A_T == 1, B_T == 1, OutT, RT>(L, stream);
     return;
   }
+  // the 256 x 256 tile from 160 tiles on (5/8 of the compute units busy in
+  // one round still beats 128 x 128 tiles on 4 waves: the 2048 x 6144 weight
+  // gradient over 8192 tokens, unsplit, takes 216 against 260 us)
   const int64_t t256 = ((g.M + 255) / 256) * ((g.N + 255) / 256) * L.ksplit;
-  if (g.group_mode == 0 && g.M >= 256 && g.N >= 256 && t256 >= 256 &&
+  if (g.group_mode == 0 && g.M >= 256 && g.N >= 256 && t256 >= 160 &&
       dma_ok(L, A_T, B_T, 256, 256)) {
     launch_dma<256, 256, 4, 4, A_T == 1, B_T == 1, OutT, RT>(L, stream);
     return;
@@ -1062,7 +1065,7 @@ catq_status gemm_run_epi(const GemmArgs& a, int a_t, int b_t, hipStream_t stream
   // plain GEMM takes the same 256 x 256 kernel, so fused and unfused results
   // are the same bits
   const int64_t t256 = ((a.M + 255) / 256) * ((a.N + 255) / 256);
-  const bool shape = t256 >= 256 && a.R == nullptr && a.alpha == 1.0f && a.N % 4 == 0 &&
+  const bool shape = t256 >= 160 && a.R == nullptr && a.alpha == 1.0f && a.N % 4 == 0 &&
                      a.ldc % 4 == 0 && a.ld_aux % 4 == 0 && aligned16(a.C) && aligned16(a.aux0) &&
                      (a.epi == 1 || aligned16(a.aux1));
   if (a.epi == 1) {

@@ -8,19 +8,24 @@ namespace catq {
 // whole compute unit (128 KB of LDS), so the (N/256)x(K/256) tiles times the
 // splits run in ceil(tiles * ks / 256) rounds, each as long as its share of
 // the tokens (64 per iteration) plus the fixed cost of writing a 256x256
-// fp32 partial (about 10 iterations, measured).  The split with the least
-// estimated time wins; each split keeps >= 1024 tokens.  (This picks the
-// measured best for every projection shape of the benchmarked block.)
+// fp32 partial (about 10 iterations, measured).  The factor-gradient pass
+// then reads every partial once: N*K*4 bytes per split, about N*K/1.77e6
+// iterations at the read rate it reaches.  The split with the least
+// estimated total wins; each split keeps >= 1024 tokens.  (This picks the
+// measured best of GEMM plus partial reads for every projection shape of
+// the benchmarked block.)
 static int choose_ksplit(int64_t M, int64_t N, int64_t K, int32_t n_experts) {
   if (n_experts > 1) return 1;
   constexpr int64_t kUnits = 256;      // compute units of the MI355X
   constexpr double kEpilogue = 10.0;   // partial write, in 64-token iterations
+  constexpr double kRead = 1.77e6;     // weights whose partial one iteration reads back
   const int64_t tiles = ((N + 255) / 256) * ((K + 255) / 256);
   int best = 1;
   double best_cost = 0.0;
   for (int ks = 1; ks <= 64 && (ks == 1 || M / ks >= 1024); ks *= 2) {
     const int64_t rounds = (tiles * ks + kUnits - 1) / kUnits;
-    const double cost = (double)rounds * ((double)M / (64.0 * ks) + kEpilogue);
+    const double cost = (double)rounds * ((double)M / (64.0 * ks) + kEpilogue) +
+                        (double)ks * (double)N * (double)K / kRead;
     if (ks == 1 || cost < best_cost) {
       best = ks;
       best_cost = cost;
