@@ -21,6 +21,7 @@
 #include <type_traits>
 
 #include "kernels.h"
+#include "lmst_math.h"
 
 namespace catq {
 
@@ -703,6 +704,11 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
     constexpr int NP = SR / RPP;                  // passes per staged part
     static_assert(NW * SR * EP * 4 <= LDS_SLOTS * 16, "epilogue staging");
     float* st = reinterpret_cast<float*>(smem) + wave * (SR * EP);
+    // factor epilogue: the half-group sums of every tile row, past the staging
+    [[maybe_unused]] float* fsum = reinterpret_cast<float*>(smem) + NW * SR * EP;
+    static_assert(EPI != 3 || (BN == 256 && WTN == 64 &&
+                               (NW * SR * EP + BM * 4 * 4) * 4 <= LDS_SLOTS * 16),
+                  "factor epilogue layout");
     const int cc = (lane % LPR) * 4;
     const int64_t n = n0 + wn * WTN + cc;
     const int64_t n_c = min(n, g.N - 4);   // clamped column for the early loads
@@ -727,7 +733,28 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
             uv[q] = raw4(gu + g.N + n_c);
           } else if constexpr (EPI == 0 && HAS_R) {
             rv[q] = raw4(R + m_c * g.ldr + n_c);
+          } else if constexpr (EPI == 3) {
+            gv[q] = raw4(reinterpret_cast<const bf16*>(g.fac.W) + ((int64_t)z * g.M + m_c) * g.N +
+                         n_c);
           }
+        }
+        // factor epilogue: lane l holds the group scalars of the part's row
+        // l % SR (its 64 columns lie in one group), handed to the lanes of
+        // that row by shuffles in each pass
+        [[maybe_unused]] float p_mu = 0.f, p_inva = 0.f, p_delta = 0.f, p_ed = 0.f;
+        [[maybe_unused]] double p_theta = 0.0;
+        if constexpr (EPI == 3) {
+          const FacEpi& F = g.fac;
+          const int64_t wrow = (int64_t)z * g.M + min(mrow + (lane % SR), m_lim - 1);
+          const int64_t grp = wrow * (g.N >> 7) + (n_c >> 7);
+          const GroupScalars gs =
+              group_scalars(F.stats[2 * grp], F.stats[2 * grp + 1], F.dmu[grp * F.s[0]],
+                            F.dal[grp * F.s[1]], F.dde[grp * F.s[2]], F.delta0);
+          p_mu = gs.mu;
+          p_inva = 1.0f / gs.alpha_div;
+          p_delta = gs.delta;
+          p_ed = one_minus_exp_neg(gs.delta * F.st.s4, gs.delta * F.st.s4l);
+          p_theta = (double)gs.delta * (double)gs.alpha_div;
         }
 #pragma unroll
         for (int j = 0; j < FN; ++j)
@@ -741,6 +768,49 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
           const int rr = q * RPP + lane / LPR;
           const int64_t m = mrow + rr;
           f32x4 v = *reinterpret_cast<const f32x4*>(st + rr * EP + cc);
+          if constexpr (EPI == 3) {
+            // G[m][n..n+3] of expert z (one split, alpha 1): the four terms
+            // of the factor gradients over these weights, summed over the 16
+            // lanes of the row's 64 columns (half of a 128-weight group)
+            const FacEpi& F = g.fac;
+            float sT = 0.f, s1 = 0.f, sW = 0.f, sD = 0.f;
+            // this row's group scalars from the lane that holds them
+            const int src = q * RPP + lane / LPR;
+            const float mu = __shfl(p_mu, src, 64), inv_a = __shfl(p_inva, src, 64);
+            const float delta = __shfl(p_delta, src, 64), ED = __shfl(p_ed, src, 64);
+            const double theta = __shfl(p_theta, src, 64);
+            if (m < m_lim && n < g.N && F.mode != CATQ_IDENTITY) {
+              const f32x4 w = widen4(gv[q]);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                const float xs = (w[e] - mu) * inv_a;
+                float f = 0.f, fW = 1.f, fD = 0.f;
+                if (!F.ste) transition_parts(xs, delta, ED, F.st, f, fW, fD);
+                const float T = (F.mode == CATQ_HARD) ? hard_code(w[e], mu, theta) : f;
+                sT = fmaf(v[e], T, sT);
+                const float gf = v[e] * fW;
+                s1 += gf;
+                sW = fmaf(gf, xs, sW);
+                sD = fmaf(v[e], fD, sD);
+              }
+            }
+#pragma unroll
+            for (int mk = 1; mk < 16; mk <<= 1) {
+              sT += __shfl_xor(sT, mk, 64);
+              s1 += __shfl_xor(s1, mk, 64);
+              sW += __shfl_xor(sW, mk, 64);
+              sD += __shfl_xor(sD, mk, 64);
+            }
+            if ((lane & 15) == 0) {
+              // [tile row][group of the tile][half of the group][term]
+              float* d = fsum + ((int)(mrow - m0 + rr) * 4 + wn) * 4;
+              d[0] = sT;
+              d[1] = s1;
+              d[2] = sW;
+              d[3] = sD;
+            }
+            continue;
+          }
           if (m < m_lim && n < g.N) {
             v *= g.alpha;
             if constexpr (EPI == 1) {
@@ -775,6 +845,32 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
               store4f(C + m * g.ldc + n, v);
             }
           }
+        }
+      }
+    }
+    if constexpr (EPI == 3) {
+      // both halves of each group in order, then the three factor gradients
+      // (the separate factor-gradient kernel's formulas)
+      __syncthreads();
+      const FacEpi& F = g.fac;
+      for (int t = tid; t < BM * 2; t += NW * 64) {
+        const int row = t >> 1, gt = t & 1;
+        const float* a0 = fsum + (row * 4 + 2 * gt) * 4;
+        const float sT = a0[0] + a0[4], s1 = a0[1] + a0[5], sW = a0[2] + a0[6], sD = a0[3] + a0[7];
+        const int64_t grp = ((int64_t)z * g.M + m0 + row) * (g.N >> 7) + (n0 >> 7) + gt;
+        const float alpha0 = F.stats[2 * grp + 1];
+        const GroupScalars gs = group_scalars(F.stats[2 * grp], alpha0, F.dmu[grp * F.s[0]],
+                                              F.dal[grp * F.s[1]], F.dde[grp * F.s[2]], F.delta0);
+        float o[3];
+        o[0] = alpha0 * (-s1);
+        o[1] = alpha0 * (sT - sW);
+        o[2] = F.delta0 * (gs.alpha * sD);
+#pragma unroll
+        for (int k = 0; k < 3; ++k) {
+          if (F.s[k] == 1)
+            F.out[k][grp] = o[k];
+          else
+            F.ws[k * F.n_groups + grp] = o[k];
         }
       }
     }
@@ -925,12 +1021,17 @@ static void launch_dma(GemmLaunch& L, hipStream_t stream) {
   char tag[112];
   std::snprintf(tag, sizeof(tag), "gemm_dma_kernel<%d, %d, %d, %d, %s%s, %s, %s, %s%s%s>", BM, BN,
                 WGM, WGN, AKM ? "k" : "n", BKM ? "k" : "t", tname<OutT>(), tname<RT>(),
-                g.R ? "true" : "false", EPI == 1 ? ", swiglu" : (EPI == 2 ? ", swiglu_bwd" : ""),
+                g.R ? "true" : "false",
+                EPI == 1 ? ", swiglu" : (EPI == 2 ? ", swiglu_bwd" : (EPI == 3 ? ", factor_grads" : "")),
                 g.group_mode ? ", experts" : "");
   double flops, bytes;
   gemm_work(L, (int)sizeof(OutT), flops, bytes);
   if (EPI == 1) bytes += (double)g.M * (double)(g.N / 2) * 2.0;          // a written
   if (EPI == 2) bytes += (double)g.M * (double)g.N * 2.0 * 4.0 - (double)g.M * g.N * sizeof(OutT);
+  if (EPI == 3) {  // W read instead of G written; per group stats, factors, gradients
+    const double w = (double)g.n_groups * g.M * g.N;
+    bytes += w * 2.0 - w * sizeof(OutT) + w / 128.0 * (8.0 + 12.0 + 12.0);
+  }
   if (g.R)
     CATQ_TRACED(stream, tag, flops, bytes, g.M, g.N, g.K,
                 hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WGM, WGN, AKM, BKM, OutT, RT, true, EPI>),
@@ -1082,6 +1183,26 @@ catq_status gemm_run_epi(const GemmArgs& a, int a_t, int b_t, hipStream_t stream
     launch_dma<256, 256, 4, 4, false, true, bf16, bf16, 2>(L, stream);
   }
   CATQ_CHECK_LAUNCH("gemm fused epilogue");
+  return CATQ_OK;
+}
+
+catq_status gemm_run_factor(const GemmArgs& a, hipStream_t stream) {
+  CATQ_REQUIRE(a.epi == 3 && a.group_mode == 2, CATQ_ERR_VALUE, "not a factor-gradient launch");
+  GemmLaunch L;
+  L.g = a;
+  L.ksplit = 1;
+  L.kchunk = a.K;
+  L.c_split_stride = 0;
+  L.tiles_m = L.tiles_n = 0;
+  // G per expert [rows][d_in] from K-major dY and X; whole 256 x 256 tiles
+  // (128-weight groups never straddle them), C only as an aligned dummy
+  const bool shape = a.M > 0 && a.N > 0 && a.M % 256 == 0 && a.N % 256 == 0 && a.alpha == 1.0f &&
+                     a.R == nullptr && a.c_gs == 0 && a.ldc % 4 == 0 && aligned16(a.C) &&
+                     a.fac.W != nullptr && (reinterpret_cast<uintptr_t>(a.fac.W) & 7) == 0 &&
+                     dma_ok(L, 1, 1, 256, 256);
+  if (!shape) return CATQ_ERR_VALUE;
+  launch_dma<256, 256, 4, 4, true, true, float, float, 3>(L, stream);
+  CATQ_CHECK_LAUNCH("gemm factor epilogue");
   return CATQ_OK;
 }
 

@@ -22,6 +22,10 @@ void trace_end(int slot, hipStream_t stream);
 // Factor gradients from G = dL/dW_fake (fp32, [n_rows][d_in]) for one weight
 // matrix (or all experts' matrices stacked along rows).  `ws_shared` holds
 // 3*n_groups floats and is used only when some factor stride is 0.
+// The gradients of stride-0 (one per matrix) factors from their per-group
+// terms in ws[k][n_groups] (fixed-order sum); stride-1 factors untouched.
+catq_status finish_shared_factors(const int64_t* strides, int64_t n_groups, const float* ws,
+                                  float* const* out, hipStream_t stream);
 catq_status launch_factor_grads(const float* G, int nsplit, int64_t split_stride, float* G_out,
                                 const void* W, catq_dtype w_dtype, int64_t n_rows, int64_t d_in,
                                 const float* stats, const float* d_mu, const float* d_alpha,
@@ -47,6 +51,35 @@ catq_status check_lmst_params(const catq_lmst_params* p, int64_t d_in);
 //                 offset by e*b_gs; blockIdx.z = expert
 //   group_mode 2: contraction grouped (k range off[e]..off[e+1]) ; C offset by
 //                 e*c_gs; blockIdx.z = expert
+// Per-launch constants of the transition function f at sharpness s (Eq. 5),
+// formed on the host in double.
+struct StConst {
+  float c2s;   // 2 s log2(e):  q_a = 2^(-|x - D| * c2s)
+  float s4;    // 4 s:          t = 4 s x
+  float s4l;   // 4 s log2(e)
+  float k2;    // 1 / tanh(s)   (f = (tanh a + tanh b) * k2 / 2)
+  float sk4;   // 2 s / tanh(s) (f_W, f_D prefactor)
+};
+
+// Factor-gradient epilogue (EPI 3) of the per-expert weight gradient G_e:
+// instead of G, the gradients of the three learnable factors of every
+// 128-weight group of W_e (the reductions of Sec. 2.3), as the separate
+// factor-gradient kernel computes them from G.
+struct FacEpi {
+  const void* W;          // bf16 weights [E][rows][d_in]
+  const float* stats;     // [n_groups][2] mu0, alpha0
+  const float* dmu;
+  const float* dal;
+  const float* dde;
+  float* out[3];          // per-group gradients (factor stride 1)
+  float* ws;              // [3][n_groups] per-group terms of stride-0 factors
+  int64_t n_groups;
+  int64_t s[3];           // factor strides (1, or 0 = one value per matrix)
+  int32_t mode, ste;
+  float delta0;
+  StConst st;
+};
+
 struct GemmArgs {
   const void* A;
   const void* B;
@@ -72,10 +105,13 @@ struct GemmArgs {
   //  2 (SwiGLU backward): C is the gradient of a [M][N]; aux0 holds the
   //    forward's [gate | up] [M][2N] and aux1 receives d[gate | up] (ld_aux);
   //    C itself is not written
+  //  3 (factor gradients, group_mode 2, both operands K-major): see FacEpi;
+  //    C is not written
   int32_t epi;
   void* aux0;
   void* aux1;
   int64_t ld_aux;
+  FacEpi fac;
 };
 
 GemmArgs gemm_args_default();
@@ -95,6 +131,10 @@ int gemm_split_count(const GemmArgs& a, int ksplit);
 // the direct-to-LDS kernel's vector epilogue (the caller then runs the
 // unfused pair of kernels).
 catq_status gemm_run_epi(const GemmArgs& a, int a_t, int b_t, hipStream_t stream);
+// Per-expert weight gradients reduced to factor gradients in the epilogue
+// (a.epi = 3, a.fac filled, group_mode 2); CATQ_ERR_VALUE when the shape is
+// not eligible (then nothing was launched).
+catq_status gemm_run_factor(const GemmArgs& a, hipStream_t stream);
 
 // ---------------------------------------------------------- fused attention
 struct FaArgs {

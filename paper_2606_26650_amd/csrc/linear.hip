@@ -1,6 +1,7 @@
 // C ABI of the fake-ternary linear layer: forward, and backward to the input
 // and to the learnable factors (Sec. 2.2-2.4).
 #include "kernels.h"
+#include "lmst_math.h"
 
 namespace catq {
 
@@ -256,6 +257,36 @@ extern "C" catq_status catq_fakeq_linear_bwd(
       a.group_mode = 2;
       a.group_off = row_offsets;
       a.n_groups = n_experts;
+      if (dW_fake == nullptr && p->group_size == 128 && dtype == CATQ_BF16 &&
+          w_dtype == CATQ_BF16) {
+        // every G element is final in one tile (no split): the factor
+        // gradients come out of the GEMM's epilogue and G never reaches memory
+        GemmArgs f = a;
+        f.epi = 3;
+        f.c_gs = 0;  // C is only an aligned dummy
+        FacEpi& fe = f.fac;
+        fe.W = W;
+        fe.stats = stats;
+        fe.dmu = d_mu;
+        fe.dal = d_alpha;
+        fe.dde = d_delta;
+        fe.out[0] = g_d_mu;
+        fe.out[1] = g_d_alpha;
+        fe.out[2] = g_d_delta;
+        fe.ws = shared_ws;
+        fe.n_groups = E * N * K / 128;
+        for (int i = 0; i < 3; ++i) fe.s[i] = p->factor_stride[i];
+        fe.mode = p->mode;
+        fe.ste = (p->mode == CATQ_HARD && p->s_bwd == 0.0f) ? 1 : 0;
+        fe.delta0 = p->delta0;
+        const double s_use = (p->mode == CATQ_HARD) ? (double)p->s_bwd : (double)p->s;
+        fe.st = make_st(s_use > 0 ? s_use : 1.0);
+        const catq_status st = gemm_run_factor(f, stream);
+        if (st == CATQ_OK)
+          return finish_shared_factors(fe.s, fe.n_groups, shared_ws, fe.out, stream);
+        if (st != CATQ_ERR_VALUE) return st;
+        clear_error();
+      }
       a.c_gs = N * K;
       CATQ_TRY(gemm_run(a, 1, 1, dtype, CATQ_F32, stream));
     } else {

@@ -1,0 +1,101 @@
+// Element-wise mathematics of the learnable modulation and the softened
+// ternarisation (Sec. 2.2-2.3, Eq. 2-6), shared by the LM+ST kernels and by
+// the weight-gradient GEMM's fused factor-gradient epilogue.
+#pragma once
+
+#include <cmath>
+
+#include "kernels.h"
+
+namespace catq {
+
+// Constants of f at sharpness s (StConst), formed on the host in double.
+static inline StConst make_st(double s) {
+  StConst c;
+  const double l2e = 1.4426950408889634;
+  c.c2s = (float)(2.0 * s * l2e);
+  c.s4 = (float)(4.0 * s);
+  c.s4l = (float)(4.0 * s * l2e);
+  c.k2 = (float)(1.0 / std::tanh(s));
+  c.sk4 = (float)(2.0 * s / std::tanh(s));
+  return c;
+}
+
+// 1 - exp(-t) for t >= 0 without cancellation: a degree-7 Taylor polynomial
+// below t = 1/4 (truncation < 2e-9 relative), the exponential above it.
+__device__ __forceinline__ float one_minus_exp_neg(float t, float t_log2e) {
+  if (t < 0.25f) {
+    float p = 1.0f / 5040.0f;
+    p = fmaf(p, t, -1.0f / 720.0f);
+    p = fmaf(p, t, 1.0f / 120.0f);
+    p = fmaf(p, t, -1.0f / 24.0f);
+    p = fmaf(p, t, 1.0f / 6.0f);
+    p = fmaf(p, t, -0.5f);
+    p = fmaf(p, t, 1.0f);
+    return t * p;
+  }
+  return 1.0f - __builtin_amdgcn_exp2f(-t_log2e);
+}
+
+// Per-group scalars of Eq. 3-4 from fp32 stats and factors.  mu and alpha are
+// formed in double (the products of two fp32 values are exact there) and
+// rounded once to fp32; Delta likewise.
+struct GroupScalars {
+  float mu, alpha, alpha_div, delta;
+};
+
+__device__ __forceinline__ GroupScalars group_scalars(float mu0, float alpha0, float dmu, float dal,
+                                                      float dde, float delta0) {
+  GroupScalars g;
+  g.mu = (float)((double)mu0 + (double)dmu * (double)alpha0);
+  g.alpha = (float)((double)dal * (double)alpha0);
+  g.delta = (float)((double)dde * (double)delta0);
+  g.alpha_div = fmaxf(g.alpha, 1.17549435e-38f);  // smallest normal: constant groups stay finite
+  if (g.alpha != g.alpha) g.alpha_div = g.alpha;  // keep NaN
+  return g;
+}
+
+// Exact hard decision of Eq. 2 on W_hat = (w - mu)/alpha against Delta,
+// without dividing: compare r = w - mu with theta = Delta*alpha in double.
+__device__ __forceinline__ float hard_code(float w, float mu, double theta) {
+  double r = (double)w - (double)mu;
+  return (float)((r > theta) - (r < -theta));
+}
+
+// Transition function f of Eq. 5 at x_hat (cancellation-free form).
+__device__ __forceinline__ float transition_f(float xs, float delta, float ED, const StConst& c) {
+  float x = fabsf(xs);
+  float d = x - delta;
+  float qa = __builtin_amdgcn_exp2f(-fabsf(d) * c.c2s);
+  float E = one_minus_exp_neg(x * c.s4, x * c.s4l);
+  bool ge = d >= 0.0f;
+  float eb = ge ? ED : E;
+  float qb = fmaf(-qa, eb, qa);
+  float den = (1.0f + qa) * (1.0f + qb);
+  float num = ge ? E : qa * E;
+  float F = num * __builtin_amdgcn_rcpf(den) * c.k2;
+  return copysignf(F, xs);
+}
+
+// f, f_W and f_Delta together (backward).
+__device__ __forceinline__ void transition_parts(float xs, float delta, float ED, const StConst& c,
+                                                 float& f, float& fW, float& fD) {
+  float x = fabsf(xs);
+  float d = x - delta;
+  float qa = __builtin_amdgcn_exp2f(-fabsf(d) * c.c2s);
+  float E = one_minus_exp_neg(x * c.s4, x * c.s4l);
+  bool ge = d >= 0.0f;
+  float eb = ge ? ED : E;
+  float qb = fmaf(-qa, eb, qa);
+  float ra = __builtin_amdgcn_rcpf(1.0f + qa);
+  float rb = __builtin_amdgcn_rcpf(1.0f + qb);
+  float num = ge ? E : qa * E;
+  f = copysignf(num * ra * rb * c.k2, xs);
+  float ra2 = ra * ra, rb2 = rb * rb;
+  fW = c.sk4 * fmaf(qa, ra2, qb * rb2);
+  float om = ge ? E : ED;  // 1 - qa*qb
+  fD = copysignf(c.sk4 * (qa * eb) * om * (ra2 * rb2), -xs);
+  if (xs == 0.0f) fD = 0.0f;
+}
+
+}  // namespace catq

@@ -150,6 +150,65 @@ def test_grouped_experts(catq, E, N, K, counts):
         assert max_norm_err(host(a), b) <= 2e-2
 
 
+@pytest.mark.parametrize("mode,s_bwd,strides", [
+    (lmst.SOFT, 30.0, (1, 1, 1)), (lmst.HARD, 30.0, (1, 1, 1)), (lmst.HARD, 0.0, (1, 1, 1)),
+    (lmst.SOFT, 30.0, (1, 1, 0))])
+def test_grouped_factor_epilogue(catq, mode, s_bwd, strides):
+    """Routed experts whose weight gradients are reduced to factor gradients
+    in the GEMM epilogue (no dW_fake requested, 128-weight groups, extents
+    that are multiples of 256): against the oracle, and against the separate
+    factor-gradient kernel on the materialised G (requested through
+    dW_fake), which sums the same terms in another order."""
+    import torch
+    E, N, K = 3, 512, 256
+    counts = np.array([300, 0, 177])
+    off = np.concatenate([[0], np.cumsum(counts)]).astype(np.int64)
+    M = int(off[-1])
+    xb = sg.normal_bf16(8, "X", (M, K))
+    wb = sg.normal_bf16(8, "W", (E, N, K), std=0.02)
+    dyb = sg.normal_bf16(8, "Y", (M, N), std=1e-3)
+    X, W, dY = to_dev_bf16(xb), to_dev_bf16(wb), to_dev_bf16(dyb)
+    offs = torch.from_numpy(off).cuda()
+    ng = E * N * K // 128
+    fac = list(sg.perturbed_factors(9, ng))
+    if strides[2] == 0:
+        fac[2] = fac[2][:1]
+    dm, da, dd = (to_dev_f32(f) for f in fac)
+    stats = torch.zeros(ng, 2, dtype=torch.float32, device="cuda")
+    wf = torch.empty_like(W)
+    p = catq.lmst_params(mode=mode, s=7.0, s_bwd=s_bwd, strides=strides)
+    catq.catq_modulate_ternarize(W, dm, da, dd, p, stats, 0, W_fake=wf)
+    ws = torch.empty(catq.catq_workspace_size(0, M, N, K, E), dtype=torch.uint8, device="cuda")
+
+    def run(with_dw):
+        g = [torch.full((ng if st else 1,), float("nan"), dtype=torch.float32, device="cuda")
+             for st in strides]
+        dW = torch.empty(E, N, K, dtype=torch.float32, device="cuda") if with_dw else None
+        catq.catq_fakeq_linear_bwd(dY, X, wf, M, N, K, W, stats, dm, da, dd, p, *g, ws,
+                                   dW_fake=dW, n_experts=E, row_offsets=offs)
+        return g
+
+    torch.cuda.synchronize()
+    catq.catq_trace_enable(64)
+    fused = run(False)
+    torch.cuda.synchronize()
+    tags = [r["tag"] for r in catq.trace_records()]
+    catq.catq_trace_disable()
+    assert any("factor_grads" in t for t in tags) and not any(t.startswith("lmst_bwd") for t in tags)
+    sep = run(True)
+    torch.cuda.synchronize()
+    Xo, Wo, dYo = f64(xb), f64(wb), f64(dyb)
+    Gref = np.zeros((E, N, K))
+    for e in range(E):
+        Gref[e] = dYo[off[e]:off[e + 1]].T @ Xo[off[e]:off[e + 1]]
+    ref = lmst.factor_grads(Gref.reshape(E * N, K), Wo.reshape(E * N, K), 128, *fac, mode, s=7.0,
+                            s_bwd=s_bwd, strides=strides)
+    for a, b, r in zip(fused, sep, ref):
+        assert torch.isfinite(a).all()
+        assert max_norm_err(host(a), r) <= 2e-2
+        assert max_norm_err(host(a), host(b)) <= 1e-4
+
+
 def test_fp32_linear(catq):
     import torch
     W, X = sg.single_linear_case(0)
