@@ -126,14 +126,15 @@ def workload_config(args, cfg):
     return conf
 
 
-def cpu_baseline(cfg, W, xb, row_frac=8):
-    """The float64 oracle on a bounded sample of the same step.
+def cpu_baseline(cfg, W, xb, row_frac=1, n_samples=None):
+    """The float64 oracle on a bounded sample of the same step (by default
+    the whole step: about 10 s of host work).
     Weight side (LM+ST forward, factor gradients, final ternarise+pack): the
     first 1/row_frac of the rows of every weight matrix, scaled by row_frac
     (the work is elementwise per group, exactly linear in the weight count).
-    Token side (block forward+backward): ONE of the calibration samples with
-    all weights; samples are independent in the block, so a full step costs
-    t_weights + batch * t_sample."""
+    Token side (block forward+backward): n_samples of the calibration samples
+    (default all), one at a time with all weights; samples are independent in
+    the block, so a full step costs t_weights + batch * (mean t_sample)."""
     import dataclasses
 
     import numpy as np
@@ -152,7 +153,7 @@ def cpu_baseline(cfg, W, xb, row_frac=8):
     Ws = {k: v[: v.shape[0] // row_frac] for k, v in Wo.items()}
     fac_s = {k: sg.init_factors(v.size // 128) for k, v in Ws.items()}
     one = dataclasses.replace(cfg, batch=1)
-    x1 = sg.bf16_bits_to_f32(xb[: cfg.seq]).astype(np.float64)
+    n_samples = cfg.batch if n_samples is None else n_samples
     # weight side on the row sample
     t0 = time.perf_counter()
     calib.fake_weights(Ws, fac_s, 128, lmst.SOFT, 15.0)
@@ -167,18 +168,24 @@ def cpu_baseline(cfg, W, xb, row_frac=8):
     # depend on the weight values, so the bf16 weights stand in for alpha*T
     # and the input for the cached target
     t3 = time.perf_counter()
-    y_q, cache = block.block_forward(x1, Wo, one)
-    loss, dy = block.recon_loss(y_q, x1)
-    block.block_backward(dy, cache, Wo, one)
+    for i in range(n_samples):
+        x1 = sg.bf16_bits_to_f32(xb[i * cfg.seq:(i + 1) * cfg.seq]).astype(np.float64)
+        y_q, cache = block.block_forward(x1, Wo, one)
+        loss, dy = block.recon_loss(y_q, x1)
+        block.block_backward(dy, cache, Wo, one)
+        del cache
     t4 = time.perf_counter()
-    t_sample = t4 - t3
+    t_sample = (t4 - t3) / n_samples
     step = t_weights + cfg.batch * t_sample
+    rows = "all rows" if row_frac == 1 else f"1/{row_frac} of the rows"
     return {"value": 1.0 / step, "unit": "block-steps/s", "cores": cores, "kind": "oracle",
             "sample": (f"float64 oracle, {cores} BLAS threads: LM+ST forward, factor gradients "
-                       f"and ternarise+pack on 1/{row_frac} of the rows of every weight "
-                       f"({(t2 - t0):.1f} s, x{row_frac}) plus block forward+backward of 1 of "
-                       f"the {cfg.batch} samples of {cfg.seq} tokens ({t_sample:.1f} s, "
-                       f"x{cfg.batch}); full-precision target excluded"),
+                       f"and ternarise+pack on {rows} of every weight ({(t2 - t0):.1f} s"
+                       f"{'' if row_frac == 1 else f', x{row_frac}'}) plus block "
+                       f"forward+backward of {n_samples} of the {cfg.batch} samples of "
+                       f"{cfg.seq} tokens, one at a time ({t4 - t3:.1f} s"
+                       f"{'' if n_samples == cfg.batch else f', x{cfg.batch / n_samples:g}'}); "
+                       "full-precision target excluded"),
             "seconds_per_step": step}
 
 
