@@ -5,19 +5,22 @@
 //   forward  Y  = X . W_fake^T      both operands contiguous along K
 //   input    dX = dY . W_fake       W_fake contracted over its rows
 //   weight   G  = dY^T . X          both operands contracted over tokens
-// One kernel template covers all three: each operand is either contiguous
-// along the contraction ("row" layout, 16-byte loads straight into LDS) or
-// contiguous along the output dimension ("transposed": every thread loads an
-// 8x8 block with eight 16-byte loads and transposes it in registers with
-// v_perm before a 16-byte LDS store).  LDS holds both tiles K-contiguous, so
-// the MFMA fragment reads are always one ds_read_b128 per lane.
-//
-// Tiles: BM x BN x 64, double-buffered LDS (one barrier per K step),
-// v_mfma_f32_32x32x16_bf16, fp32 accumulation.  Block -> tile mapping puts
-// consecutive tiles of a row band on one XCD (workgroups are dealt round-robin
-// to the 8 XCDs) and walks tiles in bands of 8 rows for L2 reuse.
+// Two kernel templates, v_mfma_f32_32x32x16_bf16 with fp32 accumulation:
+//   gemm_dma_kernel   operands straight into swizzled LDS tiles with buffer
+//                     loads, K-major operands read with transpose loads; 256
+//                     x 256 tiles on 16 waves (128 x 128 on 4 for small
+//                     problems); dense, split-K, routed experts and the fused
+//                     epilogues (SwiGLU forward/backward, factor gradients).
+//                     It serves every projection of the calibration step.
+//   gemm_bf16_kernel  register-staged tiles, operands contiguous along the
+//                     output dimension transposed in registers with v_perm;
+//                     the remaining shapes (unaligned extents, batched
+//                     attention products of the unfused path).
+// Both map workgroups to tiles so that neighbouring tiles share an XCD's L2
+// (workgroups are dealt round-robin to the 8 XCDs).
 #include <cmath>
 #include <cstdio>
+#include <cstring>
 #include <type_traits>
 
 #include "kernels.h"
@@ -27,6 +30,7 @@ namespace catq {
 
 GemmArgs gemm_args_default() {
   GemmArgs a;
+  std::memset(&a, 0, sizeof(a));  // every field, the epilogue arguments included
   a.A = a.B = a.R = nullptr;
   a.C = nullptr;
   a.M = a.N = a.K = 0;
