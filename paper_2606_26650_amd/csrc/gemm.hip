@@ -773,9 +773,10 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
           const int64_t m = mrow + rr;
           f32x4 v = *reinterpret_cast<const f32x4*>(st + rr * EP + cc);
           if constexpr (EPI == 3) {
-            // G[m][n..n+3] of expert z (one split, alpha 1): the four terms
-            // of the factor gradients over these weights, summed over the 16
-            // lanes of the row's 64 columns (half of a 128-weight group)
+            // G[m][n..n+3] of expert z, or of the one dense problem (z = 0),
+            // unsplit, alpha 1: the four terms of the factor gradients over
+            // these weights, summed over the 16 lanes of the row's 64
+            // columns (half of a 128-weight group)
             const FacEpi& F = g.fac;
             float sT = 0.f, s1 = 0.f, sW = 0.f, sD = 0.f;
             // this row's group scalars from the lane that holds them
@@ -1191,15 +1192,18 @@ catq_status gemm_run_epi(const GemmArgs& a, int a_t, int b_t, hipStream_t stream
 }
 
 catq_status gemm_run_factor(const GemmArgs& a, hipStream_t stream) {
-  CATQ_REQUIRE(a.epi == 3 && a.group_mode == 2, CATQ_ERR_VALUE, "not a factor-gradient launch");
+  CATQ_REQUIRE(a.epi == 3 && (a.group_mode == 2 || (a.group_mode == 0 && a.batch == 1 &&
+                                                     a.causal == 0)),
+               CATQ_ERR_VALUE, "not a factor-gradient launch");
   GemmLaunch L;
   L.g = a;
   L.ksplit = 1;
   L.kchunk = a.K;
   L.c_split_stride = 0;
   L.tiles_m = L.tiles_n = 0;
-  // G per expert [rows][d_in] from K-major dY and X; whole 256 x 256 tiles
-  // (128-weight groups never straddle them), C only as an aligned dummy
+  // G [rows][d_in] (per expert, or one dense unsplit problem) from K-major
+  // dY and X; whole 256 x 256 tiles (128-weight groups never straddle them),
+  // C only as an aligned dummy
   const bool shape = a.M > 0 && a.N > 0 && a.M % 256 == 0 && a.N % 256 == 0 && a.alpha == 1.0f &&
                      a.R == nullptr && a.c_gs == 0 && a.ldc % 4 == 0 && aligned16(a.C) &&
                      a.fac.W != nullptr && (reinterpret_cast<uintptr_t>(a.fac.W) & 7) == 0 &&

@@ -61,12 +61,12 @@ struct StConst {
   float sk4;   // 2 s / tanh(s) (f_W, f_D prefactor)
 };
 
-// Factor-gradient epilogue (EPI 3) of the per-expert weight gradient G_e:
-// instead of G, the gradients of the three learnable factors of every
-// 128-weight group of W_e (the reductions of Sec. 2.3), as the separate
-// factor-gradient kernel computes them from G.
+// Factor-gradient epilogue (EPI 3) of an unsplit weight gradient G (per
+// expert, or one dense matrix): instead of G, the gradients of the three
+// learnable factors of every 128-weight group of W (the reductions of
+// Sec. 2.3), as the separate factor-gradient kernel computes them from G.
 struct FacEpi {
-  const void* W;          // bf16 weights [E][rows][d_in]
+  const void* W;          // bf16 weights [E][rows][d_in] (E = 1 when dense)
   const float* stats;     // [n_groups][2] mu0, alpha0
   const float* dmu;
   const float* dal;
@@ -131,9 +131,10 @@ int gemm_split_count(const GemmArgs& a, int ksplit);
 // the direct-to-LDS kernel's vector epilogue (the caller then runs the
 // unfused pair of kernels).
 catq_status gemm_run_epi(const GemmArgs& a, int a_t, int b_t, hipStream_t stream);
-// Per-expert weight gradients reduced to factor gradients in the epilogue
-// (a.epi = 3, a.fac filled, group_mode 2); CATQ_ERR_VALUE when the shape is
-// not eligible (then nothing was launched).
+// Weight gradients reduced to factor gradients in the epilogue (a.epi = 3,
+// a.fac filled; per expert with group_mode 2, or one dense problem with
+// group_mode 0, never split); CATQ_ERR_VALUE when the shape is not eligible
+// (then nothing was launched).
 catq_status gemm_run_factor(const GemmArgs& a, hipStream_t stream);
 
 // ---------------------------------------------------------- fused attention

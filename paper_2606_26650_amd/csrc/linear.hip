@@ -241,7 +241,41 @@ extern "C" catq_status catq_fakeq_linear_bwd(
     CATQ_TRY(gemm_run(a, 0, 1, dtype, dtype, stream));
   }
   if (!want_g) return CATQ_OK;
-  // G = dY^T . X  (contraction over the tokens: both operands K-major), fp32
+  // G = dY^T . X  (contraction over the tokens: both operands K-major), fp32.
+  // Where every G element is final in one tile (experts, or a dense
+  // gradient left unsplit), 128-weight groups, bf16 and no dW_fake asked
+  // for, the factor gradients come out of the GEMM's epilogue and G never
+  // reaches memory; CATQ_ERR_VALUE from the launch means the shape does not
+  // fit that kernel, and the two-pass path below runs instead.
+  auto factor_epilogue = [&](const GemmArgs& a) -> catq_status {
+    if (!(dW_fake == nullptr && p->group_size == 128 && dtype == CATQ_BF16 &&
+          w_dtype == CATQ_BF16))
+      return CATQ_ERR_VALUE;
+    GemmArgs f = a;
+    f.epi = 3;
+    f.c_gs = 0;  // C is only an aligned dummy
+    FacEpi& fe = f.fac;
+    fe.W = W;
+    fe.stats = stats;
+    fe.dmu = d_mu;
+    fe.dal = d_alpha;
+    fe.dde = d_delta;
+    fe.out[0] = g_d_mu;
+    fe.out[1] = g_d_alpha;
+    fe.out[2] = g_d_delta;
+    fe.ws = shared_ws;
+    fe.n_groups = E * N * K / 128;
+    for (int i = 0; i < 3; ++i) fe.s[i] = p->factor_stride[i];
+    fe.mode = p->mode;
+    fe.ste = (p->mode == CATQ_HARD && p->s_bwd == 0.0f) ? 1 : 0;
+    fe.delta0 = p->delta0;
+    const double s_use = (p->mode == CATQ_HARD) ? (double)p->s_bwd : (double)p->s;
+    fe.st = make_st(s_use > 0 ? s_use : 1.0);
+    const catq_status st = gemm_run_factor(f, stream);
+    if (st == CATQ_OK) return finish_shared_factors(fe.s, fe.n_groups, shared_ws, fe.out, stream);
+    if (st == CATQ_ERR_VALUE) clear_error();
+    return st;
+  };
   {
     GemmArgs a = gemm_args_default();
     a.C = Gbuf;
@@ -249,51 +283,23 @@ extern "C" catq_status catq_fakeq_linear_bwd(
     a.N = K;
     a.K = M;
     a.ldc = K;
+    a.A = dY;
+    a.B = X;
+    a.lda = N;
+    a.ldb = K;
     if (n_experts > 1) {
-      a.A = dY;
-      a.B = X;
-      a.lda = N;
-      a.ldb = K;
       a.group_mode = 2;
       a.group_off = row_offsets;
       a.n_groups = n_experts;
-      if (dW_fake == nullptr && p->group_size == 128 && dtype == CATQ_BF16 &&
-          w_dtype == CATQ_BF16) {
-        // every G element is final in one tile (no split): the factor
-        // gradients come out of the GEMM's epilogue and G never reaches memory
-        GemmArgs f = a;
-        f.epi = 3;
-        f.c_gs = 0;  // C is only an aligned dummy
-        FacEpi& fe = f.fac;
-        fe.W = W;
-        fe.stats = stats;
-        fe.dmu = d_mu;
-        fe.dal = d_alpha;
-        fe.dde = d_delta;
-        fe.out[0] = g_d_mu;
-        fe.out[1] = g_d_alpha;
-        fe.out[2] = g_d_delta;
-        fe.ws = shared_ws;
-        fe.n_groups = E * N * K / 128;
-        for (int i = 0; i < 3; ++i) fe.s[i] = p->factor_stride[i];
-        fe.mode = p->mode;
-        fe.ste = (p->mode == CATQ_HARD && p->s_bwd == 0.0f) ? 1 : 0;
-        fe.delta0 = p->delta0;
-        const double s_use = (p->mode == CATQ_HARD) ? (double)p->s_bwd : (double)p->s;
-        fe.st = make_st(s_use > 0 ? s_use : 1.0);
-        const catq_status st = gemm_run_factor(f, stream);
-        if (st == CATQ_OK)
-          return finish_shared_factors(fe.s, fe.n_groups, shared_ws, fe.out, stream);
-        if (st != CATQ_ERR_VALUE) return st;
-        clear_error();
-      }
+    }
+    if (ns == 1) {
+      const catq_status st = factor_epilogue(a);
+      if (st != CATQ_ERR_VALUE) return st;
+    }
+    if (n_experts > 1) {
       a.c_gs = N * K;
       CATQ_TRY(gemm_run(a, 1, 1, dtype, CATQ_F32, stream));
     } else {
-      a.A = dY;
-      a.B = X;
-      a.lda = N;
-      a.ldb = K;
       CATQ_TRY(gemm_run_split(a, 1, 1, dtype, CATQ_F32, choose_ksplit(M, N, K, 1), N * K,
                               stream));
     }

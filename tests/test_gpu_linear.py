@@ -209,6 +209,62 @@ def test_grouped_factor_epilogue(catq, mode, s_bwd, strides):
         assert max_norm_err(host(a), host(b)) <= 1e-4
 
 
+
+@pytest.mark.parametrize("M,N,K,fused", [(1984, 512, 768, True),     # unsplit: epilogue
+                                         (1000, 512, 768, False),    # tokens % 64: two passes
+                                         (8192, 256, 256, False)])   # split: two passes
+@pytest.mark.parametrize("mode,s_bwd,strides", [
+    (lmst.SOFT, 30.0, (1, 1, 1)), (lmst.HARD, 30.0, (1, 1, 1)), (lmst.HARD, 0.0, (1, 1, 1)),
+    (lmst.SOFT, 30.0, (0, 1, 0)), (lmst.IDENTITY, 0.0, (1, 1, 1))])
+def test_dense_factor_epilogue(catq, M, N, K, fused, mode, s_bwd, strides):
+    """A dense weight gradient whose token contraction is not split has its
+    factor gradients reduced in the GEMM epilogue (bf16, 128-weight groups,
+    no dW_fake requested); other shapes take the two-pass path.  Both against
+    the oracle and against the separate factor-gradient kernel on the
+    materialised G (requested through dW_fake)."""
+    import torch
+    xb = sg.normal_bf16(11, "X", (M, K))
+    wb = sg.normal_bf16(11, "W", (N, K), std=0.02)
+    dyb = sg.normal_bf16(11, "Y", (M, N), std=1e-3)
+    X, W, dY = to_dev_bf16(xb), to_dev_bf16(wb), to_dev_bf16(dyb)
+    ng = N * K // 128
+    fac = list(sg.perturbed_factors(12, ng))
+    for i, st in enumerate(strides):
+        if st == 0:
+            fac[i] = fac[i][:1]
+    dm, da, dd = (to_dev_f32(f) for f in fac)
+    stats = torch.zeros(ng, 2, dtype=torch.float32, device="cuda")
+    wf = torch.empty_like(W)
+    p = catq.lmst_params(mode=mode, s=7.0, s_bwd=s_bwd, strides=strides)
+    catq.catq_modulate_ternarize(W, dm, da, dd, p, stats, 0, W_fake=wf)
+    ws = torch.empty(catq.catq_workspace_size(0, M, N, K, 1), dtype=torch.uint8, device="cuda")
+
+    def run(with_dw):
+        g = [torch.full((ng if st else 1,), float("nan"), dtype=torch.float32, device="cuda")
+             for st in strides]
+        dW = torch.empty(N, K, dtype=torch.float32, device="cuda") if with_dw else None
+        catq.catq_fakeq_linear_bwd(dY, X, wf, M, N, K, W, stats, dm, da, dd, p, *g, ws,
+                                   dW_fake=dW)
+        return g, dW
+
+    torch.cuda.synchronize()
+    catq.catq_trace_enable(64)
+    first, _ = run(False)
+    torch.cuda.synchronize()
+    tags = [r["tag"] for r in catq.trace_records()]
+    catq.catq_trace_disable()
+    assert any("factor_grads" in t for t in tags) == fused, tags
+    assert any(t.startswith("lmst_bwd") for t in tags) != fused, tags
+    sep, dW = run(True)
+    torch.cuda.synchronize()
+    Gref = f64(dyb).T @ f64(xb)
+    assert max_norm_err(host(dW), Gref) <= 1e-5
+    ref = lmst.factor_grads(Gref, f64(wb), 128, *fac, mode, s=7.0, s_bwd=s_bwd, strides=strides)
+    for a, b, r in zip(first, sep, ref):
+        assert torch.isfinite(a).all()
+        assert max_norm_err(host(a), r) <= 2e-2
+        assert max_norm_err(host(a), host(b)) <= 1e-4
+
 def test_fp32_linear(catq):
     import torch
     W, X = sg.single_linear_case(0)
