@@ -59,8 +59,13 @@ __device__ __forceinline__ unsigned short f2bf_bits(float f) {
   bf16 h = (bf16)f;
   return __builtin_bit_cast(unsigned short, h);
 }
+// Two floats -> two bf16 in one dword (lo in the low half), one packed
+// conversion (the same rounding as f2bf_bits on each).
+typedef __attribute__((ext_vector_type(2))) float f32x2;
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
 __device__ __forceinline__ unsigned int pack_bf16x2(float lo, float hi) {
-  return (unsigned int)f2bf_bits(lo) | ((unsigned int)f2bf_bits(hi) << 16);
+  const f32x2 v = {lo, hi};
+  return __builtin_bit_cast(unsigned int, __builtin_convertvector(v, bf16x2));
 }
 
 // Load 8 consecutive elements (bf16 or fp32) as floats.

@@ -516,12 +516,21 @@ __global__ __launch_bounds__(fa::NT, 2) void flash_bwd_dq_kernel(FaArgs a) {
           dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
               fa::tfrag_row<D>(sV[buf], sb * 32 + l32, 2 * t + g), of[t], dp, 0, 0, 0);
         }
+        // causal / length mask only where the 32 x 32 block crosses the
+        // wave's diagonal or the sequence end (uniform over the wave)
+        const int kb0 = k0 + sb * 32;
+        if (kb0 + 31 > q0 + 32 * w || kb0 + 32 > a.S || wave_last >= a.S) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = k0 + sb * 32 + fa::acc_row(r, g);
-          float p = __builtin_amdgcn_exp2f(fmaf(s[r], a.c, -lse));
-          if (key > qme || key >= a.S || qme >= a.S) p = 0.f;
-          dp[r] = p * (dp[r] - dsum);
+          for (int r = 0; r < 16; ++r) {
+            const int key = kb0 + fa::acc_row(r, g);
+            float p = __builtin_amdgcn_exp2f(fmaf(s[r], a.c, -lse));
+            if (key > qme || key >= a.S || qme >= a.S) p = 0.f;
+            dp[r] = p * (dp[r] - dsum);
+          }
+        } else {
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            dp[r] = __builtin_amdgcn_exp2f(fmaf(s[r], a.c, -lse)) * (dp[r] - dsum);
         }
         // dQ^T[d][q] += K^T dS  (contraction over keys)
 #pragma unroll
