@@ -13,11 +13,11 @@
 // tiles of 64 stream through LDS (K as [key][d], V transposed as [d][key]);
 // online softmax in base 2; O written token-major, and the per-query
 // log-sum-exp (base 2) kept for the backward.
-// Backward: dK/dV kernel (block = 4 x 32 keys of one kv head, looping over the
-// q heads of its group and the causal query tiles) and dQ kernel (block = 4 x
-// 32 queries, looping over key tiles); P and dS are recomputed from the saved
-// log-sum-exp and D = rowsum(dO * O).  No atomics: every output element is
-// owned by one lane.
+// Backward: dK/dV kernel (block = 128 keys of one kv head, four wavefronts
+// accumulating dV and four dK, looping over the q heads of its group and the
+// causal query tiles) and dQ kernel (block = 4 x 32 queries, looping over key
+// tiles); P and dS are recomputed from the saved log-sum-exp and
+// D = rowsum(dO * O).  No atomics: every output element is owned by one lane.
 #include <cmath>
 
 #include "kernels.h"
@@ -331,124 +331,166 @@ __global__ __launch_bounds__(256) void flash_dsum_kernel(FaArgs a) {
 }
 
 // ------------------------------------------------------------- dK and dV
+//
+// Block = 8 wavefronts over 128 keys of one kv head.  Waves 0-3 accumulate
+// dV and waves 4-7 dK, each for the 32 keys of slab w % 4; both roles form
+// S^T for their keys, the dK waves also dP^T.  A wave thus holds one
+// 32 x D accumulator set instead of two, so two waves fit on each SIMD and
+// the exponentials and packing of one overlap the matrix products of the
+// other.  The Q and dO tiles of 64 queries are staged through registers
+// (threads 0-255 stage Q, 256-511 dO) into row-major and transposed LDS
+// copies shared by all eight waves.
 
-template <int D>
-__global__ __launch_bounds__(fa::NT, 1) void flash_bwd_dkdv_kernel(FaArgs a) {
+constexpr int DKDV_NT = 512;
+
+template <int D, int ROLE>  // ROLE 0: dV, 1: dK
+__device__ __forceinline__ void dkdv_waves(const FaArgs& a, u16* sQ, u16* sQt, u16* sO, u16* sOt,
+                                           float* sL, float* sD) {
   using C = fa::Cfg<D>;
-  __shared__ u16 sQ[fa::BK * C::KP];
-  __shared__ u16 sQt[D * fa::TP];
-  __shared__ u16 sO[fa::BK * C::KP];   // dO rows
-  __shared__ u16 sOt[D * fa::TP];      // dO transposed
-  __shared__ float sL[fa::BK], sD[fa::BK];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 5, l32 = lane & 31;
-  // grid (B*Hkv*hsplit, key tiles): the low key tiles see the most queries
-  // and are dispatched first; block chunk of a kv head takes its share of the
-  // group's q heads and writes its own partial dK/dV
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
+  const int ks = __builtin_amdgcn_readfirstlane(tid >> 6) & 3;  // key slab of this wave
+  // grid (B*Hkv*hsplit, key tiles): block chunk of a kv head takes its share
+  // of the group's q heads and writes its own partial dK/dV
   const int chunk = blockIdx.x % a.hsplit, bk = blockIdx.x / a.hsplit;
   const int kt = blockIdx.y, kvh = bk % a.Hkv, b = bk / a.Hkv;
   const int G = a.Hq / a.Hkv, Gc = G / a.hsplit;
   const int k0 = kt * 128;
-  const int kme = k0 + 32 * w + l32;  // this lane's key (column of S^T[q][key])
+  const int wave_first = k0 + 32 * ks;  // queries below this see none of the wave's keys
+  const int kme = wave_first + l32;     // this lane's key (column of S^T[q][key])
   const bf16* Kb = a.K + ((int64_t)(b * a.Hkv + kvh) * a.S) * D;
   const bf16* Vb = a.V + ((int64_t)(b * a.Hkv + kvh) * a.S) * D;
-  // K and V fragments of this lane's key (operand B of S^T = Q K^T and dP^T = dO V^T)
-  bf16x8 kf[C::KS], vf[C::KS];
+  // K (and for dK, V) fragments of this lane's key: operand B of S^T = Q K^T
+  // and dP^T = dO V^T
+  bf16x8 kf[C::KS];
+  [[maybe_unused]] bf16x8 vf[C::KS];
 #pragma unroll
   for (int t = 0; t < C::KS; ++t) {
-    u32x4 kv = {0u, 0u, 0u, 0u}, vv = {0u, 0u, 0u, 0u};
-    if (kme < a.S) {
-      kv = *reinterpret_cast<const u32x4*>(Kb + (int64_t)kme * D + 16 * t + 8 * g);
-      vv = *reinterpret_cast<const u32x4*>(Vb + (int64_t)kme * D + 16 * t + 8 * g);
-    }
+    u32x4 kv = {0u, 0u, 0u, 0u};
+    if (kme < a.S) kv = *reinterpret_cast<const u32x4*>(Kb + (int64_t)kme * D + 16 * t + 8 * g);
     kf[t] = __builtin_bit_cast(bf16x8, kv);
-    vf[t] = __builtin_bit_cast(bf16x8, vv);
+    if constexpr (ROLE == 1) {
+      u32x4 vv = {0u, 0u, 0u, 0u};
+      if (kme < a.S) vv = *reinterpret_cast<const u32x4*>(Vb + (int64_t)kme * D + 16 * t + 8 * g);
+      vf[t] = __builtin_bit_cast(bf16x8, vv);
+    }
   }
-  f32x16 dk[C::DB], dv[C::DB];
+  f32x16 acc[C::DB];
 #pragma unroll
-  for (int i = 0; i < C::DB; ++i) {
-    dk[i] = fa::zero16();
-    dv[i] = fa::zero16();
-  }
-  const int wave_first = k0 + 32 * w;  // queries below this see none of the wave's keys
+  for (int i = 0; i < C::DB; ++i) acc[i] = fa::zero16();
   const int qt0 = k0 / fa::BK;
   const int nqt = (a.S + fa::BK - 1) / fa::BK;
+  const bool stage_q = tid < 256;
+  const int st = tid & 255;
   for (int gq = chunk * Gc; gq < (chunk + 1) * Gc; ++gq) {
     const int h = kvh * G + gq;
     const bf16* Qb = a.Q + ((int64_t)(b * a.Hq + h) * a.S) * D;
     const float* Lb = a.lse + (int64_t)(b * a.Hq + h) * a.S;
     const float* Db = a.Dsum + (int64_t)(b * a.Hq + h) * a.S;
     const bf16* dOb = a.dO + (int64_t)b * a.S * (a.Hq * D) + (int64_t)h * D;
-    fa::Tile<D> tq, to;
-    tq.load(Qb, D, (int64_t)qt0 * fa::BK, a.S, tid);
-    to.load(dOb, (int64_t)a.Hq * D, (int64_t)qt0 * fa::BK, a.S, tid);
+    fa::Tile<D> tl;
+    if (stage_q)
+      tl.load(Qb, D, (int64_t)qt0 * fa::BK, a.S, st);
+    else
+      tl.load(dOb, (int64_t)a.Hq * D, (int64_t)qt0 * fa::BK, a.S, st);
     for (int qt = qt0; qt < nqt; ++qt) {
       const int q0 = qt * fa::BK;
       __syncthreads();
-      tq.store_rows(sQ);
-      tq.store_transposed(sQt);
-      to.store_rows(sO);
-      to.store_transposed(sOt);
+      if (stage_q) {
+        tl.store_rows(sQ);
+        tl.store_transposed(sQt);
+      } else {
+        tl.store_rows(sO);
+        tl.store_transposed(sOt);
+      }
       if (tid < fa::BK) {
         const int q = q0 + tid;
         sL[tid] = q < a.S ? Lb[q] : 0.f;
-        sD[tid] = q < a.S ? Db[q] : 0.f;
+      } else if (tid >= 256 && tid < 256 + fa::BK) {
+        const int q = q0 + tid - 256;
+        sD[tid - 256] = q < a.S ? Db[q] : 0.f;
       }
       __syncthreads();
       if (qt + 1 < nqt) {
-        tq.load(Qb, D, (int64_t)(q0 + fa::BK), a.S, tid);
-        to.load(dOb, (int64_t)a.Hq * D, (int64_t)(q0 + fa::BK), a.S, tid);
+        if (stage_q)
+          tl.load(Qb, D, (int64_t)(q0 + fa::BK), a.S, st);
+        else
+          tl.load(dOb, (int64_t)a.Hq * D, (int64_t)(q0 + fa::BK), a.S, st);
       }
       if (q0 + fa::BK - 1 < wave_first) continue;
-#pragma unroll
+#pragma unroll 1
       for (int qb = 0; qb < 2; ++qb) {
-        // S^T[q][key] and dP^T[q][key] for 32 queries
-        f32x16 s = fa::zero16(), dp = fa::zero16();
+        // S^T[q][key] (and dP^T[q][key]) for 32 queries
+        f32x16 s = fa::zero16();
+        [[maybe_unused]] f32x16 dp = fa::zero16();
 #pragma unroll
         for (int t = 0; t < C::KS; ++t) {
           s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
               fa::frag_rows(sQ, qb * 32 + l32, 16 * t + 8 * g, C::KP), kf[t], s, 0, 0, 0);
-          dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              fa::frag_rows(sO, qb * 32 + l32, 16 * t + 8 * g, C::KP), vf[t], dp, 0, 0, 0);
+          if constexpr (ROLE == 1)
+            dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                fa::frag_rows(sO, qb * 32 + l32, 16 * t + 8 * g, C::KP), vf[t], dp, 0, 0, 0);
         }
-        // P and dS (rows = queries of this lane's registers)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
+        // P (dV) or dS = P (dP - D) (dK), rows = queries of this lane's
+        // registers; the causal / length mask only where the 32 x 32 block
+        // crosses the wave's diagonal or the sequence end (uniform)
+        const int qb0 = q0 + qb * 32;
+        auto p_of = [&](int r, bool masked) {
           const int qi = qb * 32 + fa::acc_row(r, g);
-          const int q = q0 + qi;
           float p = __builtin_amdgcn_exp2f(fmaf(s[r], a.c, -sL[qi]));
-          if (q < kme || q >= a.S || kme >= a.S) p = 0.f;
-          s[r] = p;
-          dp[r] = p * (dp[r] - sD[qi]);
+          if (masked) {
+            const int q = q0 + qi;
+            if (q < kme || q >= a.S || kme >= a.S) p = 0.f;
+          }
+          if constexpr (ROLE == 0)
+            s[r] = p;
+          else
+            dp[r] = p * (dp[r] - sD[qi]);
+        };
+        if (qb0 < wave_first + 31 || qb0 + 32 > a.S || wave_first + 31 >= a.S) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) p_of(r, true);
+        } else {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) p_of(r, false);
         }
         // dV[key][d] += P^T dO ; dK[key][d] += dS^T Q  (contraction over queries)
 #pragma unroll
         for (int hh = 0; hh < 2; ++hh) {
-          const bf16x8 pf = fa::pack8(s, hh), df = fa::pack8(dp, hh);
+          const bf16x8 pf = fa::pack8(ROLE == 0 ? s : dp, hh);
 #pragma unroll
-          for (int i = 0; i < C::DB; ++i) {
-            dv[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                pf, fa::frag_tr(sOt, i * 32 + l32, 2 * qb + hh, g), dv[i], 0, 0, 0);
-            dk[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                df, fa::frag_tr(sQt, i * 32 + l32, 2 * qb + hh, g), dk[i], 0, 0, 0);
-          }
+          for (int i = 0; i < C::DB; ++i)
+            acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                pf, fa::frag_tr(ROLE == 0 ? sOt : sQt, i * 32 + l32, 2 * qb + hh, g), acc[i], 0,
+                0, 0);
         }
       }
     }
   }
-  // dv[i][r]: key row = 32w + acc_row(r, g) within the block, d column = 32i + l32
+  // acc[i][r]: key row = 32 ks + acc_row(r, g) within the block, d column = 32 i + l32
   const int64_t part = (int64_t)chunk * a.B * a.Hkv * a.S * D;
-  float* dKb = a.dK + part + ((int64_t)(b * a.Hkv + kvh) * a.S) * D;
-  float* dVb = a.dV + part + ((int64_t)(b * a.Hkv + kvh) * a.S) * D;
+  float* outb = (ROLE == 0 ? a.dV : a.dK) + part + ((int64_t)(b * a.Hkv + kvh) * a.S) * D;
+  const float sc = ROLE == 0 ? 1.0f : a.scale;
 #pragma unroll
   for (int i = 0; i < C::DB; ++i)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int key = k0 + 32 * w + fa::acc_row(r, g);
-      if (key < a.S) {
-        dKb[(int64_t)key * D + 32 * i + l32] = dk[i][r] * a.scale;
-        dVb[(int64_t)key * D + 32 * i + l32] = dv[i][r];
-      }
+      const int key = wave_first + fa::acc_row(r, g);
+      if (key < a.S) outb[(int64_t)key * D + 32 * i + l32] = acc[i][r] * sc;
     }
+}
+
+template <int D>
+__global__ __launch_bounds__(DKDV_NT, 2) void flash_bwd_dkdv_kernel(FaArgs a) {
+  using C = fa::Cfg<D>;
+  __shared__ u16 sQ[fa::BK * C::KP];
+  __shared__ u16 sQt[D * fa::TP];
+  __shared__ u16 sO[fa::BK * C::KP];   // dO rows
+  __shared__ u16 sOt[D * fa::TP];      // dO transposed
+  __shared__ float sL[fa::BK], sD[fa::BK];
+  if (__builtin_amdgcn_readfirstlane(threadIdx.x >> 6) < 4)
+    dkdv_waves<D, 0>(a, sQ, sQt, sO, sOt, sL, sD);
+  else
+    dkdv_waves<D, 1>(a, sQ, sQt, sO, sOt, sL, sD);
 }
 
 // ------------------------------------------------------------------- dQ
@@ -586,12 +628,13 @@ catq_status flash_backward(int D, FaArgs& a, hipStream_t stream) {
   CATQ_CHECK_LAUNCH("flash dsum");
   const double half = 0.5 * 2.0 * (double)a.B * a.Hq * (double)a.S * a.S * D;
   dim3 gkv((unsigned)(a.B * a.Hkv * a.hsplit), (unsigned)((a.S + 127) / 128)), block(fa::NT);
+  const dim3 block_kv(DKDV_NT);
   if (D == 128)
     CATQ_TRACED(stream, "flash_bwd_dkdv_kernel<128>", 4.0 * half, 0.0, a.S, a.Hkv, D,
-                hipLaunchKernelGGL(flash_bwd_dkdv_kernel<128>, gkv, block, 0, stream, a));
+                hipLaunchKernelGGL(flash_bwd_dkdv_kernel<128>, gkv, block_kv, 0, stream, a));
   else
     CATQ_TRACED(stream, "flash_bwd_dkdv_kernel<64>", 4.0 * half, 0.0, a.S, a.Hkv, D,
-                hipLaunchKernelGGL(flash_bwd_dkdv_kernel<64>, gkv, block, 0, stream, a));
+                hipLaunchKernelGGL(flash_bwd_dkdv_kernel<64>, gkv, block_kv, 0, stream, a));
   CATQ_CHECK_LAUNCH("flash dK dV");
   dim3 gq((unsigned)(a.B * a.Hq), (unsigned)((a.S + 127) / 128));
   if (D == 128)
