@@ -241,28 +241,43 @@ struct BwdArgs {
   StConst st;
 };
 
-template <typename WT>
+// NS > 0: exactly NS split partials, all loads issued before any use;
+// NS = 0: any count, folded in a loop.
+template <typename WT, int NS>
 __global__ __launch_bounds__(256) void lmst_bwd_kernel(BwdArgs a) {
   const int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (o >= a.n_oct) return;
   const int L = 1 << a.lg;
   const int64_t grp = o >> a.lg;
   const int lane_in_g = (int)(o & (L - 1));
+  // the group's scalars first: their loads are in flight with the streams
+  const float mu0 = a.stats[2 * grp], alpha0 = a.stats[2 * grp + 1];
+  const float fmu = a.dmu[grp * a.s[0]], fal = a.dal[grp * a.s[1]], fde = a.dde[grp * a.s[2]];
   float w[8], G[8];
   load8<WT>(reinterpret_cast<const WT*>(a.W) + o * 8, w);
-  load8<float>(a.G + o * 8, G);
   // split-K partials of G, folded in split order (the same order and
   // rounding as a separate reduction pass)
-  for (int sp = 1; sp < a.nsplit; ++sp) {
-    float t[8];
-    load8<float>(a.G + sp * a.split_stride + o * 8, t);
+  if constexpr (NS > 0) {
+    float t[NS][8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) G[j] += t[j];
+    for (int sp = 0; sp < NS; ++sp) load8<float>(a.G + sp * a.split_stride + o * 8, t[sp]);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      G[j] = t[0][j];
+#pragma unroll
+      for (int sp = 1; sp < NS; ++sp) G[j] += t[sp][j];
+    }
+  } else {
+    load8<float>(a.G + o * 8, G);
+    for (int sp = 1; sp < a.nsplit; ++sp) {
+      float t[8];
+      load8<float>(a.G + sp * a.split_stride + o * 8, t);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) G[j] += t[j];
+    }
   }
   if (a.G_out) store8<float>(a.G_out + o * 8, G);
-  const float mu0 = a.stats[2 * grp], alpha0 = a.stats[2 * grp + 1];
-  GroupScalars gs = group_scalars(mu0, alpha0, a.dmu[grp * a.s[0]], a.dal[grp * a.s[1]],
-                                  a.dde[grp * a.s[2]], a.delta0);
+  GroupScalars gs = group_scalars(mu0, alpha0, fmu, fal, fde, a.delta0);
   float ST = 0.f, SW = 0.f, S1 = 0.f, SD = 0.f;
   if (a.mode != CATQ_IDENTITY) {
     const float inv_a = 1.0f / gs.alpha_div;
@@ -370,12 +385,23 @@ catq_status launch_factor_grads(const float* G, int nsplit, int64_t split_stride
   const double nn = (double)n, ngd = (double)a.n_groups;
   const double bytes = nn * (4.0 * a.nsplit + (G_out ? 4.0 : 0.0) + (w_dtype == CATQ_BF16 ? 2.0 : 4.0)) +
                        ngd * (8.0 + 12.0 + 12.0);
-  if (w_dtype == CATQ_BF16)
-    CATQ_TRACED(stream, "lmst_bwd_kernel<__bf16>", 0.0, bytes, n, 0, 0,
-                hipLaunchKernelGGL((lmst_bwd_kernel<bf16>), grid, dim3(256), 0, stream, a));
-  else
+  if (w_dtype == CATQ_BF16) {
+    auto go = [&](auto kern) {
+      CATQ_TRACED(stream, "lmst_bwd_kernel<__bf16>", 0.0, bytes, n, 0, 0,
+                  hipLaunchKernelGGL(kern, grid, dim3(256), 0, stream, a));
+    };
+    if (a.nsplit == 1)
+      go(lmst_bwd_kernel<bf16, 1>);
+    else if (a.nsplit == 2)
+      go(lmst_bwd_kernel<bf16, 2>);
+    else if (a.nsplit == 4)
+      go(lmst_bwd_kernel<bf16, 4>);
+    else
+      go(lmst_bwd_kernel<bf16, 0>);
+  } else {
     CATQ_TRACED(stream, "lmst_bwd_kernel<float>", 0.0, bytes, n, 0, 0,
-                hipLaunchKernelGGL((lmst_bwd_kernel<float>), grid, dim3(256), 0, stream, a));
+                hipLaunchKernelGGL((lmst_bwd_kernel<float, 0>), grid, dim3(256), 0, stream, a));
+  }
   CATQ_CHECK_LAUNCH("factor gradients");
   for (int i = 0; i < 3; ++i) {
     if (a.s[i] == 0) {
