@@ -258,17 +258,6 @@ __global__ __launch_bounds__(fa::NT, 2) void flash_fwd_kernel(FaArgs a) {
       // a lane whose query lies past the sequence end sees only masked keys
       const float msafe = (mn == -INFINITY) ? 0.f : mn;
       const float alpha = __builtin_amdgcn_exp2f(m - msafe);
-      float rs = 0.f;
-#pragma unroll
-      for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float p = __builtin_amdgcn_exp2f(fmaf(s[sb][r], a.c, -msafe));
-          s[sb][r] = p;
-          rs += p;
-        }
-      rs += __shfl_xor(rs, 32, 64);
-      l = l * alpha + rs;
       // alpha == 1 exactly unless the running max moved: skip the rescale when
       // it moved for no lane of the wave
       if (__any(mn != m)) {
@@ -278,9 +267,18 @@ __global__ __launch_bounds__(fa::NT, 2) void flash_fwd_kernel(FaArgs a) {
           for (int r = 0; r < 16; ++r) o[i][r] *= alpha;
       }
       m = mn;
-      // O^T += V^T P^T (V^T fragments by transpose reads of the V rows)
+      // per 32-key block: P, then O^T += V^T P^T (V^T fragments by transpose
+      // reads of the V rows); the exponentials of the second block are
+      // independent of the first block's products and can overlap them
+      float rs = 0.f;
 #pragma unroll
-      for (int sb = 0; sb < 2; ++sb)
+      for (int sb = 0; sb < 2; ++sb) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float p = __builtin_amdgcn_exp2f(fmaf(s[sb][r], a.c, -msafe));
+          s[sb][r] = p;
+          rs += p;
+        }
 #pragma unroll
         for (int hh = 0; hh < 2; ++hh) {
           const bf16x8 pf = fa::pack8(s[sb], hh);
@@ -289,6 +287,9 @@ __global__ __launch_bounds__(fa::NT, 2) void flash_fwd_kernel(FaArgs a) {
             o[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
                 fa::tfrag_tr<D>(sV[buf], i * 32, 2 * sb + hh, lane), pf, o[i], 0, 0, 0);
         }
+      }
+      rs += __shfl_xor(rs, 32, 64);
+      l = l * alpha + rs;
     }
     wait_vmem();
     __syncthreads();
