@@ -330,7 +330,8 @@ def main():
     x = bf16_tensor(xb)
     y_fp = blk.new_output()
     blk.target(x, y_fp)
-    fin = blk.finalize_buffers()
+    # the final ternarisation writes the 2-bit storage directly (no int8 codes)
+    fin = blk.finalize_buffers(codes=False)
 
     def step(overlap):
         blk.step(x, y_fp, mode=cq.SOFT, s=15.0, s_bwd=30.0, recompute_stats=True,

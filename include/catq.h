@@ -212,6 +212,25 @@ catq_status catq_block_recon_loss(const void* Y_q, const void* Y_fp, catq_dtype 
 catq_status catq_pack_ternary(const int8_t* codes, int64_t d_out, int64_t d_in, uint8_t* packed,
                               hipStream_t stream);
 
+/*
+ * catq_ternarize_pack -- the final hard ternarisation (Eq. 2 on the modulated
+ * weights of Eq. 3-4) written straight to the 2-bit storage above (App. B.2),
+ * with the group scales: the codes of catq_modulate_ternarize in HARD mode,
+ * packed as catq_pack_ternary packs them, in one pass over W (no int8 codes
+ * and no W_fake in memory).
+ *   W, w_dtype, d_out, d_in, d_mu, d_alpha, d_delta, stats, stats_mode
+ *              as for catq_modulate_ternarize
+ *   p          host pointer; p->mode must be CATQ_HARD
+ *   packed     uint8 [d_out][d_in/4], written
+ *   alpha_out  fp32 [n_groups] group scales alpha; may be NULL
+ * Errors: NULL W/factors/stats/packed/p, mode other than HARD, d_in % g,
+ * g out of range, delta0 <= 0, bad w_dtype, misaligned pointers.
+ */
+catq_status catq_ternarize_pack(const void* W, catq_dtype w_dtype, int64_t d_out, int64_t d_in,
+                                const float* d_mu, const float* d_alpha, const float* d_delta,
+                                const catq_lmst_params* p, float* stats, int32_t stats_mode,
+                                uint8_t* packed, float* alpha_out, hipStream_t stream);
+
 /* catq_ternary_linear -- deployment-side linear layer on that storage:
  *   Y[m][n] = sum_k X[m][k] * alpha[n][k / g] * T[n][k]
  * i.e. Y = X (alpha * T)^T with the ternary weights and group scales of the

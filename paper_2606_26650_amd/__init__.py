@@ -14,7 +14,8 @@ from ._lib import (BF16, F32, HARD, IDENTITY, SOFT, WS_LINEAR_BWD, WS_LOSS, Attn
 
 __all__ = [
     "catq_modulate_ternarize", "catq_fakeq_linear_fwd", "catq_fakeq_linear_bwd",
-    "catq_block_recon_loss", "catq_pack_ternary", "catq_fakeq_gateup_swiglu_fwd",
+    "catq_block_recon_loss", "catq_pack_ternary", "catq_ternarize_pack",
+    "catq_fakeq_gateup_swiglu_fwd",
     "catq_fakeq_down_swiglu_bwd", "catq_ternary_linear", "catq_workspace_size",
     "catq_aux_act_quant", "catq_aux_rmsnorm_fwd", "catq_aux_rmsnorm_bwd", "catq_aux_attention_fwd",
     "catq_aux_attention_bwd", "catq_attn_saved_bytes", "catq_attn_bwd_workspace_bytes",
@@ -115,6 +116,16 @@ def catq_block_recon_loss(Y_q, Y_fp, loss, dY_q, workspace, stream=None):
     st = lib.catq_block_recon_loss(_ptr(Y_q), _ptr(Y_fp), _dt(Y_q), Y_q.numel(), _ptr(loss),
                                    _ptr(dY_q), dy_dt, _ptr(workspace), ws_bytes, _stream(stream))
     _lib.check("catq_block_recon_loss", st)
+
+
+def catq_ternarize_pack(W, d_mu, d_alpha, d_delta, params, stats, stats_mode, packed,
+                        alpha_out=None, stream=None):
+    d_in = W.shape[-1]
+    rows = W.numel() // d_in
+    st = lib.catq_ternarize_pack(_ptr(W), _dt(W), rows, d_in, _ptr(d_mu), _ptr(d_alpha),
+                                 _ptr(d_delta), C.byref(params), _ptr(stats), stats_mode,
+                                 _ptr(packed), _ptr(alpha_out), _stream(stream))
+    _lib.check("catq_ternarize_pack", st)
 
 
 def catq_pack_ternary(codes, packed, stream=None):

@@ -52,6 +52,7 @@ SIGNATURES = {
                               P, P, P, P, SZ, P],
     "catq_block_recon_loss": [P, P, I32, I64, P, P, I32, P, SZ, P],
     "catq_pack_ternary": [P, I64, I64, P, P],
+    "catq_ternarize_pack": [P, I32, I64, I64, P, P, P, PP, P, I32, P, P, P],
     "catq_fakeq_gateup_swiglu_fwd": [P, P, I64, I64, I64, P, P, P],
     "catq_fakeq_down_swiglu_bwd": [P, P, I64, I64, I64, P, P, P, P],
     "catq_ternary_linear": [P, I64, I64, P, P, I64, I64, I32, P, I32, I64, P],

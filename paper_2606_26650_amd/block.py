@@ -26,7 +26,7 @@ from . import (BF16, HARD, IDENTITY, SOFT, attn_desc, catq_aux_act_quant, catq_a
                catq_aux_swiglu_bwd, catq_aux_swiglu_fwd, catq_attn_bwd_workspace_bytes,
                catq_attn_saved_bytes, catq_block_recon_loss, catq_fakeq_linear_bwd,
                catq_fakeq_down_swiglu_bwd, catq_fakeq_gateup_swiglu_fwd, catq_fakeq_linear_fwd,
-               catq_modulate_ternarize, catq_pack_ternary,
+               catq_modulate_ternarize, catq_pack_ternary, catq_ternarize_pack,
                catq_workspace_size, lmst_params, WS_LINEAR_BWD, WS_LOSS)
 
 DEV = "cuda"
@@ -129,6 +129,12 @@ class WeightArena:
         catq_modulate_ternarize(self.flat(self.W), self.d_mu, self.d_alpha, self.d_delta, p,
                                 self.stats, stats_mode, W_fake=self.flat(wf),
                                 codes=self.flat(codes), alpha_out=alpha_out)
+
+    def ternarize_pack(self, p, stats_mode, packed, alpha_out):
+        """Hard codes of every weight straight to 2-bit storage (one launch)."""
+        catq_ternarize_pack(self.flat(self.W), self.d_mu, self.d_alpha, self.d_delta, p,
+                            self.stats, stats_mode, packed.view(self.P // self.g, self.g // 4),
+                            alpha_out=alpha_out)
 
 
 class DenseBlock:
@@ -354,28 +360,35 @@ class DenseBlock:
             self.order("finalize_join", self.side_stream(), torch.cuda.current_stream())
         return self.loss
 
-    def finalize_buffers(self):
-        """Flat codes / scales / packed bytes for the whole arena, with
-        per-linear views."""
+    def finalize_buffers(self, codes=True):
+        """Flat scales / packed bytes (and int8 codes unless ``codes`` is
+        false) for the whole arena, with per-linear views."""
         A = self.arena
-        flat = dict(codes=torch.empty(A.P, dtype=torch.int8, device=DEV),
-                    alpha=torch.empty(A.n_groups, dtype=torch.float32, device=DEV),
+        flat = dict(alpha=torch.empty(A.n_groups, dtype=torch.float32, device=DEV),
                     packed=torch.empty(A.P // 4, dtype=torch.uint8, device=DEV))
+        if codes:
+            flat["codes"] = torch.empty(A.P, dtype=torch.int8, device=DEV)
         out = {"_flat": flat}
         for name, (o, n, shape) in A.spans.items():
-            out[name] = dict(codes=flat["codes"][o:o + n].view(shape),
-                             alpha=flat["alpha"][o // A.g:(o + n) // A.g],
+            out[name] = dict(alpha=flat["alpha"][o // A.g:(o + n) // A.g],
                              packed=flat["packed"][o // 4:(o + n) // 4].view(shape[0], shape[1] // 4))
+            if codes:
+                out[name]["codes"] = flat["codes"][o:o + n].view(shape)
         return out
 
     def finalize(self, bufs):
-        """Hard codes (Eq. 2), group scales and 2-bit packing of every weight
-        (one launch each over the arena)."""
+        """Hard codes (Eq. 2), group scales and 2-bit packing of every weight:
+        with int8 codes requested, the HARD LM+ST writing them and then the
+        packing (one launch each over the arena); without, one launch that
+        writes the packed codes directly (same bits)."""
         p = self.params(HARD)
         A, f = self.arena, bufs["_flat"]
-        A.modulate(p, 1 if self.stats_ready else 0, W_fake=None, codes=f["codes"],
-                   alpha_out=f["alpha"])
-        catq_pack_ternary(A.flat(f["codes"]), f["packed"].view(A.P // A.g, A.g // 4))
+        stats_mode = 1 if self.stats_ready else 0
+        if "codes" in f:
+            A.modulate(p, stats_mode, W_fake=None, codes=f["codes"], alpha_out=f["alpha"])
+            catq_pack_ternary(A.flat(f["codes"]), f["packed"].view(A.P // A.g, A.g // 4))
+        else:
+            A.ternarize_pack(p, stats_mode, f["packed"], f["alpha"])
         self.stats_ready = True
         return bufs
 

@@ -34,6 +34,7 @@ struct FwdArgs {
   float* stats;
   void* Wf;
   int8_t* codes;
+  uint8_t* packed;  // HARD: 2-bit codes, 8 per 16-bit word (pack layout)
   float* alpha_out;
   int64_t n_oct;  // number of 8-element runs
   int64_t s0, s1, s2;
@@ -148,6 +149,17 @@ __global__ __launch_bounds__(256) void lmst_fwd_kernel(FwdArgs a) {
         v.y = hi;
         *reinterpret_cast<uint2*>(a.codes + o * 8) = v;
       }
+      if (a.packed) {
+        // element 8o + j -> bits 2j..2j+1 of the little-endian word at byte
+        // 2o: code + 1 in {0, 1, 2}
+        unsigned int word = 0;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const unsigned int byte = j < 4 ? (lo >> (8 * j)) & 0xffu : (hi >> (8 * (j - 4))) & 0xffu;
+          word |= (unsigned int)((int)(int8_t)byte + 1) << (2 * j);
+        }
+        *reinterpret_cast<unsigned short*>(a.packed + o * 2) = (unsigned short)word;
+      }
     }
     if (a.Wf) store8<OT>(reinterpret_cast<OT*>(a.Wf) + o * 8, out);
   }
@@ -169,7 +181,8 @@ static void launch_fwd_mode(const FwdArgs& a, bool stats, dim3 grid, hipStream_t
   const double ng = n / (8.0 * (1 << a.lg));
   const double fac = 4.0 * ((a.s0 ? ng : 1) + (a.s1 ? ng : 1) + (a.s2 ? ng : 1));
   const double bytes = n * sizeof(WT) + (a.Wf ? n * sizeof(OT) : 0.0) + (a.codes ? n : 0.0) +
-                       fac + 8.0 * ng + (a.alpha_out ? 4.0 * ng : 0.0);
+                       (a.packed ? n / 4.0 : 0.0) + fac + 8.0 * ng +
+                       (a.alpha_out ? 4.0 * ng : 0.0);
   if (stats)
     CATQ_TRACED(stream, tag, 0.0, bytes, (int64_t)n, 0, 0,
                 hipLaunchKernelGGL((lmst_fwd_kernel<WT, OT, MODE, true>), grid, dim3(256), 0,
@@ -506,6 +519,7 @@ extern "C" catq_status catq_modulate_ternarize(const void* W, catq_dtype w_dtype
   a.stats = stats;
   a.Wf = W_fake;
   a.codes = codes;
+  a.packed = nullptr;
   a.alpha_out = alpha_out;
   a.n_oct = d_out * d_in / 8;
   a.s0 = p->factor_stride[0];
@@ -526,6 +540,49 @@ extern "C" catq_status catq_modulate_ternarize(const void* W, catq_dtype w_dtype
   else
     launch_fwd<float, float>(a, p->mode, st, grid, stream);
   CATQ_CHECK_LAUNCH("modulate_ternarize");
+  return CATQ_OK;
+}
+
+extern "C" catq_status catq_ternarize_pack(const void* W, catq_dtype w_dtype, int64_t d_out,
+                                           int64_t d_in, const float* d_mu, const float* d_alpha,
+                                           const float* d_delta, const catq_lmst_params* p,
+                                           float* stats, int32_t stats_mode, uint8_t* packed,
+                                           float* alpha_out, hipStream_t stream) {
+  clear_error();
+  CATQ_REQUIRE(W && d_mu && d_alpha && d_delta && stats && packed, CATQ_ERR_NULL,
+               "W, factors, stats and packed must not be NULL");
+  CATQ_REQUIRE(d_out > 0 && d_in > 0, CATQ_ERR_SHAPE, "d_out and d_in must be > 0");
+  CATQ_TRY(check_lmst_params(p, d_in));
+  CATQ_REQUIRE(p->mode == CATQ_HARD, CATQ_ERR_VALUE, "the packed codes are those of HARD mode");
+  CATQ_REQUIRE(dtype_ok(w_dtype), CATQ_ERR_DTYPE, "bad dtype");
+  CATQ_REQUIRE(stats_mode == 0 || stats_mode == 1, CATQ_ERR_VALUE, "stats_mode must be 0 or 1");
+  CATQ_REQUIRE(aligned16(W) && aligned16(packed) && aligned16(stats), CATQ_ERR_ALIGN,
+               "W, packed and stats must be 16-byte aligned");
+  FwdArgs a;
+  a.W = W;
+  a.dmu = d_mu;
+  a.dal = d_alpha;
+  a.dde = d_delta;
+  a.stats = stats;
+  a.Wf = nullptr;
+  a.codes = nullptr;
+  a.packed = packed;
+  a.alpha_out = alpha_out;
+  a.n_oct = d_out * d_in / 8;
+  a.s0 = p->factor_stride[0];
+  a.s1 = p->factor_stride[1];
+  a.s2 = p->factor_stride[2];
+  a.lg = ilog2(p->group_size / 8);
+  a.delta0 = p->delta0;
+  a.st = make_st(1.0);
+  a.inv_g = 1.0f / (float)p->group_size;
+  dim3 grid((unsigned)((a.n_oct + 256 * FWD_U - 1) / (256 * FWD_U)));
+  const bool st = stats_mode == 0;
+  if (w_dtype == CATQ_BF16)
+    launch_fwd_mode<bf16, bf16, CATQ_HARD>(a, st, grid, stream);
+  else
+    launch_fwd_mode<float, bf16, CATQ_HARD>(a, st, grid, stream);
+  CATQ_CHECK_LAUNCH("ternarize_pack");
   return CATQ_OK;
 }
 

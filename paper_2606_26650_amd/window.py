@@ -97,8 +97,8 @@ class Window:
         self.modulate_all(self.params(IDENTITY))
         return self.forward(x, out)
 
-    def finalize_buffers(self):
-        return [b.finalize_buffers() for b in self.blocks]
+    def finalize_buffers(self, codes=True):
+        return [b.finalize_buffers(codes) for b in self.blocks]
 
     def finalize(self, bufs):
         """Hard codes, group scales and 2-bit packing of every block."""

@@ -79,6 +79,31 @@ def test_modulate_validation(cq):
     assert "aligned" in msg
 
 
+def test_ternarize_pack_validation(cq):
+    """The fused hard ternarisation + packing rejects everything before any
+    launch: NULL pointers, a mode other than HARD, shapes, dtypes, alignment."""
+    L = cq.lib
+    hard = cq.lmst_params(mode=cq.HARD)
+
+    def tp(p, W=FAKE, w_dt=1, d_out=4, d_in=256, stats=FAKE, mode_st=1, packed=FAKE):
+        return L.catq_ternarize_pack(W, w_dt, d_out, d_in, FAKE, FAKE, FAKE,
+                                     None if p is None else C.byref(p), stats, mode_st, packed,
+                                     None, None)
+
+    assert tp(hard, W=None) == 1
+    assert tp(hard, packed=None) == 1
+    assert tp(hard, stats=None) == 1
+    assert tp(None) == 1
+    assert tp(cq.lmst_params(mode=cq.SOFT, s=10.0)) == 4
+    assert tp(cq.lmst_params(mode=cq.IDENTITY)) == 4
+    assert tp(hard, d_out=0) == 2
+    assert tp(hard, d_in=96) == 2
+    assert tp(hard, w_dt=5) == 3
+    assert tp(hard, mode_st=2) == 4
+    assert tp(hard, packed=FAKE + 2) == 5
+    assert "aligned" in L.catq_last_error_message().decode()
+
+
 def test_linear_and_loss_validation(cq):
     L = cq.lib
     fwd = L.catq_fakeq_linear_fwd

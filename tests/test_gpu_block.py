@@ -158,6 +158,13 @@ def test_finalize_codes_and_pack(catq):
             np.testing.assert_array_equal(cs[k], r["codes"])
             np.testing.assert_array_equal(ps[k], lmst.pack_ternary(r["codes"]))
             np.testing.assert_array_equal(al[k].reshape(-1), r["alpha"])
+    # without int8 codes the finalize writes the packed codes in one launch:
+    # the same bytes and scales
+    fused = blk.finalize(blk.finalize_buffers(codes=False))
+    torch.cuda.synchronize()
+    assert "codes" not in fused["_flat"]
+    assert torch.equal(fused["_flat"]["packed"], bufs["_flat"]["packed"])
+    assert torch.equal(fused["_flat"]["alpha"], bufs["_flat"]["alpha"])
 
 
 def test_block_step_deterministic(catq):

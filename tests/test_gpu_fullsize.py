@@ -101,7 +101,12 @@ def _check_weight_rows(catq, blk, W, cfg, fac, seed):
                                       lmst.pack_ternary(rh["codes"]), err_msg=name)
         np.testing.assert_array_equal(b["alpha"][grp_t].cpu().numpy().astype(np.float64),
                                       rh["alpha"], err_msg=name)
-    del bufs
+    # the one-launch finalize (no int8 codes) writes the same bytes and scales
+    fused = blk.finalize(blk.finalize_buffers(codes=False))
+    torch.cuda.synchronize()
+    assert torch.equal(fused["_flat"]["packed"], bufs["_flat"]["packed"])
+    assert torch.equal(fused["_flat"]["alpha"], bufs["_flat"]["alpha"])
+    del bufs, fused
 
 
 def _check_step_properties(blk, x, y_fp):

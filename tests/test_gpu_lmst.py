@@ -178,6 +178,43 @@ def test_pack_bit_exact(catq):
     assert int(pk.item()) == 0x46
 
 
+@pytest.mark.parametrize("rows,d_in,g,wdtype,shared,stats_mode", [
+    (41, 640, 128, "bf16", (1, 1, 1), 0), (41, 640, 128, "f32", (1, 1, 1), 0),
+    (7, 96, 16, "bf16", (0, 1, 0), 0), (300, 1024, 512, "bf16", (1, 1, 1), 1),
+    (1, 128, 128, "bf16", (1, 1, 1), 0)])
+def test_ternarize_pack_bit_exact(catq, rows, d_in, g, wdtype, shared, stats_mode):
+    """The fused hard ternarisation + packing: packed bytes equal the oracle's
+    packing of the oracle's hard codes, scales (and computed statistics) bit
+    for bit, and the same bytes as the two-launch path (codes, then pack)."""
+    import torch
+    Wo, Wd, fac = _case(9, rows, d_in, g, wdtype, shared=shared)
+    ng = rows * d_in // g
+    dm, da, dd = (to_dev_f32(f) for f in fac)
+    p = catq.lmst_params(group_size=g, mode=catq.HARD, strides=shared)
+    stats = torch.zeros(ng, 2, dtype=torch.float32, device="cuda")
+    if stats_mode == 1:  # statistics from an earlier soft call on the same W
+        wf = torch.empty(rows, d_in, dtype=torch.bfloat16, device="cuda")
+        catq.catq_modulate_ternarize(Wd, dm, da, dd, catq.lmst_params(group_size=g, mode=catq.SOFT,
+                                                                      s=5.0, strides=shared),
+                                     stats, 0, W_fake=wf)
+    packed = torch.full((rows, d_in // 4), 0xAB, dtype=torch.uint8, device="cuda")
+    alpha = torch.full((ng,), float("nan"), dtype=torch.float32, device="cuda")
+    catq.catq_ternarize_pack(Wd, dm, da, dd, p, stats, stats_mode, packed, alpha_out=alpha)
+    stats2 = stats.clone()
+    codes = torch.empty(rows, d_in, dtype=torch.int8, device="cuda")
+    packed2 = torch.empty_like(packed)
+    catq.catq_modulate_ternarize(Wd, dm, da, dd, p, stats2, 1, codes=codes)
+    catq.catq_pack_ternary(codes, packed2)
+    torch.cuda.synchronize()
+    ref = lmst.modulate_ternarize(Wo, g, *fac, lmst.HARD, strides=shared)
+    np.testing.assert_array_equal(packed.cpu().numpy(), lmst.pack_ternary(ref["codes"]))
+    assert torch.equal(packed, packed2)
+    np.testing.assert_array_equal(alpha.cpu().numpy().astype(np.float64), ref["alpha"])
+    st = stats.cpu().numpy().astype(np.float64)
+    np.testing.assert_array_equal(st[:, 0], ref["mu0"])
+    np.testing.assert_array_equal(st[:, 1], ref["alpha0"])
+
+
 def test_loss_parity(catq):
     import torch
     for n, dtype in [(8, "bf16"), (4096 * 3 + 8, "bf16"), (1 << 21, "bf16"), (40000, "f32")]:
