@@ -175,6 +175,11 @@ catq_status catq_fakeq_linear_fwd(const void* X, const void* W_fake, catq_dtype 
  * a caller can so run the input-gradient half and the weight-gradient half
  * (dX NULL) on two streams.  Otherwise all three gradient outputs are
  * required.
+ * Where G needs no split of the token contraction (routed experts, or a
+ * dense shape the library leaves unsplit) and bf16 operands, 128-weight
+ * groups and no dW_fake are given, the factor gradients are reduced inside
+ * the G product and G is not stored; they then agree with the two-pass
+ * result up to the order of the fp32 sums (deterministic either way).
  * Requires N % 8 == 0 and K % 8 == 0.
  */
 catq_status catq_fakeq_linear_bwd(const void* dY, const void* X, const void* W_fake,
