@@ -173,6 +173,41 @@ __device__ __forceinline__ bf16x8 tfrag_tr(const uint4* lds, int col0, int slice
   return __builtin_bit_cast(bf16x8, u);
 }
 
+// Per-lane offsets (in bf16 elements) of the two transpose reads of
+// tfrag_tr for each 32-column block i of a 64 x D tile.  The swizzle key of
+// a row does not depend on its 16-row slice, so the reads of slice `slice`
+// sit 16 * slice rows further: tr_read adds that as a constant.
+template <int D>
+struct TrOffsets {
+  int o[D / 32][2];
+  __device__ __forceinline__ void init(int lane) {
+    const int blk = lane >> 4, s = lane & 15;
+#pragma unroll
+    for (int i = 0; i < D / 32; ++i)
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        const int col = i * 32 + 16 * (blk & 1) + 4 * (s & 3);
+        const int row = 4 * (blk >> 1) + 8 * c + (s >> 2);
+        o[i][c] = row * D + (((col >> 3) ^ tswz<D>(row)) << 3) + (col & 7);
+      }
+  }
+};
+
+// tfrag_tr<D>(lds, 32 * i, slice, lane) from precomputed offsets
+template <int D>
+__device__ __forceinline__ bf16x8 tr_read(const uint4* lds, const TrOffsets<D>& t, int i,
+                                          int slice) {
+  const short* base = reinterpret_cast<const short*>(lds) + 16 * slice * D;
+  u32x4 u;
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    const lds_v4s v = lds_read_tr16(base + t.o[i][c]);
+    u[2 * c] = (unsigned)(unsigned short)v[0] | ((unsigned)(unsigned short)v[1] << 16);
+    u[2 * c + 1] = (unsigned)(unsigned short)v[2] | ((unsigned)(unsigned short)v[3] << 16);
+  }
+  return __builtin_bit_cast(bf16x8, u);
+}
+
 }  // namespace fa
 
 // ------------------------------------------------------------------ forward
@@ -211,6 +246,8 @@ __global__ __launch_bounds__(fa::NT, 2) void flash_fwd_kernel(FaArgs a) {
   const int q_last = min(q0 + 127, a.S - 1);
   const int nkt = q_last / fa::BK + 1;
   const int wave_first = q0 + 32 * w, wave_last = wave_first + 31;
+  fa::TrOffsets<D> tro;
+  tro.init(lane);
   auto issue = [&](int buf, int k0) {
     fa::dma_tile<D>(Kb, D, k0, a.S, sK[buf], w, lane);
     fa::dma_tile<D>(Vb, D, k0, a.S, sV[buf], w, lane);
@@ -285,7 +322,7 @@ __global__ __launch_bounds__(fa::NT, 2) void flash_fwd_kernel(FaArgs a) {
 #pragma unroll
           for (int i = 0; i < C::DB; ++i)
             o[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                fa::tfrag_tr<D>(sV[buf], i * 32, 2 * sb + hh, lane), pf, o[i], 0, 0, 0);
+                fa::tr_read<D>(sV[buf], tro, i, 2 * sb + hh), pf, o[i], 0, 0, 0);
         }
       }
       rs += __shfl_xor(rs, 32, 64);
@@ -533,6 +570,8 @@ __global__ __launch_bounds__(fa::NT, 2) void flash_bwd_dq_kernel(FaArgs a) {
   const int q_last = min(q0 + 127, a.S - 1);
   const int nkt = q_last / fa::BK + 1;
   const int wave_last = q0 + 32 * w + 31;
+  fa::TrOffsets<D> tro;
+  tro.init(lane);
   // K and V tiles of 64 keys stream into swizzled row-major LDS tiles by
   // direct copies (rows past the sequence read the last row; their P is 0);
   // K^T fragments come from transpose reads of the same K tile
@@ -582,7 +621,7 @@ __global__ __launch_bounds__(fa::NT, 2) void flash_bwd_dq_kernel(FaArgs a) {
 #pragma unroll
           for (int i = 0; i < C::DB; ++i)
             dq[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                fa::tfrag_tr<D>(sK[buf], i * 32, 2 * sb + hh, lane), df, dq[i], 0, 0, 0);
+                fa::tr_read<D>(sK[buf], tro, i, 2 * sb + hh), df, dq[i], 0, 0, 0);
         }
       }
     }
