@@ -131,11 +131,13 @@ __global__ __launch_bounds__(256) void lmst_fwd_kernel(FwdArgs a) {
         out[j] = gs.alpha * transition_f(xs, gs.delta, ED, a.st);
       }
     } else {  // HARD
-      const double theta = (double)gs.delta * (double)gs.alpha_div;
+      const HardThresh th = hard_thresh(gs.delta, gs.alpha_div);
+      float cs[8];
+      hard_codes8(w[u], gs.mu, th, cs);
       unsigned int lo = 0, hi = 0;
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        float c = hard_code(w[u][j], gs.mu, theta);
+        const float c = cs[j];
         out[j] = gs.alpha * c;
         unsigned int byte = (unsigned int)(int)c & 0xffu;
         if (j < 4)
@@ -295,7 +297,8 @@ __global__ __launch_bounds__(256) void lmst_bwd_kernel(BwdArgs a) {
   if (a.mode != CATQ_IDENTITY) {
     const float inv_a = 1.0f / gs.alpha_div;
     const float ED = one_minus_exp_neg(gs.delta * a.st.s4, gs.delta * a.st.s4l);
-    const double theta = (double)gs.delta * (double)gs.alpha_div;
+    float hc[8];
+    if (a.mode == CATQ_HARD) hard_codes8(w, gs.mu, hard_thresh(gs.delta, gs.alpha_div), hc);
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       float xs = (w[j] - gs.mu) * inv_a;
@@ -307,7 +310,7 @@ __global__ __launch_bounds__(256) void lmst_bwd_kernel(BwdArgs a) {
       } else {
         transition_parts(xs, gs.delta, ED, a.st, f, fW, fD);
       }
-      float T = (a.mode == CATQ_HARD) ? hard_code(w[j], gs.mu, theta) : f;
+      float T = (a.mode == CATQ_HARD) ? hc[j] : f;
       ST = fmaf(G[j], T, ST);
       float gf = G[j] * fW;
       S1 += gf;

@@ -62,6 +62,44 @@ __device__ __forceinline__ float hard_code(float w, float mu, double theta) {
   return (float)((r > theta) - (r < -theta));
 }
 
+// The same decision with a float32 screen.  With r = w - mu and
+// theta = Delta*alpha exact, r32 = fl(r) and b = fl(Delta*alpha) each carry a
+// relative error of at most 2^-24 (a difference of floats that falls below
+// the normal range is exact), so |r32| > b (1 + 2^-21) proves |r| > theta
+// and |r32| < b (1 - 2^-21) proves |r| < theta; only the band between them,
+// and thresholds outside [2^-120, 2^120] (zero, negative, NaN, huge), go to
+// the exact float64 comparison.
+struct HardThresh {
+  double theta;
+  float hi, lo;
+};
+__device__ __forceinline__ HardThresh hard_thresh(float delta, float alpha_div) {
+  HardThresh t;
+  t.theta = (double)delta * (double)alpha_div;
+  const float b = delta * alpha_div;
+  const bool ok = b >= 0x1p-120f && b <= 0x1p+120f;  // false for NaN
+  t.hi = ok ? b * (1.0f + 0x1p-21f) : __builtin_inff();
+  t.lo = ok ? b * (1.0f - 0x1p-21f) : -1.0f;
+  return t;
+}
+// Codes of 8 weights of one group: the screen for all 8, and the exact
+// comparison for all 8 when any of them falls in the band (rare; one branch).
+__device__ __forceinline__ void hard_codes8(const float (&w)[8], float mu, const HardThresh& t,
+                                            float (&c)[8]) {
+  bool band = false;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const float r = w[j] - mu;
+    const float a = fabsf(r);
+    c[j] = a > t.hi ? copysignf(1.0f, r) : 0.0f;
+    band |= !(a > t.hi) && !(a < t.lo);
+  }
+  if (band) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) c[j] = hard_code(w[j], mu, t.theta);
+  }
+}
+
 // Transition function f of Eq. 5 at x_hat (cancellation-free form).
 __device__ __forceinline__ float transition_f(float xs, float delta, float ED, const StConst& c) {
   float x = fabsf(xs);

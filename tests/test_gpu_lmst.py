@@ -215,6 +215,44 @@ def test_ternarize_pack_bit_exact(catq, rows, d_in, g, wdtype, shared, stats_mod
     np.testing.assert_array_equal(st[:, 1], ref["alpha0"])
 
 
+def test_hard_codes_near_threshold(catq):
+    """Thresholds placed within a few float32 ulps of |W - mu| of one weight
+    per group (so the float32 screen defers to the exact float64 decision),
+    plus zero, negative, NaN and huge thresholds: codes bit-exact against the
+    oracle, through both the codes path and the one-pass packing."""
+    import torch
+    rows, d_in, g = 64, 256, 128
+    bits = sg.normal_bf16(21, "W", (rows, d_in), std=0.02)
+    Wo = f64(bits)
+    ng = rows * d_in // g
+    rng = np.random.default_rng(21)
+    d_mu = (rng.standard_normal(ng) * 0.1).astype(np.float32)
+    d_alpha = (1.0 + rng.standard_normal(ng) * 0.1).astype(np.float32)
+    mu0, alpha0 = lmst.group_stats(Wo, g)
+    mu, alpha, _ = lmst.modulation(mu0, alpha0, d_mu, d_alpha, np.ones(ng, np.float32))
+    r = np.abs(Wo.reshape(ng, g)[np.arange(ng), rng.integers(0, g, ng)] - mu)
+    base = (r / lmst.safe_alpha(alpha) / 0.5).astype(np.float32)
+    ulps = rng.integers(-3, 4, ng).astype(np.int32)
+    d_delta = (base.view(np.int32) + ulps).view(np.float32)
+    d_delta[:4] = [0.0, -0.5, np.nan, 1e30]
+    fac = [d_mu, d_alpha, d_delta]
+    dm, da, dd = (to_dev_f32(f) for f in fac)
+    p = catq.lmst_params(group_size=g, mode=catq.HARD)
+    stats = torch.zeros(ng, 2, dtype=torch.float32, device="cuda")
+    codes = torch.empty(rows, d_in, dtype=torch.int8, device="cuda")
+    packed = torch.empty(rows, d_in // 4, dtype=torch.uint8, device="cuda")
+    Wd = to_dev_bf16(bits)
+    catq.catq_modulate_ternarize(Wd, dm, da, dd, p, stats, 0, codes=codes)
+    catq.catq_ternarize_pack(Wd, dm, da, dd, p, stats, 1, packed)
+    torch.cuda.synchronize()
+    ref = lmst.modulate_ternarize(Wo, g, *fac, lmst.HARD)["codes"]
+    np.testing.assert_array_equal(codes.cpu().numpy(), ref)
+    np.testing.assert_array_equal(packed.cpu().numpy(), lmst.pack_ternary(ref))
+    # the placed weights decide both ways across the groups
+    placed = ref.reshape(ng, g)
+    assert (placed != 0).any() and (placed == 0).any()
+
+
 def test_loss_parity(catq):
     import torch
     for n, dtype in [(8, "bf16"), (4096 * 3 + 8, "bf16"), (1 << 21, "bf16"), (40000, "f32")]:
