@@ -746,7 +746,7 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
         // l % SR (its 64 columns lie in one group), handed to the lanes of
         // that row by shuffles in each pass
         [[maybe_unused]] float p_mu = 0.f, p_inva = 0.f, p_delta = 0.f, p_ed = 0.f;
-        [[maybe_unused]] double p_theta = 0.0;
+        [[maybe_unused]] HardThresh p_th = {0.0, 0.f, 0.f};
         if constexpr (EPI == 3) {
           const FacEpi& F = g.fac;
           const int64_t wrow = (int64_t)z * g.M + min(mrow + (lane % SR), m_lim - 1);
@@ -758,7 +758,7 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
           p_inva = 1.0f / gs.alpha_div;
           p_delta = gs.delta;
           p_ed = one_minus_exp_neg(gs.delta * F.st.s4, gs.delta * F.st.s4l);
-          p_theta = (double)gs.delta * (double)gs.alpha_div;
+          p_th = hard_thresh(gs.delta, gs.alpha_div);
         }
 #pragma unroll
         for (int j = 0; j < FN; ++j)
@@ -783,15 +783,23 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
             const int src = q * RPP + lane / LPR;
             const float mu = __shfl(p_mu, src, 64), inv_a = __shfl(p_inva, src, 64);
             const float delta = __shfl(p_delta, src, 64), ED = __shfl(p_ed, src, 64);
-            const double theta = __shfl(p_theta, src, 64);
             if (m < m_lim && n < g.N && F.mode != CATQ_IDENTITY) {
               const f32x4 w = widen4(gv[q]);
+              float hc[4];
+              if (F.mode == CATQ_HARD) {
+                HardThresh th;
+                th.theta = __shfl(p_th.theta, src, 64);
+                th.hi = __shfl(p_th.hi, src, 64);
+                th.lo = __shfl(p_th.lo, src, 64);
+                const float w4[4] = {w[0], w[1], w[2], w[3]};
+                hard_codes_n<4>(w4, mu, th, hc);
+              }
 #pragma unroll
               for (int e = 0; e < 4; ++e) {
                 const float xs = (w[e] - mu) * inv_a;
                 float f = 0.f, fW = 1.f, fD = 0.f;
                 if (!F.ste) transition_parts(xs, delta, ED, F.st, f, fW, fD);
-                const float T = (F.mode == CATQ_HARD) ? hard_code(w[e], mu, theta) : f;
+                const float T = (F.mode == CATQ_HARD) ? hc[e] : f;
                 sT = fmaf(v[e], T, sT);
                 const float gf = v[e] * fW;
                 s1 += gf;

@@ -82,13 +82,14 @@ __device__ __forceinline__ HardThresh hard_thresh(float delta, float alpha_div) 
   t.lo = ok ? b * (1.0f - 0x1p-21f) : -1.0f;
   return t;
 }
-// Codes of 8 weights of one group: the screen for all 8, and the exact
-// comparison for all 8 when any of them falls in the band (rare; one branch).
-__device__ __forceinline__ void hard_codes8(const float (&w)[8], float mu, const HardThresh& t,
-                                            float (&c)[8]) {
+// Codes of N weights of one group: the screen for all N, and the exact
+// comparison for all N when any of them falls in the band (rare; one branch).
+template <int N>
+__device__ __forceinline__ void hard_codes_n(const float (&w)[N], float mu, const HardThresh& t,
+                                             float (&c)[N]) {
   bool band = false;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
+  for (int j = 0; j < N; ++j) {
     const float r = w[j] - mu;
     const float a = fabsf(r);
     c[j] = a > t.hi ? copysignf(1.0f, r) : 0.0f;
@@ -96,8 +97,12 @@ __device__ __forceinline__ void hard_codes8(const float (&w)[8], float mu, const
   }
   if (band) {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) c[j] = hard_code(w[j], mu, t.theta);
+    for (int j = 0; j < N; ++j) c[j] = hard_code(w[j], mu, t.theta);
   }
+}
+__device__ __forceinline__ void hard_codes8(const float (&w)[8], float mu, const HardThresh& t,
+                                            float (&c)[8]) {
+  hard_codes_n<8>(w, mu, t, c);
 }
 
 // Transition function f of Eq. 5 at x_hat (cancellation-free form).
