@@ -25,3 +25,17 @@ def test_bench_refuses_a_multi_rank_launch():
     r = _run([], {"WORLD_SIZE": "4"})
     assert r.returncode == 2
     assert "one GPU" in r.stderr
+
+
+def test_cpu_baseline_fields_small_block():
+    """The CPU baseline (the oracle timed on the step) on a small dense block:
+    the reported fields and a positive rate."""
+    sys.path.insert(0, ROOT)
+    import bench
+    import synthgen as sg
+    cfg = sg.small_dense(batch=2, seq=32, hidden=256, n_q=4, n_kv=2, head_dim=64, ffn=384)
+    r = bench.cpu_baseline(cfg, sg.block_weights(cfg, 0), sg.activations(cfg, 0))
+    assert r["kind"] == "oracle" and r["unit"] == "block-steps/s"
+    assert r["value"] > 0 and r["cores"] >= 1
+    assert abs(r["value"] * r["seconds_per_step"] - 1.0) < 1e-9
+    assert "all rows" in r["sample"] and "2 of the 2 samples" in r["sample"]
