@@ -716,32 +716,46 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
     const int cc = (lane % LPR) * 4;
     const int64_t n = n0 + wn * WTN + cc;
     const int64_t n_c = min(n, g.N - 4);   // clamped column for the early loads
+    // The parts' other inputs (residual, or gate and up of the forward, or
+    // the weights) are loaded one part ahead: those of part p + 1 are in
+    // flight while part p goes through LDS and out.  Rows clamped into the
+    // matrix, the values of lanes outside it unused.
+    constexpr int HP = 32 / SR, PARTS = FM * HP;
+    using RawR = decltype(raw4((const RT*)nullptr));
+    [[maybe_unused]] RawR rvb[2][NP];
+    [[maybe_unused]] uint2 gvb[2][NP], uvb[2][NP];
+    auto load_part = [&](int p, int slot) {
+      const int64_t mr = m0 + wm * WTM + (p / HP) * 32 + (p % HP) * SR;
 #pragma unroll
-    for (int i = 0; i < FM; ++i) {
-#pragma unroll
-      for (int h = 0; h < 32 / SR; ++h) {
-        const int64_t mrow = m0 + wm * WTM + i * 32 + h * SR;
-        // The part's other inputs (residual, or gate and up of the forward)
-        // are loaded for all its passes before the LDS round trip, so their
-        // latency is paid once; rows clamped into the matrix, the values of
-        // lanes outside it unused.
-        using RawR = decltype(raw4((const RT*)nullptr));
-        [[maybe_unused]] RawR rv[NP];
-        [[maybe_unused]] uint2 gv[NP], uv[NP];
-#pragma unroll
-        for (int q = 0; q < NP; ++q) {
-          const int64_t m_c = min(mrow + q * RPP + lane / LPR, m_lim - 1);
-          if constexpr (EPI == 2) {
-            const bf16* gu = reinterpret_cast<const bf16*>(g.aux0) + m_c * g.ld_aux;
-            gv[q] = raw4(gu + n_c);
-            uv[q] = raw4(gu + g.N + n_c);
-          } else if constexpr (EPI == 0 && HAS_R) {
-            rv[q] = raw4(R + m_c * g.ldr + n_c);
-          } else if constexpr (EPI == 3) {
-            gv[q] = raw4(reinterpret_cast<const bf16*>(g.fac.W) + ((int64_t)z * g.M + m_c) * g.N +
-                         n_c);
-          }
+      for (int q = 0; q < NP; ++q) {
+        const int64_t m_c = min(mr + q * RPP + lane / LPR, m_lim - 1);
+        if constexpr (EPI == 2) {
+          const bf16* gu = reinterpret_cast<const bf16*>(g.aux0) + m_c * g.ld_aux;
+          gvb[slot][q] = raw4(gu + n_c);
+          uvb[slot][q] = raw4(gu + g.N + n_c);
+        } else if constexpr (EPI == 0 && HAS_R) {
+          rvb[slot][q] = raw4(R + m_c * g.ldr + n_c);
+        } else if constexpr (EPI == 3) {
+          gvb[slot][q] = raw4(reinterpret_cast<const bf16*>(g.fac.W) +
+                              ((int64_t)z * g.M + m_c) * g.N + n_c);
         }
+      }
+    };
+    // (the factor epilogue holds too many registers to load ahead: there
+    // each part loads its own weights first)
+    if constexpr (EPI != 3) load_part(0, 0);
+#pragma unroll
+    for (int p = 0; p < PARTS; ++p) {
+      const int i = p / HP, h = p % HP;
+      {
+        const int64_t mrow = m0 + wm * WTM + i * 32 + h * SR;
+        if constexpr (EPI == 3)
+          load_part(p, p & 1);
+        else if (p + 1 < PARTS)
+          load_part(p + 1, (p + 1) & 1);
+        [[maybe_unused]] auto& rv = rvb[p & 1];
+        [[maybe_unused]] auto& gv = gvb[p & 1];
+        [[maybe_unused]] auto& uv = uvb[p & 1];
         // factor epilogue: lane l holds the group scalars of the part's row
         // l % SR (its 64 columns lie in one group), handed to the lanes of
         // that row by shuffles in each pass
