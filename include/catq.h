@@ -377,10 +377,12 @@ catq_status catq_aux_moe_scatter_add(const void* dxg, const int32_t* perm_row, i
  * AdamW on one factor array (fp32 [n]): m, v moments updated in place,
  * p -= lr * mhat / (sqrt(vhat) + eps), no weight decay; then clamped to
  * [lo, hi] (the constraints -1 < d_mu < 1, d_alpha > 0, d_Delta > 0 of Sec. 2.2).
- * step is 1-based.
+ * step is 1-based.  beta1, beta2 and eps are taken in double: the kernel's
+ * 1 - beta and the bias corrections are formed from them in double and
+ * rounded once to fp32 (1 - (float)0.999 would miss 0.001 by 1.3e-5).
  */
 catq_status catq_aux_adamw(float* p, const float* grad, float* m, float* v, int64_t n,
-                           int64_t step, float lr, float beta1, float beta2, float eps, float lo,
+                           int64_t step, float lr, double beta1, double beta2, double eps, float lo,
                            float hi, hipStream_t stream);
 
 /* Elementwise y = a + b (bf16 or f32), n % 8 == 0. */

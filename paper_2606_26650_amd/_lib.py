@@ -74,7 +74,7 @@ SIGNATURES = {
     "catq_aux_moe_combine": [P, P, P, P, I64, I32, I64, P, I32, P],
     "catq_aux_moe_combine_bwd": [P, P, P, I64, I32, I64, P, P],
     "catq_aux_moe_scatter_add": [P, P, I64, I32, I64, P, P],
-    "catq_aux_adamw": [P, P, P, P, I64, I64, F, F, F, F, F, F, P],
+    "catq_aux_adamw": [P, P, P, P, I64, I64, F, C.c_double, C.c_double, C.c_double, F, F, P],
     "catq_aux_add": [P, P, P, I32, I64, P],
     "catq_trace_enable": [I32],
     "catq_trace_pause": [I32],

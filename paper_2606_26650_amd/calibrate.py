@@ -73,6 +73,10 @@ class BlockCalibrator:
         self.step_no = 0          # optimiser steps taken
         self.epoch = 0            # next epoch to run
         self.losses = []          # one device scalar per step (copied)
+        # optional callable(phase, calibrator, batch, mode, s, lr): "grads"
+        # after a step's backward (factors and moments not yet updated),
+        # "update" after its AdamW launches
+        self.observer = None
         self.targets = [block.new_output() for _ in range(self.n_batches)]
         for b in range(self.n_batches):
             block.target(self.batch(b), self.targets[b])
@@ -89,8 +93,12 @@ class BlockCalibrator:
             self.losses.append(loss.clone())
             self.step_no += 1
             lr = linear_lr(self.step_no - 1, self.total_steps, self.lr0)
+            if self.observer is not None:
+                self.observer("grads", self, b, mode, s, lr)
             for p, g, m, v, (lo, hi) in zip(self.params, self.grads, self.m, self.v, self.bounds):
                 catq_aux_adamw(p, g, m, v, self.step_no, lr, lo=lo, hi=hi)
+            if self.observer is not None:
+                self.observer("update", self, b, mode, s, lr)
         self.epoch += 1
 
     def run(self, checkpoint_dir: str | None = None):

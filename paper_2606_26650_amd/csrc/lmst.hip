@@ -461,14 +461,16 @@ __global__ __launch_bounds__(256) void pack_kernel(const int8_t* codes, int64_t 
 // ----------------------------------------------------------------- adamw
 
 __global__ __launch_bounds__(256) void adamw_kernel(float* p, const float* g, float* m, float* v,
-                                                    int64_t n, float lr, float b1, float b2,
-                                                    float eps, float inv_bc1, float inv_sqrt_bc2,
-                                                    float lo, float hi) {
+                                                    int64_t n, float lr, float b1, float c1,
+                                                    float b2, float c2, float eps, float inv_bc1,
+                                                    float inv_sqrt_bc2, float lo, float hi) {
+  // c1 = 1 - beta1 and c2 = 1 - beta2 are formed in double on the host and
+  // rounded once: 1 - (float)0.999 would be 1.3e-5 off 0.001.
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
   float gi = g[i];
-  float mi = fmaf(b1, m[i], (1.0f - b1) * gi);
-  float vi = fmaf(b2, v[i], (1.0f - b2) * gi * gi);
+  float mi = fmaf(b1, m[i], c1 * gi);
+  float vi = fmaf(b2, v[i], c2 * gi * gi);
   m[i] = mi;
   v[i] = vi;
   float upd = (mi * inv_bc1) / (sqrtf(vi) * inv_sqrt_bc2 + eps);
@@ -609,17 +611,18 @@ extern "C" catq_status catq_pack_ternary(const int8_t* codes, int64_t d_out, int
 }
 
 extern "C" catq_status catq_aux_adamw(float* p, const float* grad, float* m, float* v, int64_t n,
-                                      int64_t step, float lr, float beta1, float beta2, float eps,
-                                      float lo, float hi, hipStream_t stream) {
+                                      int64_t step, float lr, double beta1, double beta2,
+                                      double eps, float lo, float hi, hipStream_t stream) {
   clear_error();
   CATQ_REQUIRE(p && grad && m && v, CATQ_ERR_NULL, "NULL argument");
   CATQ_REQUIRE(n > 0 && step >= 1, CATQ_ERR_SHAPE, "n must be > 0 and step >= 1");
   CATQ_REQUIRE(beta1 >= 0 && beta1 < 1 && beta2 >= 0 && beta2 < 1 && eps > 0 && lo <= hi,
                CATQ_ERR_VALUE, "bad optimizer hyper-parameters");
-  const double bc1 = 1.0 - std::pow((double)beta1, (double)step);
-  const double bc2 = 1.0 - std::pow((double)beta2, (double)step);
+  const double bc1 = 1.0 - std::pow(beta1, (double)step);
+  const double bc2 = 1.0 - std::pow(beta2, (double)step);
   hipLaunchKernelGGL(adamw_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, p,
-                     grad, m, v, n, lr, beta1, beta2, eps, (float)(1.0 / bc1),
+                     grad, m, v, n, lr, (float)beta1, (float)(1.0 - beta1), (float)beta2,
+                     (float)(1.0 - beta2), (float)eps, (float)(1.0 / bc1),
                      (float)(1.0 / std::sqrt(bc2)), lo, hi);
   CATQ_CHECK_LAUNCH("adamw");
   return CATQ_OK;

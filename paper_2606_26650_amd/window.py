@@ -150,6 +150,10 @@ class SlidingCalibrator:
         if x_all.shape[0] % self.tok_per_batch:
             raise ValueError("the calibration set must hold whole batches of samples")
         self.history = []     # (span, loss history) per finished window
+        # optional observer handed to each window's BlockCalibrator (see
+        # there); self.span names the window being calibrated
+        self.observer = None
+        self.span = None
 
     def _fp_forward(self, blk, acts):
         """Full-precision output of one block on every batch (fp32)."""
@@ -171,6 +175,8 @@ class SlidingCalibrator:
                 at += 1
             win = Window(self.blocks[a:e])
             cal = BlockCalibrator(win, acts, self.n_epochs, self.gamma, self.s0, self.lr0)
+            cal.observer = self.observer
+            self.span = (a, e)
             ck = None
             if checkpoint_dir:
                 ck = os.path.join(checkpoint_dir, f"window{w:03d}_blocks{a:03d}-{e:03d}")
