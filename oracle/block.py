@@ -120,17 +120,31 @@ def _aq(x, group):
     return actquant.quantize(actquant.bf16_round(x32), group)[0]
 
 
+def _q8(a8, name, x, group):
+    """The W1.58A8 quantized value of activation ``name``: the quantizer on
+    the oracle's own value, or, when ``a8`` is a dict, the quantized
+    activation given there (same shape), so that a comparison can take the
+    quantizer's code decisions from another computation of the same step."""
+    if isinstance(a8, dict):
+        q = np.asarray(a8[name], np.float64)
+        assert q.shape == x.shape, (name, q.shape, x.shape)
+        return q
+    return _aq(x, group)
+
+
 def attn_forward(x, W, cfg, a8=False):
     """x [M][h] -> h1 = x + o_proj(attention(...)).  W maps names to [d_out][d_in].
     a8: the inputs of q|k|v and o, and Q, K, V of the attention products, are
     fake-quantized to 8 bits (per token; per token and head for Q, K, V) and
-    the cache holds the quantized values (the backward is straight-through)."""
+    the cache holds the quantized values (the backward is straight-through).
+    a8 may be a dict of given quantized activations (see _q8): "xn1", "qr",
+    "kr", "v", "attn", "xn2", "a"."""
     B, S = cfg.batch, cfg.seq
     Hq, Hkv, hd = cfg.n_q, cfg.n_kv, cfg.head_dim
     c = {"x": x}
     xn1, r1 = rmsnorm(x)
     if a8:
-        xn1 = _aq(xn1, xn1.shape[-1])
+        xn1 = _q8(a8, "xn1", xn1, xn1.shape[-1])
     c.update(xn1=xn1, r1=r1)
     q = (xn1 @ W["Wq"].T).reshape(B, S, Hq, hd)
     k = (xn1 @ W["Wk"].T).reshape(B, S, Hkv, hd)
@@ -144,14 +158,14 @@ def attn_forward(x, W, cfg, a8=False):
     c.update(cos=cos, sin=sin, q_n=q, k_n=k)
     qr, kr = rope(q, cos, sin), rope(k, cos, sin)
     if a8:
-        qr, kr, v = _aq(qr, hd), _aq(kr, hd), _aq(v, hd)
+        qr, kr, v = _q8(a8, "qr", qr, hd), _q8(a8, "kr", kr, hd), _q8(a8, "v", v, hd)
         c["v"] = v
     c.update(qr=qr, kr=kr)
     O, P = causal_attention(qr, kr, v)
     c["P"] = P
     attn = O.reshape(B * S, Hq * hd)
     if a8:
-        attn = _aq(attn, attn.shape[-1])
+        attn = _q8(a8, "attn", attn, attn.shape[-1])
     c["attn"] = attn
     h1 = x + attn @ W["Wo"].T
     return h1, c
@@ -185,12 +199,12 @@ def attn_backward(dh1, c, W, cfg):
 def mlp_forward(h1, W, a8=False):
     xn2, r2 = rmsnorm(h1)
     if a8:
-        xn2 = _aq(xn2, xn2.shape[-1])
+        xn2 = _q8(a8, "xn2", xn2, xn2.shape[-1])
     gt = xn2 @ W["Wg"].T
     up = xn2 @ W["Wu"].T
     a = silu(gt) * up
     if a8:
-        a = _aq(a, a.shape[-1])
+        a = _q8(a8, "a", a, a.shape[-1])
     y = h1 + a @ W["Wd"].T
     return y, dict(h1=h1, xn2=xn2, r2=r2, gt=gt, up=up, a=a)
 

@@ -1,7 +1,8 @@
 """GPU parity of the W1.58A8 activation fake quantization: the standalone
 quantizer bit for bit against the oracle on the same inputs (codes decided in
 fp32 on both sides), Q/K/V quantization inside the attention preparation,
-and the a8 calibration step of a dense block against the oracle's a8 step."""
+and the a8 calibration step of a dense block against the oracle's a8 step
+fed the GPU's quantized activations."""
 import numpy as np
 import pytest
 
@@ -83,8 +84,37 @@ def test_attention_operands_quantized(catq):
                                       actquant.quantize(plain.astype(np.float64).reshape(-1, d), d)[0])
 
 
+def _saved_heads(saved, cfg):
+    """Q, K, V heads as the attention preparation saved them (quantized when
+    act_quant is on), in the oracle's [B][S][H][d] layout.  Saved layout: Q
+    heads, K heads, q/k rstd, rope cos, sin, V heads ([B][H][S][d] each,
+    regions rounded up to 256 bytes)."""
+    ru = lambda b: (b + 255) // 256 * 256
+    B, S, d = cfg.batch, cfg.seq, cfg.head_dim
+    nq, nk = B * cfg.n_q * S * d, B * cfg.n_kv * S * d
+    o_k = ru(nq * 2)
+    o_v = o_k + ru(nk * 2) + ru(B * S * (cfg.n_q + cfg.n_kv) * 4) + 2 * ru(S * (d // 2) * 4)
+    out = []
+    for off, cnt, H in ((0, nq, cfg.n_q), (o_k, nk, cfg.n_kv), (o_v, nk, cfg.n_kv)):
+        t = saved[off:off + 2 * cnt].view(torch_bf16()).float().cpu().numpy().astype(np.float64)
+        out.append(t.reshape(B, H, S, d).transpose(0, 2, 1, 3))
+    return out
+
+
+def torch_bf16():
+    import torch
+    return torch.bfloat16
+
+
 @pytest.mark.parametrize("mode,s", [(lmst.SOFT, 15.0), (lmst.HARD, 0.0)])
 def test_a8_dense_step(catq, mode, s):
+    """The a8 calibration step against the oracle's a8 step fed the GPU's own
+    quantized activations (so both sides take the same code decisions; the
+    quantizer itself is checked bit for bit above): output, loss, input
+    gradient and every factor gradient at 2e-2.  Reported: the oracle on its
+    own quantization, whose codes near a rounding boundary land one step
+    (1/127 of the group maximum) away from the GPU's because the two
+    quantize activations that differ by upstream bf16 rounding."""
     import torch
     from paper_2606_26650_amd.block import DenseBlock
     cfg = sg.small_dense(batch=2, seq=136, hidden=256, n_q=4, n_kv=2, head_dim=64, ffn=384)
@@ -104,27 +134,34 @@ def test_a8_dense_step(catq, mode, s):
     blk.target(x, y_fp)
     loss = blk.step(x, y_fp, mode=mode, s=s, s_bwd=30.0)
     torch.cuda.synchronize()
-    Wo = {k: f64(v) for k, v in W.items()}
-    ref = calib.dense_step(f64(xb), Wo, fac, cfg, mode, s=s if s else None, s_bwd=30.0, a8=True)
-    tol = 2e-2
-    assert max_norm_err(host(y_fp), ref["y_fp"]) <= tol
-    assert max_norm_err(host(blk.y), ref["y_q"]) <= tol
-    assert abs(loss.item() - ref["loss"]) <= tol * ref["loss"], (loss.item(), ref["loss"])
-    assert max_norm_err(host(blk.dx), ref["dx"]) <= tol
-    # Factor gradients: the two sides quantize activations that differ by the
-    # upstream bf16 rounding, so a code whose quotient lies within that
-    # rounding of a half-integer lands one step apart (1/127 of its group's
-    # maximum, ~15% of the codes at 2^-8 relative noise).  In G = dY^T X_q
-    # that is about 1% of extra relative noise, which the signed per-group
-    # sums of the factor gradients amplify: their bound is doubled.
-    tol_g = 2 * tol
+    qr, kr, v = _saved_heads(blk.saved, cfg)
+    given = {"xn1": host(blk.xn1), "qr": qr, "kr": kr, "v": v, "attn": host(blk.attn_q),
+             "xn2": host(blk.xn2), "a": host(blk.a)}
+    got_g = {}
     for name, L in blk.lin.items():
         parts = [DenseBlock.split_fused(cfg, name, host(a)) for a in (L.g_mu, L.g_alpha, L.g_delta)]
         for k in parts[0]:
-            for i in range(3):
-                g = np.asarray(parts[i][k]).reshape(-1)
-                err = max_norm_err(g, ref["fgrads"][k][i])
-                assert err <= tol_g, (k, i, err, median_rel(g, ref["fgrads"][k][i]))
+            got_g[k] = [np.asarray(parts[i][k]).reshape(-1) for i in range(3)]
+    Wo = {k: f64(v) for k, v in W.items()}
+    sv = s if s else None
+    tol = 2e-2
+    ref = calib.dense_step(f64(xb), Wo, fac, cfg, mode, s=sv, s_bwd=30.0, a8=given)
+    own = calib.dense_step(f64(xb), Wo, fac, cfg, mode, s=sv, s_bwd=30.0, a8=True)
+    for r in (ref, own):
+        assert max_norm_err(host(y_fp), r["y_fp"]) <= tol
+        assert max_norm_err(host(blk.y), r["y_q"]) <= tol
+        assert abs(loss.item() - r["loss"]) <= tol * r["loss"], (loss.item(), r["loss"])
+        assert max_norm_err(host(blk.dx), r["dx"]) <= tol
+    worst = worst_own = 0.0
+    for k in got_g:
+        for i in range(3):
+            err = max_norm_err(got_g[k][i], ref["fgrads"][k][i])
+            worst = max(worst, err)
+            assert err <= tol, (k, i, err, median_rel(got_g[k][i], ref["fgrads"][k][i]))
+            worst_own = max(worst_own, max_norm_err(got_g[k][i], own["fgrads"][k][i]))
+    print(f"[a8] factor-gradient error {worst:.4f} on the GPU's quantized activations, "
+          f"{worst_own:.4f} on the oracle's own", flush=True)
+    assert worst_own <= 5e-2
     # the a8 step and its two-stream schedule agree bit for bit
     a = blk.step(x, y_fp, mode=mode, s=s, s_bwd=30.0, overlap=False).clone()
     g1 = [L.g_delta.clone() for L in blk.lin.values()]

@@ -7,7 +7,7 @@ import pytest
 
 import synthgen as sg
 from helpers import f64, host, max_norm_err, median_rel, to_dev_bf16
-from oracle import calib, lmst, window
+from oracle import block, calib, lmst, window
 
 pytestmark = pytest.mark.gpu
 
@@ -65,21 +65,35 @@ def test_window_step_parity(catq, mode, s):
     assert abs(loss.item() - ref["loss"]) <= tol * ref["loss"], (loss.item(), ref["loss"])
     assert max_norm_err(host(win.dx), ref["dx"]) <= tol
     assert max_norm_err(host(blks[1].dx), _inner_dy(ref, cfg)) <= tol
-    # The factor gradients of block b come through the backward of the
-    # n - b blocks from the loss down to it, each adding the bf16 rounding of
-    # its activations and gradients: the one-block bound scales with that
-    # depth.
+    # Factor gradients.  The last block is gated end to end.  An earlier
+    # block b is gated on its own backward given the gradient that reaches
+    # its output (the GPU's input gradient of block b + 1): end to end its
+    # factor gradients sit on a floor set by the bf16 forward of both
+    # windows (the loss gradient is a small difference of two bf16
+    # pipelines that passed through n - b blocks).  An exact float64
+    # emulation of every bf16 rounding the GPU performs gives 0.017 on block
+    # 0 of this case, independent of the token count, so that figure is
+    # reported, with a loose tripwire only.
     n = len(blks)
+    xs = [ref["inputs"][0]] + [ref["inputs"][b] for b in range(1, n)]
     for b, blk in enumerate(blks):
-        worst = 0.0
+        if b == n - 1:
+            gate = ref["fgrads"][b]
+        else:
+            _, cache = block.block_forward(xs[b], ref["W_fake"][b], cfg)
+            _, dW = block.block_backward(host(blks[b + 1].dx), cache, ref["W_fake"][b], cfg)
+            gate = calib.factor_grads_all(dW, Wos[b], facs[b], 128, mode, s if s else None, 30.0)
+        worst = worst_e2e = 0.0
         for name, L in blk.lin.items():
             for k, v in _split(cfg, name, (L.g_mu, L.g_alpha, L.g_delta)).items():
                 for i in range(3):
-                    r = ref["fgrads"][b][k][i]
-                    err = max_norm_err(v[i], r)
+                    err = max_norm_err(v[i], gate[k][i])
                     worst = max(worst, err)
-                    assert err <= tol * (n - b), (b, k, i, err, median_rel(v[i], r))
-        print(f"[window] block {b}: worst factor-gradient error {worst:.4f}", flush=True)
+                    assert err <= tol, (b, k, i, err, median_rel(v[i], gate[k][i]))
+                    worst_e2e = max(worst_e2e, max_norm_err(v[i], ref["fgrads"][b][k][i]))
+        print(f"[window] block {b}: worst factor-gradient error {worst:.4f} (gated), "
+              f"{worst_e2e:.4f} end to end", flush=True)
+        assert worst_e2e <= 5e-2
 
 
 def _inner_dy(ref, cfg):
@@ -123,8 +137,10 @@ N_SAMPLES, N_EPOCHS = 4, 3
 def test_sliding_calibration_against_oracle(catq):
     """Window-by-window calibration of three blocks (l = 2, stride 1).  Gated
     per optimiser step on the GPU's own state: the oracle's window step on
-    the factors the GPU held (loss, every block's factor gradients) and the
-    oracle's AdamW on the same factors, gradients and moments; the final
+    the factors the GPU held (loss; the last block's factor gradients end to
+    end, the earlier block's from its own backward of the gradient reaching
+    its output) and the oracle's AdamW on the same factors, gradients and
+    moments; the final
     codes against the oracle's hard decision on the GPU's final factors, bit
     for bit.  Reported: the oracle's own trajectory."""
     import torch
@@ -143,6 +159,8 @@ def test_sliding_calibration_against_oracle(catq):
     def obs(phase, c, b, mode, s, lr):
         rec.span = cal.span
         rec(phase, c, b, mode, s, lr)
+        if phase == "grads":   # gradients reaching the outputs of the earlier blocks
+            rec.steps[-1]["dy_in"] = [host(blk.dx) for blk in c.blk.blocks[1:]]
 
     cal.observer = obs
     bufs = cal.run()
@@ -155,7 +173,7 @@ def test_sliding_calibration_against_oracle(catq):
         acts.append(np.concatenate([block.block_forward(acts[i][b * tpb:(b + 1) * tpb], Wos[i],
                                                         cfg)[0] for b in range(nb)]))
     assert len(rec.steps) == 2 * N_EPOCHS * nb
-    worst = {}
+    worst, worst_e2e = {}, {}
     for r in rec.steps:
         bef, (a, e) = r["before"], r["span"]
         xw = acts[a][bef["batch"] * tpb:(bef["batch"] + 1) * tpb]
@@ -166,13 +184,23 @@ def test_sliding_calibration_against_oracle(catq):
         assert abs(bef["loss"] - ref["loss"]) <= 2e-2 * ref["loss"], ((a, e), bef["step"])
         for j in range(e - a):
             grads = per_linear(blks[a + j], DenseBlock.split_fused, cfg, bef["g"][3 * j:3 * j + 3])
+            if j == e - a - 1:
+                gate = ref["fgrads"][j]
+            else:   # an earlier block: its own backward from the gradient at its output
+                _, cache = block.block_forward(ref["inputs"][j], ref["W_fake"][j], cfg)
+                _, dW = block.block_backward(r["dy_in"][j], cache, ref["W_fake"][j], cfg)
+                gate = calib.factor_grads_all(dW, Wos[a + j], facs[j], 128, bef["mode"], s, 30.0)
             for k in grads:
                 for i in range(3):
-                    err = max_norm_err(grads[k][i], ref["fgrads"][j][k][i])
+                    err = max_norm_err(grads[k][i], gate[k][i])
                     worst[j] = max(worst.get(j, 0.0), err)
                     assert err <= 2e-2, ((a, e), bef["step"], j, k, i, err)
+                    e2e = max_norm_err(grads[k][i], ref["fgrads"][j][k][i])
+                    worst_e2e[j] = max(worst_e2e.get(j, 0.0), e2e)
         check_adamw(r)
-    print(f"[sliding] worst factor-gradient error per window position {worst}", flush=True)
+    print(f"[sliding] worst factor-gradient error per window position {worst} (gated), "
+          f"{worst_e2e} end to end", flush=True)
+    assert max(worst_e2e.values()) <= 5e-2
     for i, blk in enumerate(blks):
         for name, L in blk.lin.items():
             gf = _split(cfg, name, (L.d_mu, L.d_alpha, L.d_delta))

@@ -139,3 +139,29 @@ def test_a8_step_is_close_to_the_w16_step():
     d = np.abs(a["y_q"] - b["y_q"]).max() / np.abs(b["y_q"] - x).max()
     assert 0 < d < 0.05
     assert 0 < abs(a["loss"] - b["loss"]) < 0.2 * b["loss"]
+
+
+def test_given_quantized_activations_reproduce_the_a8_step():
+    """The a8 path fed its own quantized activations as a dict (the form a
+    comparison uses to take another computation's code decisions) gives the
+    a8 step bit for bit: every quantization point is wired to its name."""
+    from oracle import block, calib, lmst
+    cfg = sg.small_dense(batch=2, seq=24, hidden=128, n_q=4, n_kv=2, head_dim=64, ffn=256)
+    W = {k: sg.bf16_bits_to_f32(v).astype(np.float64) for k, v in sg.block_weights(cfg, 0).items()}
+    x = sg.bf16_bits_to_f32(sg.activations(cfg, 0)).astype(np.float64)
+    fac = {k: list(sg.perturbed_factors(3, v.size // 128)) for k, v in W.items()}
+    ref = calib.dense_step(x, W, fac, cfg, lmst.SOFT, s=15.0, s_bwd=30.0, a8=True)
+    Wf = calib.fake_weights(W, fac, 128, lmst.SOFT, 15.0)
+    _, (ca, cm) = block.block_forward(x, Wf, cfg, True)
+    given = {"xn1": ca["xn1"], "qr": ca["qr"], "kr": ca["kr"], "v": ca["v"], "attn": ca["attn"],
+             "xn2": cm["xn2"], "a": cm["a"]}
+    got = calib.dense_step(x, W, fac, cfg, lmst.SOFT, s=15.0, s_bwd=30.0, a8=given)
+    assert got["loss"] == ref["loss"]
+    np.testing.assert_array_equal(got["dx"], ref["dx"])
+    for k in W:
+        for i in range(3):
+            np.testing.assert_array_equal(got["fgrads"][k][i], ref["fgrads"][k][i])
+    # a different given activation changes the step (the values are used)
+    given["a"] = given["a"] * 1.01
+    assert calib.dense_step(x, W, fac, cfg, lmst.SOFT, s=15.0, s_bwd=30.0,
+                            a8=given)["loss"] != ref["loss"]
