@@ -1,29 +1,33 @@
-"""Throughput of the CAT-Q calibration step on one MI355X.
+"""Throughput of CAT-Q calibration on one MI355X.
 
-Workload: one decoder block shaped like Qwen3-1.7B (hidden 2048, 16 q / 8 kv
-heads of 128, SwiGLU 6144, QK-norm, RoPE) on 4 synthetic calibration samples
-of 2048 tokens (Student-t(4) activations, N(0, 0.02^2) bf16 weights, seed 0).
+Workload (default): one decoder block shaped like Qwen3-14B (hidden 5120, 40 q
+/ 8 kv heads of 128, SwiGLU 17408, QK-norm, RoPE; 330.3M weights) on 2
+synthetic calibration samples of 4096 tokens (Student-t(4) activations,
+N(0, 0.015^2) bf16 weights, seed 0), calibrated for K steps and then
+ternarised and packed.
 
-One step = every part of the hot path on one batch:
-  group statistics + learnable modulation + softened ternarisation of all
-  seven weights (s = 15, SOFT), block forward with the fake-ternary weights,
-  reconstruction loss against the cached full-precision output, backward to
-  the input and to every group's three factors, then hard ternarisation and
-  2-bit packing of all weights.
-The full-precision target is computed once before timing (it does not change
-during calibration).  Inputs are resident in HBM when the timed region starts.  The step runs on
-two streams: each linear's weight-gradient half (G = dY^T X and the factor
-gradients) and the hard finalize go to a side stream and overlap the
-input-gradient chain (--no-overlap: one stream).
+The timed region is one calibration of the block as the library's
+BlockCalibrator runs it: K steps on the Eq. 6 schedule (step k at t = k/K:
+softened ternarisation with s = (t/0.8)*30 while t <= 0.8, the hard quantiser
+with the backward at s0 = 30 after), each step being LM+ST of all seven
+weights, block forward with the fake-ternary weights, reconstruction loss
+against the cached full-precision output, backward to the input and to every
+group's three factors, and one AdamW update of the factors; the group
+statistics are computed at the first step (the weights are frozen) and the
+final hard ternarisation with 2-bit packing of every weight runs once after
+the last step.  K = 10 is the 10-step calibration of the workload.  The
+full-precision target is computed before timing (it does not change during
+calibration); inputs are resident in HBM when the timed region starts.  The
+step runs on two streams: each linear's weight-gradient half (G = dY^T X and
+the factor gradients) goes to a side stream and overlaps the input-gradient
+chain (--no-overlap: one stream).
 
-Prints one JSON line.  ``value`` and ``ms_per_step`` come from the timed pass
-(the production schedule: two streams, no per-launch instrumentation; --graph
-replays the step captured as a HIP graph instead).  A
-kernel pass then repeats the same steps on one stream with a HIP event pair
-recorded by the library around each of its launches, on the launch stream:
-the per-kernel durations behind ``roofline`` come from there, so a kernel's
-time is not shared with concurrent work.  The CPU baseline times the float64
-oracle on a bounded sample.
+Prints one JSON line.  ``value`` = K / (timed seconds), in block-steps/s.  A
+kernel pass then repeats the same calibration on one stream with a HIP event
+pair recorded by the library around each of its launches, on the launch
+stream: the per-kernel durations behind ``roofline`` come from there, so a
+kernel's time is not shared with concurrent work.  The CPU baseline times the
+float64 oracle on a bounded sample of the same step.
 """
 from __future__ import annotations
 
@@ -44,8 +48,10 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E peak
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=10,
+                    help="calibration steps in the timed region (the schedule runs over them)")
+    ap.add_argument("--warmup", type=int, default=2,
+                    help="untimed soft steps before the timed calibration")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-gib", type=float, default=0.0,
                     help="only run a plain device copy of this size (counter calibration)")
@@ -53,31 +59,38 @@ def parse():
     ap.add_argument("--no-overlap", action="store_true",
                     help="run the step on one stream (no side stream for the weight-gradient "
                          "halves and the finalize)")
-    ap.add_argument("--graph", action="store_true",
-                    help="replay the step captured as a HIP graph in the timed pass (measured "
-                         "slower than issuing the launches on this step: it is not launch-bound)")
     ap.add_argument("--ternary", type=int, default=0, metavar="M",
                     help="only time the packed-ternary decode layers of a Qwen3-14B-shaped "
                          "block at M tokens (deployment on the 2-bit storage)")
     ap.add_argument("--a8", action="store_true",
                     help="the W1.58A8 setting: activations fake-quantized to 8 bits in the step")
-    ap.add_argument("--block", default="qwen3-1.7b",
+    ap.add_argument("--block", default="qwen3-14b",
                     choices=["qwen3-1.7b", "llama3-8b", "qwen3-14b", "qwen3-235b-moe",
                              "qwen3-235b-moe-skew"],
-                    help="block shape of the step (the default is the headline workload; the "
-                         "others are reported without a CPU baseline)")
+                    help="block shape of the step (the default is the headline workload)")
     ap.add_argument("--window", type=int, default=1,
                     help="calibrate this many consecutive blocks jointly (sliding-window "
                          "reconstruction; 1 = the single-block step)")
     return ap.parse_args()
 
 
-def counted_traffic(kernel_tag):
-    """HBM bytes per launch of `kernel_tag` as last counted with rocprofv3
-    (FETCH_SIZE and WRITE_SIZE runs, scaled by a plain copy's reading; the
-    summary under profiles/ records the figure with a hash of the kernel
-    sources).  None when no summary covers this kernel or when the sources
-    changed since the count."""
+def workload_key(args, cfg):
+    """Short name of the measured workload: block shape, batch x tokens,
+    window and activation settings (keys the counted-traffic summaries)."""
+    key = f"{args.block}/{cfg.batch}x{cfg.seq}"
+    if args.window > 1:
+        key += f"/window{args.window}"
+    if args.a8:
+        key += "/a8"
+    return key
+
+
+def counted_traffic(kernel_tag, workload):
+    """HBM bytes per launch of `kernel_tag` on `workload` as last counted
+    with rocprofv3 (FETCH_SIZE and WRITE_SIZE runs, scaled by a plain copy's
+    reading; the summary under profiles/ records the figure with the
+    workload and a hash of the kernel sources).  None when no summary covers
+    this kernel on this workload or when the sources changed since."""
     import glob
     import hashlib
     for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "traffic_*.md"))):
@@ -86,7 +99,8 @@ def counted_traffic(kernel_tag):
             if ":" in line and not line.startswith(("|", "#", " ")):
                 k, _, v = line.partition(":")
                 fields[k.strip()] = v.strip()
-        if fields.get("kernel") != kernel_tag or "traffic_bytes_per_launch" not in fields:
+        if (fields.get("kernel") != kernel_tag or fields.get("workload") != workload
+                or "traffic_bytes_per_launch" not in fields):
             continue
         h = hashlib.sha256()
         try:
@@ -110,12 +124,14 @@ def workload_config(args, cfg):
     name = shape[args.block] + "-shaped decoder block"
     if args.window > 1:
         name = f"window of {args.window} {name}s"
-    name += (f", {cfg.batch} x {cfg.seq} tokens, one CAT-Q calibration step (LM+ST s=15, fwd, "
-             "loss, bwd to factors, ternarise+pack)")
+    name += (f", {cfg.batch} x {cfg.seq} tokens, CAT-Q calibration of {args.steps} steps "
+             "(Eq. 6 schedule: LM+ST, fwd, loss, bwd to factors, AdamW; statistics at the first "
+             "step) then hard ternarise + 2-bit pack")
     if args.a8:
         name += ", W1.58A8 (8-bit activations)"
-    conf = {"workload": name, "hidden": cfg.hidden, "heads": [cfg.n_q, cfg.n_kv, cfg.head_dim],
-            "tokens": cfg.tokens, "group_size": 128}
+    conf = {"workload": name, "key": workload_key(args, cfg), "hidden": cfg.hidden,
+            "heads": [cfg.n_q, cfg.n_kv, cfg.head_dim], "tokens": cfg.tokens, "group_size": 128,
+            "calibration_steps": args.steps}
     if moe:
         n_w = sum(a * b for a, b in cfg.attn_shapes().values())
         n_w += sum(e * a * b for e, a, b in cfg.expert_shapes().values())
@@ -314,6 +330,8 @@ def main():
     moe = hasattr(cfg, "n_experts")
     if (moe or args.block != "qwen3-1.7b") and (args.window > 1 or args.a8):
         sys.exit("--window and --a8 run on the qwen3-1.7b-shaped dense block only")
+    if args.steps < 1:
+        sys.exit("--steps must be >= 1")
     W = sg.block_weights(cfg, 0)
     xb = sg.activations(cfg, 0)
     if moe:
@@ -326,54 +344,47 @@ def main():
                       for i in range(1, args.window)])
     else:
         blk = DenseBlock(cfg, W, a8=args.a8)
-    del W
+    from paper_2606_26650_amd.calibrate import BlockCalibrator
     x = bf16_tensor(xb)
-    y_fp = blk.new_output()
-    blk.target(x, y_fp)
+    # the full-precision target is computed here, once (not timed)
+    cal = BlockCalibrator(blk, x, args.steps, overlap=not args.no_overlap)
     # the final ternarisation writes the 2-bit storage directly (no int8 codes)
     fin = blk.finalize_buffers(codes=False)
 
-    def step(overlap):
-        blk.step(x, y_fp, mode=cq.SOFT, s=15.0, s_bwd=30.0, recompute_stats=True,
-                 overlap=overlap, finalize=fin)
+    def calibrate():
+        """One calibration: K steps (statistics at the first), AdamW after
+        each, then the hard ternarisation + packing of every weight."""
+        cal.reset()
+        cal.run()
+        blk.finalize(fin)
 
-    # timed pass: the production schedule (two streams; optionally the step
-    # replayed as a HIP graph), no per-launch instrumentation
-    run = lambda: step(not args.no_overlap)
-    if args.graph:
-        from paper_2606_26650_amd.block import StepGraph
-        graph = StepGraph(blk, x, y_fp, mode=cq.SOFT, s=15.0, s_bwd=30.0, recompute_stats=True,
-                          overlap=not args.no_overlap, finalize=fin)
-        run = graph.replay
     for _ in range(args.warmup):
-        run()
+        blk.step(x, cal.targets[0], mode=cq.SOFT, s=15.0, s_bwd=30.0,
+                 overlap=not args.no_overlap)
     torch.cuda.synchronize()
+    # timed pass: the production schedule, no per-launch instrumentation
     t0 = time.perf_counter()
-    for _ in range(args.steps):
-        run()
+    calibrate()
     torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    elapsed = t1 - t0
+    elapsed = time.perf_counter() - t0
     ms_step = 1000.0 * elapsed / args.steps
-    loss = float(blk.loss.item())
+    losses = cal.loss_history()
 
-    # kernel pass: the same steps on one stream with a HIP event pair around
-    # every library launch (on its launch stream), so each kernel's duration
-    # is its own and not shared with concurrent work
-    step(False)
-    torch.cuda.synchronize()
-    cq.catq_trace_enable(64 * max(args.steps, 1) + 64)
+    # kernel pass: the same calibration on one stream with a HIP event pair
+    # around every library launch (on its launch stream), so each kernel's
+    # duration is its own and not shared with concurrent work
+    cal.overlap = False
+    cq.catq_trace_enable(96 * args.steps + 256)
     torch.cuda.synchronize()
     k0 = time.perf_counter()
-    for _ in range(args.steps):
-        step(False)
+    calibrate()
     torch.cuda.synchronize()
     k1 = time.perf_counter()
     recs = cq.trace_records()
     cq.catq_trace_disable()
     kernel_pass_ms = 1000.0 * (k1 - k0) / args.steps
 
-    # per-kernel aggregation over the timed steps
+    # per-kernel aggregation over the calibration
     agg = {}
     for r in recs:
         a = agg.setdefault(r["tag"], {"n": 0, "ms": 0.0, "flops": 0.0, "bytes": 0.0})
@@ -382,17 +393,24 @@ def main():
         a["flops"] += r["flops"]
         a["bytes"] += r["bytes"]
     gemm = {k: v for k, v in agg.items() if k.startswith("gemm") and v["flops"] > 0}
-    # dominant kernel: the GEMM variant with the largest share of step time
+    # dominant kernel: the GEMM variant with the largest share of the time
     dom_tag, dom = max(gemm.items(), key=lambda kv: kv[1]["ms"])
     dom_tflops = dom["flops"] / (dom["ms"] * 1e-3) / 1e12
     all_gemm_ms = sum(v["ms"] for v in gemm.values())
     all_gemm_flops = sum(v["flops"] for v in gemm.values())
-    lm_fwd = {k: v for k, v in agg.items() if k.startswith("lmst_fwd_kernel")}
-    lmf_ms = sum(v["ms"] for v in lm_fwd.values())
-    lmf_bytes = sum(v["bytes"] for v in lm_fwd.values())
-    lmb = agg.get("lmst_bwd_kernel<__bf16>", {"ms": 0.0, "bytes": 0.0})
-    step_gemm_flops = all_gemm_flops / args.steps
 
+    def hbm(prefix):
+        """Algorithmic GB/s of the elementwise launches whose tag starts with
+        `prefix` (their bytes / their summed durations), with launch count."""
+        sel = {k: v for k, v in agg.items() if k.startswith(prefix)}
+        ms = sum(v["ms"] for v in sel.values())
+        if not ms:
+            return None
+        gbs = sum(v["bytes"] for v in sel.values()) / (ms * 1e-3) / 1e9
+        return {"GB/s": gbs, "frac": gbs / PEAK_HBM_GBS, "launches": sum(v["n"] for v in sel.values()),
+                "us_per_launch": 1000.0 * ms / sum(v["n"] for v in sel.values())}
+
+    key = workload_key(args, cfg)
     out = {
         "metric": METRIC,
         "value": args.steps / elapsed,
@@ -415,23 +433,27 @@ def main():
             "unit": "TFLOP/s",
             "frac": dom_tflops / PEAK_BF16_TFLOPS,
             "avg_launch_us": 1000.0 * dom["ms"] / dom["n"],
+            "launches": dom["n"],
             "flops_per_launch": dom["flops"] / dom["n"],
-            "traffic": counted_traffic(dom_tag),
+            "traffic": counted_traffic(dom_tag, key),
         },
         "schedule": ("two streams" if not args.no_overlap else "one stream") +
-                    (", step replayed as a HIP graph" if args.graph else ", launches issued per step"),
+                    ", launches issued per step",
         "kernel_pass": {"ms_per_step": kernel_pass_ms, "streams": 1, "steps": args.steps,
                         "instrumented": "HIP event pair per launch"},
         "gemm_tflops_all": all_gemm_flops / (all_gemm_ms * 1e-3) / 1e12,
+        "gemm_frac_all": all_gemm_flops / (all_gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
         "gemm_share_of_step": all_gemm_ms / args.steps / kernel_pass_ms,
-        "step_gemm_tflop": step_gemm_flops / 1e12,
-        "lmst_fwd_gbs": lmf_bytes / (lmf_ms * 1e-3) / 1e9 if lmf_ms else None,
-        "lmst_fwd_frac_hbm": (lmf_bytes / (lmf_ms * 1e-3) / 1e9) / PEAK_HBM_GBS if lmf_ms else None,
-        "lmst_bwd_gbs": lmb["bytes"] / (lmb["ms"] * 1e-3) / 1e9 if lmb["ms"] else None,
-        "loss": loss,
+        "step_gemm_tflop": all_gemm_flops / args.steps / 1e12,
+        "lmst_fwd": hbm("lmst_fwd_kernel"),
+        "lmst_bwd": hbm("lmst_bwd_kernel"),
+        "loss_first_last": [float(losses[0]), float(losses[-1])],
     }
-    if not args.no_cpu_baseline and args.window == 1 and not args.a8 and args.block == "qwen3-1.7b":
-        out["cpu_baseline"] = cpu_baseline(cfg, sg.block_weights(cfg, 0), xb)
+    if not args.no_cpu_baseline and args.window == 1 and not args.a8 and not moe:
+        # a bounded sample: about 10-30 s of host work on the GPU machine
+        row_frac, n_samples = {"qwen3-1.7b": (1, None), "llama3-8b": (8, 1),
+                               "qwen3-14b": (8, 1)}[args.block]
+        out["cpu_baseline"] = cpu_baseline(cfg, W, xb, row_frac, n_samples)
     if args.breakdown:
         shp = {}
         for r in recs:
@@ -441,12 +463,12 @@ def main():
                 a[1] += r["ms"]
                 a[2] += r["flops"]
         for (t, m, n, k), (c, ms, fl) in sorted(shp.items(), key=lambda kv: -kv[1][1]):
-            print(f"{ms / args.steps:9.3f} ms/step {c // args.steps:3d}x {fl / (ms * 1e-3) / 1e12:8.1f} TF/s"
-                  f"  M={m} N={n} K={k}  {t}", file=sys.stderr)
+            print(f"{ms / args.steps:9.3f} ms/step {c / args.steps:5.1f}x "
+                  f"{fl / (ms * 1e-3) / 1e12:8.1f} TF/s  M={m} N={n} K={k}  {t}", file=sys.stderr)
         for k, v in sorted(agg.items(), key=lambda kv: -kv[1]["ms"]):
             tf = v["flops"] / (v["ms"] * 1e-3) / 1e12 if v["flops"] else 0
             gb = v["bytes"] / (v["ms"] * 1e-3) / 1e9
-            print(f"{v['ms'] / args.steps:9.3f} ms/step {v['n'] // args.steps:3d}x "
+            print(f"{v['ms'] / args.steps:9.3f} ms/step {v['n'] / args.steps:5.1f}x "
                   f"{tf:8.1f} TF/s {gb:8.1f} GB/s  {k}", file=sys.stderr)
     print(json.dumps(out))
 

@@ -54,8 +54,9 @@ class BlockCalibrator:
     are computed once (identity branch) and kept on the device."""
 
     def __init__(self, block, x_all: torch.Tensor, n_epochs: int, gamma: float = 0.8,
-                 s0: float = 30.0, lr0: float = 1e-3):
+                 s0: float = 30.0, lr0: float = 1e-3, overlap: bool = True):
         self.blk = block
+        self.overlap = overlap    # the step's side stream (see the block drivers)
         cfg = block.cfg
         self.tok_per_batch = cfg.batch * cfg.seq
         if x_all.shape[0] % self.tok_per_batch:
@@ -89,7 +90,7 @@ class BlockCalibrator:
         mode, s = time_state(self.epoch, self.n_epochs, self.gamma, self.s0)
         for b in range(self.n_batches):
             loss = self.blk.step(self.batch(b), self.targets[b], mode=mode, s=s, s_bwd=self.s0,
-                                 recompute_stats=self.step_no == 0)
+                                 recompute_stats=self.step_no == 0, overlap=self.overlap)
             self.losses.append(loss.clone())
             self.step_no += 1
             lr = linear_lr(self.step_no - 1, self.total_steps, self.lr0)
@@ -100,6 +101,19 @@ class BlockCalibrator:
             if self.observer is not None:
                 self.observer("update", self, b, mode, s, lr)
         self.epoch += 1
+
+    def reset(self):
+        """Back to the start of the schedule: identity factors (Sec. 2.2 at
+        delta_mu = 0, delta_alpha = delta_Delta = 1), zero moments, no steps
+        taken; the cached targets are kept."""
+        for i in range(0, len(self.params), 3):
+            self.params[i].zero_()
+            self.params[i + 1].fill_(1.0)
+            self.params[i + 2].fill_(1.0)
+        for t in self.m + self.v:
+            t.zero_()
+        self.step_no = self.epoch = 0
+        self.losses = []
 
     def run(self, checkpoint_dir: str | None = None):
         while self.epoch < self.n_epochs:
