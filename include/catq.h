@@ -149,7 +149,11 @@ catq_status catq_fakeq_linear_fwd(const void* X, const void* W_fake, catq_dtype 
 
 /*
  * catq_fakeq_linear_bwd -- backward of the fake-ternary linear layer to its
- * input and to the learnable factors of its weight.
+ * input and to the learnable factors of its weight: the gradient of the
+ * reconstruction loss of Eq. 7 (Sec. 2.4) taken through the softened
+ * ternarisation of Eq. 5-6 (Sec. 2.3; in the hard branch, the derivatives of
+ * the last soft sharpness stand in for the step) and the modulation of
+ * Eq. 3-4 (Sec. 2.2).  Only the three factors are learned; W is frozen.
  *
  *   dX[M][K]      = dY[M][N] . W_fake[N][K]            (NULL: not computed)
  *   G[N][K]       = dY^T . X  (= dL/dW_fake, fp32)     (into dW_fake if given,
