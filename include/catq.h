@@ -211,6 +211,24 @@ catq_status catq_block_recon_loss(const void* Y_q, const void* Y_fp, catq_dtype 
                                   size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * catq_block_recon_loss_noalloc -- catq_block_recon_loss without a workspace
+ * argument and without any allocation, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Same kernels, same arguments otherwise, same bits.
+ * Its partial sums live in a library-owned file-scope device array of 1024
+ * doubles (8 KiB; each GPU the library runs on holds one copy until the
+ * process ends); every n accepted by catq_block_recon_loss needs at most 1024
+ * partials, and each partial is written before it is read, so nothing has to
+ * be cleared between calls.  Calls that overlap on one GPU (two streams, or
+ * two host threads) share that array and race: issue them in order.
+ * Errors as catq_block_recon_loss (no CATQ_ERR_WORKSPACE); CATQ_ERR_HIP if
+ * the array's device address cannot be obtained.
+ */
+catq_status catq_block_recon_loss_noalloc(const void* Y_q, const void* Y_fp, catq_dtype dtype,
+                                          int64_t n, float* loss, void* dY_q, catq_dtype dy_dtype,
+                                          hipStream_t stream);
+
+/*
  * catq_pack_ternary -- 2-bit storage of ternary codes for deployment
  * (App. B.2: T in {-1,0,+1} plus the group scale alpha, zero-point free).
  * Code c = T + 1 in {0,1,2}; byte b of row r holds elements 4b..4b+3 of that

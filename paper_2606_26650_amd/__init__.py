@@ -14,7 +14,7 @@ from ._lib import (BF16, F32, HARD, IDENTITY, SOFT, WS_LINEAR_BWD, WS_LOSS, Attn
 
 __all__ = [
     "catq_modulate_ternarize", "catq_fakeq_linear_fwd", "catq_fakeq_linear_bwd",
-    "catq_block_recon_loss", "catq_pack_ternary", "catq_ternarize_pack",
+    "catq_block_recon_loss", "catq_block_recon_loss_noalloc", "catq_pack_ternary", "catq_ternarize_pack",
     "catq_fakeq_gateup_swiglu_fwd",
     "catq_fakeq_down_swiglu_bwd", "catq_ternary_linear", "catq_workspace_size",
     "catq_aux_act_quant", "catq_aux_rmsnorm_fwd", "catq_aux_rmsnorm_bwd", "catq_aux_attention_fwd",
@@ -116,6 +116,15 @@ def catq_block_recon_loss(Y_q, Y_fp, loss, dY_q, workspace, stream=None):
     st = lib.catq_block_recon_loss(_ptr(Y_q), _ptr(Y_fp), _dt(Y_q), Y_q.numel(), _ptr(loss),
                                    _ptr(dY_q), dy_dt, _ptr(workspace), ws_bytes, _stream(stream))
     _lib.check("catq_block_recon_loss", st)
+
+
+def catq_block_recon_loss_noalloc(Y_q, Y_fp, loss, dY_q, stream=None):
+    """catq_block_recon_loss with the library's own scratch (no workspace,
+    no allocation); calls that overlap on one GPU race on that scratch."""
+    dy_dt = _dt(dY_q) if dY_q is not None else BF16
+    st = lib.catq_block_recon_loss_noalloc(_ptr(Y_q), _ptr(Y_fp), _dt(Y_q), Y_q.numel(),
+                                           _ptr(loss), _ptr(dY_q), dy_dt, _stream(stream))
+    _lib.check("catq_block_recon_loss_noalloc", st)
 
 
 def catq_ternarize_pack(W, d_mu, d_alpha, d_delta, params, stats, stats_mode, packed,

@@ -51,6 +51,7 @@ SIGNATURES = {
     "catq_fakeq_linear_bwd": [P, P, P, I32, I64, I64, I64, I32, P, P, I32, P, P, P, P, PP, P, P,
                               P, P, P, P, SZ, P],
     "catq_block_recon_loss": [P, P, I32, I64, P, P, I32, P, SZ, P],
+    "catq_block_recon_loss_noalloc": [P, P, I32, I64, P, P, I32, P],
     "catq_pack_ternary": [P, I64, I64, P, P],
     "catq_ternarize_pack": [P, I32, I64, I64, P, P, P, PP, P, I32, P, P, P],
     "catq_fakeq_gateup_swiglu_fwd": [P, P, I64, I64, I64, P, P, P],

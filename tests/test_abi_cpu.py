@@ -143,6 +143,12 @@ def test_linear_and_loss_validation(cq):
     assert L.catq_block_recon_loss(FAKE, FAKE, 1, 16, FAKE, None, 1, FAKE, 8, None) == 6
     assert L.catq_block_recon_loss(FAKE, None, 1, 16, FAKE, None, 1, FAKE, 1 << 20, None) == 1
     assert L.catq_block_recon_loss(FAKE, FAKE, 0, 16, FAKE, FAKE, 4, FAKE, 1 << 20, None) == 3
+    nl = L.catq_block_recon_loss_noalloc                       # rejected before any HIP call
+    assert nl(FAKE, FAKE, 1, 12, FAKE, None, 1, None) == 2
+    assert nl(FAKE, None, 1, 16, FAKE, None, 1, None) == 1
+    assert nl(FAKE, FAKE, 0, 16, FAKE, FAKE, 4, None) == 3
+    assert nl(FAKE, FAKE, 7, 16, FAKE, FAKE, 1, None) == 3
+    assert nl(FAKE + 2, FAKE, 1, 16, FAKE, None, 1, None) == 5
     assert L.catq_pack_ternary(FAKE, 4, 6, FAKE, None) == 2
     assert L.catq_pack_ternary(None, 4, 8, FAKE, None) == 1
 
