@@ -58,10 +58,21 @@ typedef enum {
   CATQ_ERR_VALUE = 4,      /* a scalar parameter is out of range               */
   CATQ_ERR_ALIGN = 5,      /* a pointer is not 16-byte aligned                 */
   CATQ_ERR_WORKSPACE = 6,  /* workspace missing or smaller than required       */
-  CATQ_ERR_HIP = 7         /* a HIP launch or runtime call failed              */
+  CATQ_ERR_HIP = 7,        /* a HIP launch or runtime call failed              */
+  /* never returned: they make every int32 value a valid catq_status, so a
+     caller's out-of-range value is checked, not undefined (C++) */
+  CATQ_STATUS_RANGE_MIN_ = INT32_MIN,
+  CATQ_STATUS_RANGE_MAX_ = INT32_MAX
 } catq_status;
 
-typedef enum { CATQ_F32 = 0, CATQ_BF16 = 1 } catq_dtype;
+typedef enum {
+  CATQ_F32 = 0,
+  CATQ_BF16 = 1,
+  /* not dtypes: every int32 value is a valid catq_dtype, and the calls reject
+     all but the two above with CATQ_ERR_DTYPE */
+  CATQ_DTYPE_RANGE_MIN_ = INT32_MIN,
+  CATQ_DTYPE_RANGE_MAX_ = INT32_MAX
+} catq_dtype;
 
 /* Branch of the softened-ternarisation schedule, Eq. 6. */
 typedef enum {

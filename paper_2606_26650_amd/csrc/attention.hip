@@ -101,6 +101,10 @@ static catq_status check_desc(const catq_attn_desc* a) {
   CATQ_REQUIRE(a->batch > 0 && a->seq > 0 && a->n_q > 0 && a->n_kv > 0, CATQ_ERR_SHAPE,
                "batch, seq and head counts must be > 0");
   CATQ_REQUIRE(a->n_q % a->n_kv == 0, CATQ_ERR_SHAPE, "n_q must be a multiple of n_kv");
+  CATQ_REQUIRE(count_ok((int64_t)a->batch * a->seq, (int64_t)a->n_q + 2 * (int64_t)a->n_kv,
+                        a->head_dim > 0 ? a->head_dim : 1) &&
+                   count_ok((int64_t)a->batch * a->n_q, a->seq, a->seq),
+               CATQ_ERR_SHAPE, "batch, seq and heads too large (more than 2^38 elements)");
   CATQ_REQUIRE(a->head_dim == 64 || a->head_dim == 128 || a->head_dim == 256, CATQ_ERR_SHAPE,
                "head_dim must be 64, 128 or 256");
   CATQ_REQUIRE(a->seq % 8 == 0 && a->seq <= 8192, CATQ_ERR_SHAPE,

@@ -43,6 +43,19 @@ inline bool dtype_ok(int d) { return d == CATQ_F32 || d == CATQ_BF16; }
 inline size_t dtype_size(int d) { return d == CATQ_F32 ? 4 : 2; }
 inline size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+// Element counts the library accepts: products of positive sizes that stay at
+// or below 2^38 (more elements than any MI355X buffer holds), so the byte
+// sizes, offsets and grid sizes derived from them cannot overflow.
+constexpr int64_t MAX_ELEMS = int64_t(1) << 38;
+inline bool count_ok(int64_t a, int64_t b = 1, int64_t c = 1, int64_t d = 1) {
+  if (a <= 0 || b <= 0 || c <= 0 || d <= 0) return false;
+  int64_t p;
+  if (__builtin_mul_overflow(a, b, &p) || __builtin_mul_overflow(p, c, &p) ||
+      __builtin_mul_overflow(p, d, &p))
+    return false;
+  return p <= MAX_ELEMS;
+}
+
 // ---- device-side types ----
 typedef __bf16 bf16;
 typedef unsigned short u16;

@@ -348,7 +348,8 @@ extern "C" catq_status catq_aux_rmsnorm_fwd(const void* x, catq_dtype x_dtype, i
   clear_error();
   CATQ_REQUIRE(dtype_ok(x_dtype), CATQ_ERR_DTYPE, "bad dtype");
   CATQ_REQUIRE(x && y, CATQ_ERR_NULL, "x and y must not be NULL");
-  CATQ_REQUIRE(rows > 0 && n > 0 && n % 8 == 0, CATQ_ERR_SHAPE, "need rows > 0 and n a multiple of 8");
+  CATQ_REQUIRE(count_ok(rows, n) && n % 8 == 0, CATQ_ERR_SHAPE,
+               "need rows > 0, n a multiple of 8 and rows*n <= 2^38");
   CATQ_REQUIRE(eps >= 0, CATQ_ERR_VALUE, "eps must be >= 0");
   CATQ_REQUIRE(aligned16(x) && aligned16(y), CATQ_ERR_ALIGN, "misaligned");
   const double xs = x_dtype == CATQ_BF16 ? 2.0 : 4.0;
@@ -371,7 +372,8 @@ extern "C" catq_status catq_aux_rmsnorm_bwd(const void* x, catq_dtype x_dtype, c
   clear_error();
   CATQ_REQUIRE(dtype_ok(x_dtype), CATQ_ERR_DTYPE, "bad dtype");
   CATQ_REQUIRE(x && rstd && dy && dx, CATQ_ERR_NULL, "NULL argument");
-  CATQ_REQUIRE(rows > 0 && n > 0 && n % 8 == 0, CATQ_ERR_SHAPE, "need rows > 0 and n a multiple of 8");
+  CATQ_REQUIRE(count_ok(rows, n) && n % 8 == 0, CATQ_ERR_SHAPE,
+               "need rows > 0, n a multiple of 8 and rows*n <= 2^38");
   CATQ_REQUIRE(aligned16(x) && aligned16(dy) && aligned16(dres) && aligned16(dx), CATQ_ERR_ALIGN,
                "misaligned");
   const double xs = x_dtype == CATQ_BF16 ? 2.0 : 4.0;
@@ -400,7 +402,8 @@ extern "C" catq_status catq_aux_act_quant(const void* x, catq_dtype x_dtype, int
   CATQ_REQUIRE(dtype_ok(x_dtype), CATQ_ERR_DTYPE, "x must be bf16 or fp32");
   CATQ_REQUIRE(n > 0 && group > 0 && n % group == 0 && group % 8 == 0, CATQ_ERR_SHAPE,
                "group must be a multiple of 8 dividing n");
-  CATQ_REQUIRE(rows <= INT32_MAX && n / group <= 65535, CATQ_ERR_SHAPE, "too many rows or groups");
+  CATQ_REQUIRE(rows <= INT32_MAX && n / group <= 65535 && count_ok(rows, n), CATQ_ERR_SHAPE,
+               "too many rows or groups");
   CATQ_REQUIRE(aligned16(x) && aligned16(y), CATQ_ERR_ALIGN, "misaligned");
   CATQ_REQUIRE(x_dtype == CATQ_BF16 || x != y, CATQ_ERR_VALUE,
                "an fp32 input cannot be quantized in place (y is bf16)");
@@ -422,7 +425,8 @@ extern "C" catq_status catq_aux_swiglu_fwd(const void* gu, int64_t rows, int64_t
                                            hipStream_t stream) {
   clear_error();
   CATQ_REQUIRE(gu && a, CATQ_ERR_NULL, "NULL argument");
-  CATQ_REQUIRE(rows > 0 && F > 0 && F % 8 == 0, CATQ_ERR_SHAPE, "need rows > 0 and F a multiple of 8");
+  CATQ_REQUIRE(count_ok(rows, 2 * F) && F % 8 == 0, CATQ_ERR_SHAPE,
+               "need rows > 0, F a multiple of 8 and rows*2F <= 2^38");
   CATQ_REQUIRE(aligned16(gu) && aligned16(a), CATQ_ERR_ALIGN, "misaligned");
   const int64_t n = rows * (F / 8);
   CATQ_TRACED(stream, "swiglu_fwd_kernel", 0.0, 6.0 * (double)rows * F, rows, F, 0,
@@ -436,7 +440,8 @@ extern "C" catq_status catq_aux_swiglu_bwd(const void* gu, const void* da, int64
                                            void* dgu, hipStream_t stream) {
   clear_error();
   CATQ_REQUIRE(gu && da && dgu, CATQ_ERR_NULL, "NULL argument");
-  CATQ_REQUIRE(rows > 0 && F > 0 && F % 8 == 0, CATQ_ERR_SHAPE, "need rows > 0 and F a multiple of 8");
+  CATQ_REQUIRE(count_ok(rows, 2 * F) && F % 8 == 0, CATQ_ERR_SHAPE,
+               "need rows > 0, F a multiple of 8 and rows*2F <= 2^38");
   CATQ_REQUIRE(aligned16(gu) && aligned16(da) && aligned16(dgu), CATQ_ERR_ALIGN, "misaligned");
   const int64_t n = rows * (F / 8);
   CATQ_TRACED(stream, "swiglu_bwd_kernel", 0.0, 10.0 * (double)rows * F, rows, F, 0,
@@ -461,7 +466,8 @@ extern "C" catq_status catq_aux_moe_route(const float* logits, int64_t T, int32_
                CATQ_ERR_NULL, "NULL argument");
   CATQ_REQUIRE(T > 0 && E > 0 && E <= 1024 && k >= 1 && k <= 16 && k <= E, CATQ_ERR_SHAPE,
                "need T > 0, 1 <= k <= min(16, E), E <= 1024");
-  CATQ_REQUIRE(T * k < (int64_t)1 << 31, CATQ_ERR_SHAPE, "too many routed rows");
+  CATQ_REQUIRE(count_ok(T, k) && T * k < (int64_t)1 << 31 && count_ok(T, E), CATQ_ERR_SHAPE,
+               "too many routed rows");
   CATQ_REQUIRE(workspace_bytes >= catq_aux_moe_route_workspace_bytes(T, E, k), CATQ_ERR_WORKSPACE,
                "workspace too small");
   int64_t* counts = reinterpret_cast<int64_t*>(workspace);
@@ -483,7 +489,8 @@ extern "C" catq_status catq_aux_moe_gather(const void* x, const int32_t* perm_ro
                                            int32_t k, int64_t h, void* xg, hipStream_t stream) {
   clear_error();
   CATQ_REQUIRE(x && perm_row && xg, CATQ_ERR_NULL, "NULL argument");
-  CATQ_REQUIRE(T > 0 && k > 0 && h > 0 && h % 8 == 0, CATQ_ERR_SHAPE, "bad shape");
+  CATQ_REQUIRE(count_ok(T, k, h) && h % 8 == 0, CATQ_ERR_SHAPE,
+               "need T, k, h > 0, h a multiple of 8 and T*k*h <= 2^38");
   CATQ_REQUIRE(aligned16(x) && aligned16(xg), CATQ_ERR_ALIGN, "misaligned");
   hipLaunchKernelGGL(moe_gather_kernel, dim3((unsigned)(T * k), chunks_y(h)), dim3(256), 0, stream,
                      (const bf16*)x, perm_row, k, h, (bf16*)xg);
@@ -498,7 +505,8 @@ extern "C" catq_status catq_aux_moe_combine(const void* yg, const int32_t* perm_
   clear_error();
   CATQ_REQUIRE(dtype_ok(y_dtype), CATQ_ERR_DTYPE, "bad dtype");
   CATQ_REQUIRE(yg && perm_row && weights && y, CATQ_ERR_NULL, "NULL argument");
-  CATQ_REQUIRE(T > 0 && k > 0 && h > 0 && h % 8 == 0, CATQ_ERR_SHAPE, "bad shape");
+  CATQ_REQUIRE(count_ok(T, k, h) && h % 8 == 0, CATQ_ERR_SHAPE,
+               "need T, k, h > 0, h a multiple of 8 and T*k*h <= 2^38");
   CATQ_REQUIRE(aligned16(yg) && aligned16(res) && aligned16(y), CATQ_ERR_ALIGN, "misaligned");
   if (y_dtype == CATQ_BF16)
     hipLaunchKernelGGL(moe_combine_kernel<bf16>, dim3((unsigned)T, chunks_y(h)), dim3(256), 0,
@@ -517,7 +525,8 @@ extern "C" catq_status catq_aux_moe_combine_bwd(const void* dy, const int32_t* p
                                                 int64_t h, void* dyg, hipStream_t stream) {
   clear_error();
   CATQ_REQUIRE(dy && perm_row && weights && dyg, CATQ_ERR_NULL, "NULL argument");
-  CATQ_REQUIRE(T > 0 && k > 0 && h > 0 && h % 8 == 0, CATQ_ERR_SHAPE, "bad shape");
+  CATQ_REQUIRE(count_ok(T, k, h) && h % 8 == 0, CATQ_ERR_SHAPE,
+               "need T, k, h > 0, h a multiple of 8 and T*k*h <= 2^38");
   CATQ_REQUIRE(aligned16(dy) && aligned16(dyg), CATQ_ERR_ALIGN, "misaligned");
   hipLaunchKernelGGL(moe_combine_bwd_kernel, dim3((unsigned)(T * k), chunks_y(h)), dim3(256), 0,
                      stream, (const bf16*)dy, perm_row, weights, k, h, (bf16*)dyg);
@@ -530,7 +539,8 @@ extern "C" catq_status catq_aux_moe_scatter_add(const void* dxg, const int32_t* 
                                                 hipStream_t stream) {
   clear_error();
   CATQ_REQUIRE(dxg && perm_row && dx, CATQ_ERR_NULL, "NULL argument");
-  CATQ_REQUIRE(T > 0 && k > 0 && h > 0 && h % 8 == 0, CATQ_ERR_SHAPE, "bad shape");
+  CATQ_REQUIRE(count_ok(T, k, h) && h % 8 == 0, CATQ_ERR_SHAPE,
+               "need T, k, h > 0, h a multiple of 8 and T*k*h <= 2^38");
   CATQ_REQUIRE(aligned16(dxg) && aligned16(dx), CATQ_ERR_ALIGN, "misaligned");
   hipLaunchKernelGGL(moe_scatter_add_kernel, dim3((unsigned)T, chunks_y(h)), dim3(256), 0, stream,
                      (const bf16*)dxg, perm_row, k, h, (bf16*)dx);

@@ -48,6 +48,8 @@ static catq_status check_linear_common(const void* X, const void* W_fake, catq_d
                                        const int64_t* row_offsets) {
   CATQ_REQUIRE(X && W_fake, CATQ_ERR_NULL, "X and W_fake must not be NULL");
   CATQ_REQUIRE(M > 0 && N > 0 && K > 0, CATQ_ERR_SHAPE, "M, N, K must be > 0");
+  CATQ_REQUIRE(n_experts < 1 || (count_ok(M, K) && count_ok(M, N) && count_ok(n_experts, N, K)),
+               CATQ_ERR_SHAPE, "M*K, M*N and n_experts*N*K must each be at most 2^38");
   CATQ_REQUIRE(dtype_ok(dtype), CATQ_ERR_DTYPE, "bad dtype");
   CATQ_REQUIRE(K % 8 == 0, CATQ_ERR_SHAPE, "K must be a multiple of 8");
   CATQ_REQUIRE(n_experts >= 1, CATQ_ERR_SHAPE, "n_experts must be >= 1");
@@ -64,7 +66,10 @@ using namespace catq;
 
 extern "C" size_t catq_workspace_size(int32_t which_call, int64_t M, int64_t N, int64_t K,
                                       int32_t n_experts) {
-  if (M <= 0 || N <= 0 || K <= 0 || n_experts < 1) return 0;
+  // sizes the calls would reject need no workspace
+  if (M <= 0 || N <= 0 || K <= 0 || n_experts < 1 || !count_ok(M, K) || !count_ok(M, N) ||
+      !count_ok(n_experts, N, K))
+    return 0;
   if (which_call == CATQ_WS_LINEAR_BWD) {
     const int64_t E = n_experts;
     const int ns = splits_used(M, N, K, n_experts);
@@ -120,7 +125,8 @@ extern "C" catq_status catq_fakeq_gateup_swiglu_fwd(const void* X, const void* W
                                                     hipStream_t stream) {
   clear_error();
   CATQ_REQUIRE(X && W_fake && gu && a, CATQ_ERR_NULL, "NULL argument");
-  CATQ_REQUIRE(M > 0 && F > 0 && K > 0 && F % 8 == 0, CATQ_ERR_SHAPE,
+  CATQ_REQUIRE(count_ok(M, K) && count_ok(M, 2 * F) && count_ok(2 * F, K) && F % 8 == 0,
+               CATQ_ERR_SHAPE,
                "M, K must be > 0 and F a positive multiple of 8");
   CATQ_REQUIRE(aligned16(X) && aligned16(W_fake) && aligned16(gu) && aligned16(a),
                CATQ_ERR_ALIGN, "pointers must be 16-byte aligned");
@@ -152,7 +158,8 @@ extern "C" catq_status catq_fakeq_down_swiglu_bwd(const void* dY, const void* W_
                                                   void* da, hipStream_t stream) {
   clear_error();
   CATQ_REQUIRE(dY && W_fake && gu && dgu, CATQ_ERR_NULL, "NULL argument");
-  CATQ_REQUIRE(M > 0 && N > 0 && F > 0 && F % 8 == 0, CATQ_ERR_SHAPE,
+  CATQ_REQUIRE(count_ok(M, N) && count_ok(M, 2 * F) && count_ok(N, F) && F % 8 == 0,
+               CATQ_ERR_SHAPE,
                "M, N must be > 0 and F a positive multiple of 8");
   CATQ_REQUIRE(aligned16(dY) && aligned16(W_fake) && aligned16(gu) && aligned16(dgu) &&
                    aligned16(da),

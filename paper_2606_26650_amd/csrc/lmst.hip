@@ -506,7 +506,8 @@ extern "C" catq_status catq_modulate_ternarize(const void* W, catq_dtype w_dtype
   clear_error();
   CATQ_REQUIRE(W && d_mu && d_alpha && d_delta && stats, CATQ_ERR_NULL,
                "W, factors and stats must not be NULL");
-  CATQ_REQUIRE(d_out > 0 && d_in > 0, CATQ_ERR_SHAPE, "d_out and d_in must be > 0");
+  CATQ_REQUIRE(count_ok(d_out, d_in), CATQ_ERR_SHAPE,
+               "d_out and d_in must be > 0 with d_out*d_in <= 2^38");
   CATQ_TRY(check_lmst_params(p, d_in));
   CATQ_REQUIRE(dtype_ok(w_dtype) && dtype_ok(wf_dtype), CATQ_ERR_DTYPE, "bad dtype");
   CATQ_REQUIRE(stats_mode == 0 || stats_mode == 1, CATQ_ERR_VALUE, "stats_mode must be 0 or 1");
@@ -556,7 +557,8 @@ extern "C" catq_status catq_ternarize_pack(const void* W, catq_dtype w_dtype, in
   clear_error();
   CATQ_REQUIRE(W && d_mu && d_alpha && d_delta && stats && packed, CATQ_ERR_NULL,
                "W, factors, stats and packed must not be NULL");
-  CATQ_REQUIRE(d_out > 0 && d_in > 0, CATQ_ERR_SHAPE, "d_out and d_in must be > 0");
+  CATQ_REQUIRE(count_ok(d_out, d_in), CATQ_ERR_SHAPE,
+               "d_out and d_in must be > 0 with d_out*d_in <= 2^38");
   CATQ_TRY(check_lmst_params(p, d_in));
   CATQ_REQUIRE(p->mode == CATQ_HARD, CATQ_ERR_VALUE, "the packed codes are those of HARD mode");
   CATQ_REQUIRE(dtype_ok(w_dtype), CATQ_ERR_DTYPE, "bad dtype");
@@ -595,7 +597,8 @@ extern "C" catq_status catq_pack_ternary(const int8_t* codes, int64_t d_out, int
                                          uint8_t* packed, hipStream_t stream) {
   clear_error();
   CATQ_REQUIRE(codes && packed, CATQ_ERR_NULL, "codes and packed must not be NULL");
-  CATQ_REQUIRE(d_out > 0 && d_in > 0, CATQ_ERR_SHAPE, "d_out and d_in must be > 0");
+  CATQ_REQUIRE(count_ok(d_out, d_in), CATQ_ERR_SHAPE,
+               "d_out and d_in must be > 0 with d_out*d_in <= 2^38");
   CATQ_REQUIRE(d_in % 4 == 0, CATQ_ERR_SHAPE, "d_in must be a multiple of 4");
   CATQ_REQUIRE(aligned16(codes) && aligned16(packed), CATQ_ERR_ALIGN,
                "codes and packed must be 16-byte aligned");
@@ -615,7 +618,7 @@ extern "C" catq_status catq_aux_adamw(float* p, const float* grad, float* m, flo
                                       double eps, float lo, float hi, hipStream_t stream) {
   clear_error();
   CATQ_REQUIRE(p && grad && m && v, CATQ_ERR_NULL, "NULL argument");
-  CATQ_REQUIRE(n > 0 && step >= 1, CATQ_ERR_SHAPE, "n must be > 0 and step >= 1");
+  CATQ_REQUIRE(count_ok(n) && step >= 1, CATQ_ERR_SHAPE, "n must be in [1, 2^38] and step >= 1");
   CATQ_REQUIRE(beta1 >= 0 && beta1 < 1 && beta2 >= 0 && beta2 < 1 && eps > 0 && lo <= hi,
                CATQ_ERR_VALUE, "bad optimizer hyper-parameters");
   const double bc1 = 1.0 - std::pow(beta1, (double)step);
@@ -632,7 +635,8 @@ extern "C" catq_status catq_aux_add(const void* a, const void* b, void* y, catq_
                                     int64_t n, hipStream_t stream) {
   clear_error();
   CATQ_REQUIRE(a && b && y, CATQ_ERR_NULL, "NULL argument");
-  CATQ_REQUIRE(n > 0 && n % 8 == 0, CATQ_ERR_SHAPE, "n must be a positive multiple of 8");
+  CATQ_REQUIRE(count_ok(n) && n % 8 == 0, CATQ_ERR_SHAPE,
+               "n must be a positive multiple of 8, at most 2^38");
   CATQ_REQUIRE(dtype_ok(dtype), CATQ_ERR_DTYPE, "bad dtype");
   CATQ_REQUIRE(aligned16(a) && aligned16(b) && aligned16(y), CATQ_ERR_ALIGN, "misaligned");
   const int64_t n8 = n / 8;

@@ -91,7 +91,8 @@ catq_status check_loss_args(const void* Y_q, const void* Y_fp, catq_dtype dtype,
                             float* loss, void* dY_q, catq_dtype dy_dtype) {
   CATQ_REQUIRE(dtype_ok(dy_dtype), CATQ_ERR_DTYPE, "bad dy dtype");
   CATQ_REQUIRE(Y_q && Y_fp && loss, CATQ_ERR_NULL, "Y_q, Y_fp and loss must not be NULL");
-  CATQ_REQUIRE(n > 0 && n % 8 == 0, CATQ_ERR_SHAPE, "n must be a positive multiple of 8");
+  CATQ_REQUIRE(count_ok(n) && n % 8 == 0, CATQ_ERR_SHAPE,
+               "n must be a positive multiple of 8, at most 2^38");
   CATQ_REQUIRE(dtype_ok(dtype), CATQ_ERR_DTYPE, "bad dtype");
   CATQ_REQUIRE(aligned16(Y_q) && aligned16(Y_fp) && aligned16(dY_q), CATQ_ERR_ALIGN,
                "pointers must be 16-byte aligned");

@@ -20,7 +20,7 @@ void clear_error() { g_msg[0] = '\0'; }
 }  // namespace catq
 
 extern "C" const char* catq_status_string(catq_status s) {
-  switch (s) {
+  switch ((int)s) {
     case CATQ_OK: return "CATQ_OK";
     case CATQ_ERR_NULL: return "CATQ_ERR_NULL";
     case CATQ_ERR_SHAPE: return "CATQ_ERR_SHAPE";

@@ -251,7 +251,8 @@ extern "C" catq_status catq_ternary_linear(const void* X, int64_t M, int64_t ldx
   CATQ_REQUIRE(M >= 0, CATQ_ERR_SHAPE, "M must be >= 0");
   if (M == 0) return CATQ_OK;
   CATQ_REQUIRE(X && packed && alpha && Y, CATQ_ERR_NULL, "X, packed, alpha and Y must not be NULL");
-  CATQ_REQUIRE(d_out > 0 && d_in > 0, CATQ_ERR_SHAPE, "d_out and d_in must be > 0");
+  CATQ_REQUIRE(count_ok(d_out, d_in), CATQ_ERR_SHAPE,
+               "d_out and d_in must be > 0 with d_out*d_in <= 2^38");
   CATQ_REQUIRE(g >= 128 && g % 128 == 0 && ((g / 128) & (g / 128 - 1)) == 0, CATQ_ERR_VALUE,
                "g must be 128 times a power of two");
   CATQ_REQUIRE(d_in % g == 0, CATQ_ERR_SHAPE, "d_in (%lld) must be a multiple of g (%d)",
