@@ -402,7 +402,7 @@ def main():
     def hbm(prefix):
         """Algorithmic GB/s of the elementwise launches whose tag starts with
         `prefix` (their bytes / their summed durations), with launch count."""
-        sel = {k: v for k, v in agg.items() if k.startswith(prefix)}
+        sel = {k: v for k, v in agg.items() if k.startswith(prefix)}   # str or tuple
         ms = sum(v["ms"] for v in sel.values())
         if not ms:
             return None
@@ -445,7 +445,8 @@ def main():
         "gemm_frac_all": all_gemm_flops / (all_gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
         "gemm_share_of_step": all_gemm_ms / args.steps / kernel_pass_ms,
         "step_gemm_tflop": all_gemm_flops / args.steps / 1e12,
-        "lmst_fwd": hbm("lmst_fwd_kernel"),
+        "lmst_fwd": hbm(("lmst_fwd_kernel", "lmst_soft_kernel")),  # every LM+ST forward launch
+        "lmst_soft": hbm("lmst_soft_kernel"),  # the soft steps with cached statistics
         "lmst_bwd": hbm("lmst_bwd_kernel"),
         "loss_first_last": [float(losses[0]), float(losses[-1])],
     }

@@ -123,13 +123,7 @@ __global__ __launch_bounds__(256) void lmst_fwd_kernel(FwdArgs a) {
 #pragma unroll
       for (int j = 0; j < 8; ++j) out[j] = w[u][j];
     } else if (MODE == CATQ_SOFT) {
-      const float inv_a = 1.0f / gs.alpha_div;
-      const float ED = one_minus_exp_neg(gs.delta * a.st.s4, gs.delta * a.st.s4l);
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        float xs = (w[u][j] - gs.mu) * inv_a;
-        out[j] = gs.alpha * transition_f(xs, gs.delta, ED, a.st);
-      }
+      soft_values<8>(w[u], soft_group(gs, a.st), out);
     } else {  // HARD
       const HardThresh th = hard_thresh(gs.delta, gs.alpha_div);
       float cs[8];
@@ -164,6 +158,39 @@ __global__ __launch_bounds__(256) void lmst_fwd_kernel(FwdArgs a) {
       }
     }
     if (a.Wf) store8<OT>(reinterpret_cast<OT*>(a.Wf) + o * 8, out);
+  }
+}
+
+// SOFT branch with cached statistics, the launch a calibration repeats every
+// soft step: one lane owns OCT octets (8 * OCT weights) of one group, so the
+// group's constants are formed once per 8 * OCT weights; a group of g weights
+// is g / (8 * OCT) adjacent lanes, and load u of lane i of a group reads octet
+// u * (g / (8 * OCT)) + i, so every load instruction of a wave covers whole
+// segments of 16 bytes per lane of a group.  Same arithmetic as
+// lmst_fwd_kernel's SOFT branch (bit-identical fake weights).
+template <typename WT, typename OT, int OCT>
+__global__ __launch_bounds__(256) void lmst_soft_kernel(FwdArgs a) {
+  constexpr int LOCT = OCT == 8 ? 3 : 2;
+  const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= (a.n_oct >> LOCT)) return;
+  const int lgl = a.lg - LOCT;              // log2(lanes per group)
+  const int64_t grp = c >> lgl;
+  const int li = (int)(c & ((1 << lgl) - 1));
+  const int64_t base = (grp << (a.lg + 3)) + 8 * (int64_t)li;   // element of octet li
+  const int64_t step = (int64_t)8 << lgl;                        // next octet of this lane
+  float w[OCT][8];
+#pragma unroll
+  for (int u = 0; u < OCT; ++u)
+    load8<WT>(reinterpret_cast<const WT*>(a.W) + base + u * step, w[u]);
+  const GroupScalars gs = group_scalars(a.stats[2 * grp], a.stats[2 * grp + 1], a.dmu[grp * a.s0],
+                                        a.dal[grp * a.s1], a.dde[grp * a.s2], a.delta0);
+  if (a.alpha_out && li == 0) a.alpha_out[grp] = gs.alpha;
+  const SoftGroup q = soft_group(gs, a.st);
+#pragma unroll
+  for (int u = 0; u < OCT; ++u) {
+    float out[8];
+    soft_values<8>(w[u], q, out);
+    store8<OT>(reinterpret_cast<OT*>(a.Wf) + base + u * step, out);
   }
 }
 
@@ -203,6 +230,22 @@ static void launch_fwd(const FwdArgs& a, int mode, bool stats, dim3 grid, hipStr
     launch_fwd_mode<WT, OT, CATQ_SOFT>(a, stats, grid, stream);
   else
     launch_fwd_mode<WT, OT, CATQ_HARD>(a, stats, grid, stream);
+}
+
+template <typename WT, typename OT>
+static void launch_soft(const FwdArgs& a, hipStream_t stream) {
+  char tag[96];
+  std::snprintf(tag, sizeof(tag), "lmst_soft_kernel<%s, %s>", tname<WT>(), tname<OT>());
+  const double n = (double)a.n_oct * 8.0;
+  const double ng = n / (8.0 * (1 << a.lg));
+  const double fac = 4.0 * ((a.s0 ? ng : 1) + (a.s1 ? ng : 1) + (a.s2 ? ng : 1));
+  const double bytes = n * sizeof(WT) + n * sizeof(OT) + fac + 8.0 * ng +
+                       (a.alpha_out ? 4.0 * ng : 0.0);
+  // 32 weights per lane (64 per lane measured slower: fewer waves in flight)
+  const int64_t lanes = a.n_oct >> 2;
+  CATQ_TRACED(stream, tag, 0.0, bytes, (int64_t)n, 0, 0,
+              hipLaunchKernelGGL((lmst_soft_kernel<WT, OT, 4>),
+                                 dim3((unsigned)((lanes + 255) / 256)), dim3(256), 0, stream, a));
 }
 
 catq_status check_lmst_params(const catq_lmst_params* p, int64_t d_in) {
@@ -535,8 +578,20 @@ extern "C" catq_status catq_modulate_ternarize(const void* W, catq_dtype w_dtype
   a.delta0 = p->delta0;
   a.st = make_st(p->mode == CATQ_SOFT ? (double)p->s : 1.0);
   a.inv_g = 1.0f / (float)p->group_size;
-  dim3 grid((unsigned)((a.n_oct + 256 * FWD_U - 1) / (256 * FWD_U)));
   const bool st = stats_mode == 0;
+  if (p->mode == CATQ_SOFT && !st && p->group_size >= 32) {
+    if (w_dtype == CATQ_BF16 && wf_dtype == CATQ_BF16)
+      launch_soft<bf16, bf16>(a, stream);
+    else if (w_dtype == CATQ_BF16)
+      launch_soft<bf16, float>(a, stream);
+    else if (wf_dtype == CATQ_BF16)
+      launch_soft<float, bf16>(a, stream);
+    else
+      launch_soft<float, float>(a, stream);
+    CATQ_CHECK_LAUNCH("modulate_ternarize");
+    return CATQ_OK;
+  }
+  dim3 grid((unsigned)((a.n_oct + 256 * FWD_U - 1) / (256 * FWD_U)));
   if (w_dtype == CATQ_BF16 && wf_dtype == CATQ_BF16)
     launch_fwd<bf16, bf16>(a, p->mode, st, grid, stream);
   else if (w_dtype == CATQ_BF16)

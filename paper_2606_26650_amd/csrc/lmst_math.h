@@ -105,6 +105,83 @@ __device__ __forceinline__ void hard_codes8(const float (&w)[8], float mu, const
   hard_codes_n<8>(w, mu, t, c);
 }
 
+// The softened ternarisation of one group in the base-2 exponent domain.
+// With z = (w - mu) * sc = 2 s W_hat log2(e), y = |z| and x = |W_hat|:
+//   q_a = e^{-2 s |x - Delta|} = 2^{-|y - dz|},   e^{-4 s x} = 2^{-2 y},
+//   E = 1 - e^{-4 s x},  q_b = q_a (1 - E) (x < Delta) or q_a (1 - E_Delta),
+//   alpha f = copysign(num / ((1 + q_a)(1 + q_b)), z) * alpha / tanh(s),
+//   num = E (x >= Delta) or q_a E (x < Delta)
+// (the cancellation-free form of Eq. 5; the scalings of the exponents and of
+// the output are folded into per-group constants).
+struct SoftGroup {
+  float mu;     // mu of Eq. 3
+  float sc;     // 2 s log2(e) / alpha:  z = (w - mu) * sc
+  float inv_a;  // 1 / alpha  (when sc does not fit a float)
+  float c2s;    // 2 s log2(e)
+  float dz;     // 2 s Delta log2(e)
+  float ed;     // E_Delta = 1 - e^{-4 s Delta}
+  float ak;     // alpha / tanh(s)
+  bool fast;    // sc finite: z in one product
+};
+
+__device__ __forceinline__ SoftGroup soft_group(const GroupScalars& gs, const StConst& c) {
+  SoftGroup q;
+  q.mu = gs.mu;
+  q.inv_a = __builtin_amdgcn_rcpf(gs.alpha_div);  // 1 ulp; W_hat needs no more
+  q.c2s = c.c2s;
+  q.sc = q.inv_a * c.c2s;
+  q.fast = fabsf(q.sc) <= 3.0e38f;  // false for inf and NaN
+  q.dz = gs.delta * c.c2s;
+  q.ed = one_minus_exp_neg(gs.delta * c.s4, gs.delta * c.s4l);
+  q.ak = gs.alpha * c.k2;
+  return q;
+}
+
+// 1 - 2^{-2y} (= 1 - e^{-t}, t = 2 y ln 2) for y >= 0 given T = 2^{-2y}:
+// below t = 1/8 the series of 1 - e^{-t} to t^5 in powers of y (truncation
+// below 5e-8 relative), above it 1 - T (no cancellation: T < 0.89).
+__device__ __forceinline__ float one_minus_exp2_neg2(float y, float T) {
+  if (y < 0.09016844f) {
+    float p = 0.04266738519f;
+    p = fmaf(p, y, -0.1538900584f);
+    p = fmaf(p, y, 0.4440328777f);
+    p = fmaf(p, y, -0.9609060287f);
+    p = fmaf(p, y, 1.386294365f);
+    return y * p;
+  }
+  return 1.0f - T;
+}
+
+// alpha * f(W_hat; s, Delta) of one weight (Eq. 5 times the group scale).
+template <bool FAST>
+__device__ __forceinline__ float soft_value(float w, const SoftGroup& q) {
+  const float z = FAST ? (w - q.mu) * q.sc : ((w - q.mu) * q.inv_a) * q.c2s;
+  const float y = fabsf(z);
+  const float d = y - q.dz;
+  const float qa = __builtin_amdgcn_exp2f(-fabsf(d));
+  const float T = __builtin_amdgcn_exp2f(-(y + y));
+  const float E = one_minus_exp2_neg2(y, T);
+  const bool ge = d >= 0.0f;
+  const float eb = ge ? q.ed : E;
+  const float qb = fmaf(-qa, eb, qa);
+  const float opa = 1.0f + qa;
+  const float den = fmaf(opa, qb, opa);
+  const float num = ge ? E : qa * E;
+  return copysignf(num * __builtin_amdgcn_rcpf(den), z) * q.ak;
+}
+
+template <int N>
+__device__ __forceinline__ void soft_values(const float (&w)[N], const SoftGroup& q,
+                                            float (&out)[N]) {
+  if (q.fast) {
+#pragma unroll
+    for (int j = 0; j < N; ++j) out[j] = soft_value<true>(w[j], q);
+  } else {
+#pragma unroll
+    for (int j = 0; j < N; ++j) out[j] = soft_value<false>(w[j], q);
+  }
+}
+
 // Transition function f of Eq. 5 at x_hat (cancellation-free form).
 __device__ __forceinline__ float transition_f(float xs, float delta, float ED, const StConst& c) {
   float x = fabsf(xs);

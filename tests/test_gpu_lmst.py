@@ -85,6 +85,38 @@ def test_soft_bf16_output_and_cached_stats(catq):
     assert np.all(np.abs(got - ref) <= 2.0 ** -8 * np.abs(ref) + 1e-30)
 
 
+@pytest.mark.parametrize("g", [32, 64, 128, 256, 512])
+@pytest.mark.parametrize("wdtype,odtype", [("bf16", "bf16"), ("bf16", "f32"), ("f32", "bf16"),
+                                           ("f32", "f32")])
+def test_soft_cached_stats_kernel(catq, g, wdtype, odtype):
+    """The soft step with cached statistics (its own kernel: 32 weights per
+    lane) writes the same bits as the soft branch that computes the
+    statistics, for every group size it takes, a ragged row count and a
+    shared threshold factor; fp32 outputs within 1e-5 of the oracle."""
+    import torch
+    rows, d_in = 45, 1536
+    for s, shared in ((15.0, (1, 1, 1)), (0.625, (1, 1, 0)), (30.0, (0, 1, 1))):
+        Wo, Wd, fac = _case(5, rows, d_in, g, wdtype, shared=shared)
+        ng = rows * d_in // g
+        dt = torch.bfloat16 if odtype == "bf16" else torch.float32
+        stats = torch.zeros(ng, 2, dtype=torch.float32, device="cuda")
+        wf = torch.empty(rows, d_in, dtype=dt, device="cuda")
+        wf2 = torch.empty_like(wf)
+        al, al2 = (torch.empty(ng, dtype=torch.float32, device="cuda") for _ in range(2))
+        dm, da, dd = (to_dev_f32(f) for f in fac)
+        p = catq.lmst_params(group_size=g, mode=catq.SOFT, s=s, strides=shared)
+        catq.catq_modulate_ternarize(Wd, dm, da, dd, p, stats, 0, W_fake=wf, alpha_out=al)
+        catq.catq_modulate_ternarize(Wd, dm, da, dd, p, stats, 1, W_fake=wf2, alpha_out=al2)
+        torch.cuda.synchronize()
+        bits = torch.int16 if odtype == "bf16" else torch.int32
+        assert torch.equal(wf.view(bits), wf2.view(bits)), (g, s, shared)
+        assert torch.equal(al, al2)
+        if odtype == "f32":
+            ref = lmst.modulate_ternarize(Wo, g, *fac, lmst.SOFT, s=s, strides=shared)
+            ok, worst = elem_rel_ok(host(wf2), ref["W_fake"], 1e-5)
+            assert ok, (g, s, worst)
+
+
 @pytest.mark.parametrize("shared", [(1, 1, 1), (1, 1, 0), (0, 0, 0)])
 @pytest.mark.parametrize("wdtype", ["bf16", "f32"])
 def test_hard_codes_bit_exact(catq, shared, wdtype):
