@@ -197,6 +197,17 @@ __device__ __forceinline__ void dma16_buf(i32x4_rsrc rsrc, uint32_t voff, uint32
                : "memory", "m0");
 #endif
 }
+// 4-byte buffer -> LDS copy (lane l landing at lds_base + 4*l) from byte
+// offset voff of the resource; offsets past its size land as zero.
+__device__ __forceinline__ void dma4_buf(i32x4_rsrc rsrc, uint32_t voff, const void* lds_base) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  const unsigned l = __builtin_amdgcn_readfirstlane(
+      (unsigned)(uintptr_t)(__attribute__((address_space(3))) const void*)lds_base);
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, 0 offen lds" ::"s"(l), "v"(voff),
+               "s"(rsrc)
+               : "memory", "m0");
+#endif
+}
 #pragma clang diagnostic pop
 
 __device__ __forceinline__ void wait_vmem() {

@@ -371,20 +371,26 @@ __global__ __launch_bounds__(256) void flash_dsum_kernel(FaArgs a) {
 // ------------------------------------------------------------- dK and dV
 //
 // Block = 8 wavefronts over 128 keys of one kv head.  Waves 0-3 accumulate
-// dV and waves 4-7 dK, each for the 32 keys of slab w % 4; both roles form
-// S^T for their keys, the dK waves also dP^T.  A wave thus holds one
-// 32 x D accumulator set instead of two, so two waves fit on each SIMD and
-// the exponentials and packing of one overlap the matrix products of the
-// other.  The Q and dO tiles of 64 queries are staged through registers
-// (threads 0-255 stage Q, 256-511 dO) into row-major and transposed LDS
-// copies shared by all eight waves.
+// dV and waves 4-7 dK, each for the 32 keys of slab w % 4.  Q and dO tiles of
+// 64 queries stream into double-buffered swizzled row-major LDS tiles by
+// direct copies (waves 0-3 copy Q, 4-7 dO, with the tile's log-sum-exp and
+// D), one tile ahead.  Per tile the dV wave of a slab forms S^T and P
+// (exponentials, mask) and hands P to the dK wave of the same slab through
+// LDS, while that wave forms dP^T; the two waves hold P and dP in the same
+// register layout (lane = key, registers = queries), so after one barrier
+// the dK wave forms dS = P (dP - D) from P read back at its own lane.  The
+// products with dO^T and Q^T take their operands by transpose reads of the
+// row-major tiles.  Each wave holds one 32 x D accumulator set and issues 32
+// MFMAs per tile (two independent 32-query chains for the scores, four
+// accumulators for the products); two waves share a SIMD.
 
 constexpr int DKDV_NT = 512;
 
 template <int D, int ROLE>  // ROLE 0: dV, 1: dK
-__device__ __forceinline__ void dkdv_waves(const FaArgs& a, u16* sQ, u16* sQt, u16* sO, u16* sOt,
-                                           float* sL, float* sD) {
+__device__ __forceinline__ void dkdv_waves(const FaArgs& a, uint4* sQ, uint4* sO, float* sL,
+                                           float* sD, float* sP) {
   using C = fa::Cfg<D>;
+  constexpr int TW = 64 * D / 8;  // 16-byte slots of one 64 x D tile
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
   const int ks = __builtin_amdgcn_readfirstlane(tid >> 6) & 3;  // key slab of this wave
   // grid (B*Hkv*hsplit, key tiles): block chunk of a kv head takes its share
@@ -395,113 +401,142 @@ __device__ __forceinline__ void dkdv_waves(const FaArgs& a, u16* sQ, u16* sQt, u
   const int k0 = kt * 128;
   const int wave_first = k0 + 32 * ks;  // queries below this see none of the wave's keys
   const int kme = wave_first + l32;     // this lane's key (column of S^T[q][key])
-  const bf16* Kb = a.K + ((int64_t)(b * a.Hkv + kvh) * a.S) * D;
-  const bf16* Vb = a.V + ((int64_t)(b * a.Hkv + kvh) * a.S) * D;
-  // K (and for dK, V) fragments of this lane's key: operand B of S^T = Q K^T
-  // and dP^T = dO V^T
-  bf16x8 kf[C::KS];
-  [[maybe_unused]] bf16x8 vf[C::KS];
+  // this lane's K row (dV waves: operand B of S^T = Q K^T) or V row (dK
+  // waves: operand B of dP^T = dO V^T)
+  const bf16* Rb = (ROLE == 0 ? a.K : a.V) + ((int64_t)(b * a.Hkv + kvh) * a.S) * D;
+  bf16x8 rf[C::KS];
 #pragma unroll
   for (int t = 0; t < C::KS; ++t) {
-    u32x4 kv = {0u, 0u, 0u, 0u};
-    if (kme < a.S) kv = *reinterpret_cast<const u32x4*>(Kb + (int64_t)kme * D + 16 * t + 8 * g);
-    kf[t] = __builtin_bit_cast(bf16x8, kv);
-    if constexpr (ROLE == 1) {
-      u32x4 vv = {0u, 0u, 0u, 0u};
-      if (kme < a.S) vv = *reinterpret_cast<const u32x4*>(Vb + (int64_t)kme * D + 16 * t + 8 * g);
-      vf[t] = __builtin_bit_cast(bf16x8, vv);
-    }
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (kme < a.S) v = *reinterpret_cast<const u32x4*>(Rb + (int64_t)kme * D + 16 * t + 8 * g);
+    rf[t] = __builtin_bit_cast(bf16x8, v);
   }
   f32x16 acc[C::DB];
 #pragma unroll
   for (int i = 0; i < C::DB; ++i) acc[i] = fa::zero16();
+  fa::TrOffsets<D> tro;
+  tro.init(lane);
   const int qt0 = k0 / fa::BK;
   const int nqt = (a.S + fa::BK - 1) / fa::BK;
-  const bool stage_q = tid < 256;
-  const int st = tid & 255;
+  // P of this slab and a tile's 64 queries: [2 x 32-query blocks][4][64
+  // lanes][4] floats (lane-major 16-byte chunks, no bank conflicts)
+  float* P = sP + ks * (2 * 16 * 64);
   for (int gq = chunk * Gc; gq < (chunk + 1) * Gc; ++gq) {
     const int h = kvh * G + gq;
     const bf16* Qb = a.Q + ((int64_t)(b * a.Hq + h) * a.S) * D;
-    const float* Lb = a.lse + (int64_t)(b * a.Hq + h) * a.S;
-    const float* Db = a.Dsum + (int64_t)(b * a.Hq + h) * a.S;
     const bf16* dOb = a.dO + (int64_t)b * a.S * (a.Hq * D) + (int64_t)h * D;
-    fa::Tile<D> tl;
-    if (stage_q)
-      tl.load(Qb, D, (int64_t)qt0 * fa::BK, a.S, st);
-    else
-      tl.load(dOb, (int64_t)a.Hq * D, (int64_t)qt0 * fa::BK, a.S, st);
+    // log-sum-exp (Q copiers) or D (dO copiers) of the head's queries; reads
+    // past the sequence end land as zero
+    const float* LDb = (ROLE == 0 ? a.lse : a.Dsum) + (int64_t)(b * a.Hq + h) * a.S;
+    const i32x4_rsrc ld_rs = buf_rsrc(LDb, (uint32_t)a.S * 4u);
+    // this wave's share of the copies of tile q0n into buffer buf
+    auto issue = [&](int buf, int q0n) {
+      if (ROLE == 0)
+        fa::dma_tile<D>(Qb, D, q0n, a.S, sQ + buf * TW, ks, lane);
+      else
+        fa::dma_tile<D>(dOb, (int64_t)a.Hq * D, q0n, a.S, sO + buf * TW, ks, lane);
+      if (ks == 0) dma4_buf(ld_rs, (uint32_t)(q0n + lane) * 4u, (ROLE == 0 ? sL : sD) + buf * 64);
+    };
+    // the first tile's copies; a tile's buffers are refilled only after the
+    // barrier that ends the tile two before it
+    issue(0, qt0 * fa::BK);
+    wait_vmem();
+    __syncthreads();
     for (int qt = qt0; qt < nqt; ++qt) {
-      const int q0 = qt * fa::BK;
-      __syncthreads();
-      if (stage_q) {
-        tl.store_rows(sQ);
-        tl.store_transposed(sQt);
-      } else {
-        tl.store_rows(sO);
-        tl.store_transposed(sOt);
-      }
-      if (tid < fa::BK) {
-        const int q = q0 + tid;
-        sL[tid] = q < a.S ? Lb[q] : 0.f;
-      } else if (tid >= 256 && tid < 256 + fa::BK) {
-        const int q = q0 + tid - 256;
-        sD[tid - 256] = q < a.S ? Db[q] : 0.f;
-      }
-      __syncthreads();
-      if (qt + 1 < nqt) {
-        if (stage_q)
-          tl.load(Qb, D, (int64_t)(q0 + fa::BK), a.S, st);
-        else
-          tl.load(dOb, (int64_t)a.Hq * D, (int64_t)(q0 + fa::BK), a.S, st);
-      }
-      if (q0 + fa::BK - 1 < wave_first) continue;
-#pragma unroll 1
-      for (int qb = 0; qb < 2; ++qb) {
-        // S^T[q][key] (and dP^T[q][key]) for 32 queries
-        f32x16 s = fa::zero16();
-        [[maybe_unused]] f32x16 dp = fa::zero16();
+      const int q0 = qt * fa::BK, buf = (qt - qt0) & 1;
+      if (qt + 1 < nqt) issue(buf ^ 1, q0 + fa::BK);
+      const uint4* tQ = sQ + buf * TW;
+      const uint4* tO = sO + buf * TW;
+      const float* tL = sL + buf * 64;
+      const float* tD = sD + buf * 64;
+      // a tile wholly before the slab's keys is skipped, but its copies and
+      // barriers are kept (both waves of a slab skip alike)
+      const bool active = q0 + fa::BK - 1 >= wave_first;
+      // S^T[q][key] (dV waves) or dP^T[q][key] (dK waves) for the two 32-query
+      // blocks: two independent accumulation chains, each fragment read one
+      // step ahead of its products
+      f32x16 s[2];
+      s[0] = fa::zero16();
+      s[1] = fa::zero16();
+      if (active) {
+        const uint4* src = ROLE == 0 ? tQ : tO;
+        bf16x8 fr[2][2];
+        fr[0][0] = fa::tfrag_row<D>(src, l32, g);
+        fr[0][1] = fa::tfrag_row<D>(src, 32 + l32, g);
 #pragma unroll
         for (int t = 0; t < C::KS; ++t) {
-          s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              fa::frag_rows(sQ, qb * 32 + l32, 16 * t + 8 * g, C::KP), kf[t], s, 0, 0, 0);
-          if constexpr (ROLE == 1)
-            dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                fa::frag_rows(sO, qb * 32 + l32, 16 * t + 8 * g, C::KP), vf[t], dp, 0, 0, 0);
-        }
-        // P (dV) or dS = P (dP - D) (dK), rows = queries of this lane's
-        // registers; the causal / length mask only where the 32 x 32 block
-        // crosses the wave's diagonal or the sequence end (uniform)
-        const int qb0 = q0 + qb * 32;
-        auto p_of = [&](int r, bool masked) {
-          const int qi = qb * 32 + fa::acc_row(r, g);
-          float p = __builtin_amdgcn_exp2f(fmaf(s[r], a.c, -sL[qi]));
-          if (masked) {
-            const int q = q0 + qi;
-            if (q < kme || q >= a.S || kme >= a.S) p = 0.f;
+          if (t + 1 < C::KS) {
+            fr[(t + 1) & 1][0] = fa::tfrag_row<D>(src, l32, 2 * (t + 1) + g);
+            fr[(t + 1) & 1][1] = fa::tfrag_row<D>(src, 32 + l32, 2 * (t + 1) + g);
           }
-          if constexpr (ROLE == 0)
-            s[r] = p;
-          else
-            dp[r] = p * (dp[r] - sD[qi]);
-        };
-        if (qb0 < wave_first + 31 || qb0 + 32 > a.S || wave_first + 31 >= a.S) {
-#pragma unroll
-          for (int r = 0; r < 16; ++r) p_of(r, true);
-        } else {
-#pragma unroll
-          for (int r = 0; r < 16; ++r) p_of(r, false);
+          s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[t & 1][0], rf[t], s[0], 0, 0, 0);
+          s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[t & 1][1], rf[t], s[1], 0, 0, 0);
         }
-        // dV[key][d] += P^T dO ; dK[key][d] += dS^T Q  (contraction over queries)
+        if constexpr (ROLE == 0) {
+          // P, rows = queries of this lane's registers; the causal / length
+          // mask only on the 32 x 32 blocks that cross the slab's diagonal or
+          // the sequence end (uniform)
 #pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const bf16x8 pf = fa::pack8(ROLE == 0 ? s : dp, hh);
+          for (int qb = 0; qb < 2; ++qb) {
+            const int qb0 = q0 + qb * 32;
+            const bool masked = qb0 < wave_first + 31 || qb0 + 32 > a.S || wave_first + 31 >= a.S;
+            if (masked) {
 #pragma unroll
-          for (int i = 0; i < C::DB; ++i)
-            acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                pf, fa::frag_tr(ROLE == 0 ? sOt : sQt, i * 32 + l32, 2 * qb + hh, g), acc[i], 0,
-                0, 0);
+              for (int r = 0; r < 16; ++r) {
+                const int qi = qb * 32 + fa::acc_row(r, g);
+                const int q = q0 + qi;
+                const float p = __builtin_amdgcn_exp2f(fmaf(s[qb][r], a.c, -tL[qi]));
+                s[qb][r] = (q < kme || q >= a.S || kme >= a.S) ? 0.f : p;
+              }
+            } else {
+#pragma unroll
+              for (int r = 0; r < 16; ++r) {
+                const int qi = qb * 32 + fa::acc_row(r, g);
+                s[qb][r] = __builtin_amdgcn_exp2f(fmaf(s[qb][r], a.c, -tL[qi]));
+              }
+            }
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+              f32x4 v = {s[qb][4 * c], s[qb][4 * c + 1], s[qb][4 * c + 2], s[qb][4 * c + 3]};
+              *reinterpret_cast<f32x4*>(P + ((qb * 4 + c) * 64 + lane) * 4) = v;
+            }
+          }
         }
       }
+      __syncthreads();
+      if (active) {
+        if constexpr (ROLE == 1) {
+          // dS = P (dP - D)
+#pragma unroll
+          for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+              const f32x4 pv = *reinterpret_cast<const f32x4*>(P + ((qb * 4 + c) * 64 + lane) * 4);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                const int r = 4 * c + e;
+                const int qi = qb * 32 + fa::acc_row(r, g);
+                s[qb][r] = pv[e] * (s[qb][r] - tD[qi]);
+              }
+            }
+        }
+        // dV[key][d] += P^T dO ; dK[key][d] += dS^T Q  (contraction over the
+        // tile's queries, 16 at a time; dO^T and Q^T by transpose reads)
+        const uint4* tsrc = ROLE == 0 ? tO : tQ;
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {
+            const bf16x8 pf = fa::pack8(s[qb], hh);
+#pragma unroll
+            for (int i = 0; i < C::DB; ++i)
+              acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                  pf, fa::tr_read<D>(tsrc, tro, i, 2 * qb + hh), acc[i], 0, 0, 0);
+          }
+      }
+      // the next tile's copies have landed; this tile's buffers and P are free
+      wait_vmem();
+      __syncthreads();
     }
   }
   // acc[i][r]: key row = 32 ks + acc_row(r, g) within the block, d column = 32 i + l32
@@ -519,16 +554,15 @@ __device__ __forceinline__ void dkdv_waves(const FaArgs& a, u16* sQ, u16* sQt, u
 
 template <int D>
 __global__ __launch_bounds__(DKDV_NT, 2) void flash_bwd_dkdv_kernel(FaArgs a) {
-  using C = fa::Cfg<D>;
-  __shared__ u16 sQ[fa::BK * C::KP];
-  __shared__ u16 sQt[D * fa::TP];
-  __shared__ u16 sO[fa::BK * C::KP];   // dO rows
-  __shared__ u16 sOt[D * fa::TP];      // dO transposed
-  __shared__ float sL[fa::BK], sD[fa::BK];
+  constexpr int TW = 64 * D / 8;
+  __shared__ uint4 sQ[2 * TW];  // Q tiles (row-major, swizzled), double-buffered
+  __shared__ uint4 sO[2 * TW];  // dO tiles
+  __shared__ __attribute__((aligned(16))) float sL[2 * 64], sD[2 * 64];
+  __shared__ __attribute__((aligned(16))) float sP[4 * 2 * 16 * 64];  // P handed from dV to dK waves
   if (__builtin_amdgcn_readfirstlane(threadIdx.x >> 6) < 4)
-    dkdv_waves<D, 0>(a, sQ, sQt, sO, sOt, sL, sD);
+    dkdv_waves<D, 0>(a, sQ, sO, sL, sD, sP);
   else
-    dkdv_waves<D, 1>(a, sQ, sQt, sO, sOt, sL, sD);
+    dkdv_waves<D, 1>(a, sQ, sO, sL, sD, sP);
 }
 
 // ------------------------------------------------------------------- dQ
