@@ -261,15 +261,24 @@ __global__ __launch_bounds__(fa::NT, 2) void flash_fwd_kernel(FaArgs a) {
     // the previous barrier
     if (kt + 1 < nkt) issue(buf ^ 1, k0 + fa::BK);
     if (k0 <= wave_last) {
-      // S^T for the two 32-key blocks
+      // S^T for the two 32-key blocks: two independent accumulation chains,
+      // each fragment read one step ahead of its products
       f32x16 s[2];
+      s[0] = fa::zero16();
+      s[1] = fa::zero16();
+      {
+        bf16x8 fr[2][2];
+        fr[0][0] = fa::tfrag_row<D>(sK[buf], l32, g);
+        fr[0][1] = fa::tfrag_row<D>(sK[buf], 32 + l32, g);
 #pragma unroll
-      for (int sb = 0; sb < 2; ++sb) {
-        s[sb] = fa::zero16();
-#pragma unroll
-        for (int t = 0; t < C::KS; ++t)
-          s[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              fa::tfrag_row<D>(sK[buf], sb * 32 + l32, 2 * t + g), qf[t], s[sb], 0, 0, 0);
+        for (int t = 0; t < C::KS; ++t) {
+          if (t + 1 < C::KS) {
+            fr[(t + 1) & 1][0] = fa::tfrag_row<D>(sK[buf], l32, 2 * (t + 1) + g);
+            fr[(t + 1) & 1][1] = fa::tfrag_row<D>(sK[buf], 32 + l32, 2 * (t + 1) + g);
+          }
+          s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[t & 1][0], qf[t], s[0], 0, 0, 0);
+          s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[t & 1][1], qf[t], s[1], 0, 0, 0);
+        }
       }
       // causal / length mask, only on tiles that cross the wave's diagonal or
       // the sequence end; then the tile max of the raw scores (the scale c > 0
