@@ -137,10 +137,11 @@ N_SAMPLES, N_EPOCHS = 4, 3
 def test_sliding_calibration_against_oracle(catq):
     """Window-by-window calibration of three blocks (l = 2, stride 1).  Gated
     per optimiser step on the GPU's own state: the oracle's window step on
-    the factors the GPU held (loss; the last block's factor gradients end to
-    end, the earlier block's from its own backward of the gradient reaching
-    its output) and the oracle's AdamW on the same factors, gradients and
-    moments; the final
+    the factors the GPU held (loss; every block's factor gradients from its
+    own backward of the gradient reaching its output, for the last block the
+    loss gradient; end to end they carry the earlier block's forward noise
+    through the loss gradient and are reported, under a 5e-2 tripwire) and
+    the oracle's AdamW on the same factors, gradients and moments; the final
     codes against the oracle's hard decision on the GPU's final factors, bit
     for bit.  Reported: the oracle's own trajectory."""
     import torch
@@ -159,8 +160,9 @@ def test_sliding_calibration_against_oracle(catq):
     def obs(phase, c, b, mode, s, lr):
         rec.span = cal.span
         rec(phase, c, b, mode, s, lr)
-        if phase == "grads":   # gradients reaching the outputs of the earlier blocks
-            rec.steps[-1]["dy_in"] = [host(blk.dx) for blk in c.blk.blocks[1:]]
+        if phase == "grads":   # gradients reaching the outputs of the window's blocks
+            rec.steps[-1]["dy_in"] = ([host(blk.dx) for blk in c.blk.blocks[1:]] +
+                                      [host(c.blk.blocks[-1].dy)])
 
     cal.observer = obs
     bufs = cal.run()
@@ -184,12 +186,11 @@ def test_sliding_calibration_against_oracle(catq):
         assert abs(bef["loss"] - ref["loss"]) <= 2e-2 * ref["loss"], ((a, e), bef["step"])
         for j in range(e - a):
             grads = per_linear(blks[a + j], DenseBlock.split_fused, cfg, bef["g"][3 * j:3 * j + 3])
-            if j == e - a - 1:
-                gate = ref["fgrads"][j]
-            else:   # an earlier block: its own backward from the gradient at its output
-                _, cache = block.block_forward(ref["inputs"][j], ref["W_fake"][j], cfg)
-                _, dW = block.block_backward(r["dy_in"][j], cache, ref["W_fake"][j], cfg)
-                gate = calib.factor_grads_all(dW, Wos[a + j], facs[j], 128, bef["mode"], s, 30.0)
+            # each block on its own backward from the gradient that reaches its
+            # output (the last block: the loss gradient the GPU computed)
+            _, cache = block.block_forward(ref["inputs"][j], ref["W_fake"][j], cfg)
+            _, dW = block.block_backward(r["dy_in"][j], cache, ref["W_fake"][j], cfg)
+            gate = calib.factor_grads_all(dW, Wos[a + j], facs[j], 128, bef["mode"], s, 30.0)
             for k in grads:
                 for i in range(3):
                     err = max_norm_err(grads[k][i], gate[k][i])
