@@ -147,6 +147,31 @@ __device__ __forceinline__ void dma_tile(const bf16* base, int64_t ld, int64_t r
   }
 }
 
+// The same 64 x D tile copy through a buffer resource: a lane keeps the byte
+// offsets of its NI 16-byte chunks within a tile (rows past the sequence
+// read as zero; their queries are masked), and each tile costs one resource
+// and NI copies.
+template <int D>
+struct TileCopy {
+  static constexpr int CPR = D / 8, RPI = 64 / CPR, NI = 64 / RPI / 4;
+  uint32_t voff[NI];
+  // wave: 0..3 within the four copying waves
+  __device__ __forceinline__ void init(int64_t ld, int wave, int lane) {
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int r = (wave * NI + i) * RPI + lane / CPR;
+      const int c = (lane % CPR) ^ tswz<D>(r);
+      voff[i] = (uint32_t)((int64_t)r * ld * 2 + c * 16);
+    }
+  }
+  __device__ __forceinline__ void issue(const bf16* base, int64_t ld, int row0, int rows, uint4* lds,
+                                        int wave) const {
+    const i32x4_rsrc rs = buf_rsrc(base + (int64_t)row0 * ld, (uint32_t)((int64_t)(rows - row0) * ld * 2));
+#pragma unroll
+    for (int i = 0; i < NI; ++i) dma16_buf(rs, voff[i], 0u, &lds[(wave * NI + i) * 64]);
+  }
+};
+
 // Fragment of row `row`, 16-byte chunk `chunk` (8 consecutive columns).
 template <int D>
 __device__ __forceinline__ bf16x8 tfrag_row(const uint4* lds, int row, int chunk) {
@@ -425,6 +450,8 @@ __device__ __forceinline__ void dkdv_waves(const FaArgs& a, uint4* sQ, uint4* sO
   for (int i = 0; i < C::DB; ++i) acc[i] = fa::zero16();
   fa::TrOffsets<D> tro;
   tro.init(lane);
+  fa::TileCopy<D> tcp;
+  tcp.init(ROLE == 0 ? (int64_t)D : (int64_t)a.Hq * D, ks, lane);
   const int qt0 = k0 / fa::BK;
   const int nqt = (a.S + fa::BK - 1) / fa::BK;
   // P of this slab and a tile's 64 queries: [2 x 32-query blocks][4][64
@@ -441,9 +468,9 @@ __device__ __forceinline__ void dkdv_waves(const FaArgs& a, uint4* sQ, uint4* sO
     // this wave's share of the copies of tile q0n into buffer buf
     auto issue = [&](int buf, int q0n) {
       if (ROLE == 0)
-        fa::dma_tile<D>(Qb, D, q0n, a.S, sQ + buf * TW, ks, lane);
+        tcp.issue(Qb, D, q0n, a.S, sQ + buf * TW, ks);
       else
-        fa::dma_tile<D>(dOb, (int64_t)a.Hq * D, q0n, a.S, sO + buf * TW, ks, lane);
+        tcp.issue(dOb, (int64_t)a.Hq * D, q0n, a.S, sO + buf * TW, ks);
       if (ks == 0) dma4_buf(ld_rs, (uint32_t)(q0n + lane) * 4u, (ROLE == 0 ? sL : sD) + buf * 64);
     };
     // the first tile's copies; a tile's buffers are refilled only after the
@@ -510,6 +537,12 @@ __device__ __forceinline__ void dkdv_waves(const FaArgs& a, uint4* sQ, uint4* sO
               *reinterpret_cast<f32x4*>(P + ((qb * 4 + c) * 64 + lane) * 4) = v;
             }
           }
+        } else {
+          // dP - D while the dV waves form P
+#pragma unroll
+          for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) s[qb][r] -= tD[qb * 32 + fa::acc_row(r, g)];
         }
       }
       __syncthreads();
@@ -522,11 +555,7 @@ __device__ __forceinline__ void dkdv_waves(const FaArgs& a, uint4* sQ, uint4* sO
             for (int c = 0; c < 4; ++c) {
               const f32x4 pv = *reinterpret_cast<const f32x4*>(P + ((qb * 4 + c) * 64 + lane) * 4);
 #pragma unroll
-              for (int e = 0; e < 4; ++e) {
-                const int r = 4 * c + e;
-                const int qi = qb * 32 + fa::acc_row(r, g);
-                s[qb][r] = pv[e] * (s[qb][r] - tD[qi]);
-              }
+              for (int e = 0; e < 4; ++e) s[qb][4 * c + e] *= pv[e];
             }
         }
         // dV[key][d] += P^T dO ; dK[key][d] += dS^T Q  (contraction over the
@@ -568,8 +597,12 @@ __global__ __launch_bounds__(DKDV_NT, 2) void flash_bwd_dkdv_kernel(FaArgs a) {
   __shared__ uint4 sO[2 * TW];  // dO tiles
   __shared__ __attribute__((aligned(16))) float sL[2 * 64], sD[2 * 64];
   __shared__ __attribute__((aligned(16))) float sP[4 * 2 * 16 * 64];  // P handed from dV to dK waves
-  if (__builtin_amdgcn_readfirstlane(threadIdx.x >> 6) < 4)
+  if (__builtin_amdgcn_readfirstlane(threadIdx.x >> 6) < 4) {
+    // the dV waves issue first: their score chains end early and their
+    // exponentials overlap the dK waves' products
+    __builtin_amdgcn_s_setprio(1);
     dkdv_waves<D, 0>(a, sQ, sO, sL, sD, sP);
+  }
   else
     dkdv_waves<D, 1>(a, sQ, sO, sL, sD, sP);
 }
