@@ -11,8 +11,9 @@ BlockCalibrator runs it: K steps on the Eq. 6 schedule (step k at t = k/K:
 softened ternarisation with s = (t/0.8)*30 while t <= 0.8, the hard quantiser
 with the backward at s0 = 30 after), each step being LM+ST of all seven
 weights, block forward with the fake-ternary weights, reconstruction loss
-against the cached full-precision output, backward to the input and to every
-group's three factors, and one AdamW update of the factors; the group
+against the cached full-precision output, backward through the block to every
+group's three factors (the block input is fixed calibration data: its gradient
+is not formed), and one AdamW update of the factors; the group
 statistics are computed at the first step (the weights are frozen) and the
 final hard ternarisation with 2-bit packing of every weight runs once after
 the last step.  K = 10 is the 10-step calibration of the workload.  The

@@ -284,14 +284,18 @@ class DenseBlock:
             self._act = self.a8
 
     # --------------------------------------------------------------- backward
-    def backward(self, x, p, overlap=True, dy=None, join=True):
+    def backward(self, x, p, overlap=True, dy=None, join=True, input_grad=True):
         """Backward to the block input and to every factor.  With ``overlap``
         each linear's weight-gradient half (G = dY^T X and the factor
         gradients) runs on the side stream as soon as dY is ready, while the
         main stream carries on with dX and the glue; the main stream waits
         for the side stream at the end (unless ``join`` is false: a window
         of blocks joins once, after its first block).  ``dy`` is the
-        gradient of the block output (default: the loss's, in self.dy)."""
+        gradient of the block output (default: the loss's, in self.dy).
+        ``input_grad`` false skips the gradient of the block input (self.dx):
+        the factors' gradients do not need it when the input is fixed data
+        (a calibrated block, or the first block of a window), so the q|k|v
+        projection runs its weight-gradient half only."""
         c, M = self.cfg, self.M
         h = c.hidden
         ws = self.lin_ws
@@ -311,6 +315,15 @@ class DenseBlock:
                                       L.d_alpha, L.d_delta, p, L.g_mu, L.g_alpha, L.g_delta, ws)
             catq_fakeq_linear_bwd(dY, X, L.W_fake, M, L.d_out, L.d_in, L.W, L.stats, L.d_mu,
                                   L.d_alpha, L.d_delta, p, None, None, None, None, dX=dX)
+
+        def lbwd_weights(name, dY, X):
+            # the weight-gradient half alone (on the side stream with overlap)
+            L = self.lin[name]
+            if side is not None:
+                self.order(name, main, side)
+            with torch.cuda.stream(side if side is not None else main):
+                catq_fakeq_linear_bwd(dY, X, L.W_fake, M, L.d_out, L.d_in, L.W, L.stats, L.d_mu,
+                                      L.d_alpha, L.d_delta, p, L.g_mu, L.g_alpha, L.g_delta, ws)
 
         dy = self.dy if dy is None else dy
         if self.fuse_swiglu:
@@ -332,18 +345,22 @@ class DenseBlock:
         lbwd("o", self.dh1, self.o_in, self.dattn)
         catq_aux_attention_bwd(self.fwd_desc, self.qkv, self.attn, self.saved, self.dattn,
                                self.dqkv, self.attn_ws)
-        lbwd("qkv", self.dqkv, self.xn1, self.dxn1)
-        catq_aux_rmsnorm_bwd(x, self.rstd1, self.dxn1, self.dx, dres=self.dh1)
+        if input_grad:
+            lbwd("qkv", self.dqkv, self.xn1, self.dxn1)
+            catq_aux_rmsnorm_bwd(x, self.rstd1, self.dxn1, self.dx, dres=self.dh1)
+        else:
+            lbwd_weights("qkv", self.dqkv, self.xn1)
         if side is not None and join:
             self.order("join", side, main)
 
     # ------------------------------------------------------------------- step
     def step(self, x, y_fp, mode=SOFT, s=15.0, s_bwd=30.0, recompute_stats=False, overlap=True,
-             finalize=None):
+             finalize=None, input_grad=True):
         """LM+ST -> forward -> loss -> backward.  Loss stays on the device.
         ``finalize`` (buffers from finalize_buffers) also runs the hard
         ternarisation + packing, on the side stream once LM+ST has the
-        statistics (it reads only W, the statistics and the factors)."""
+        statistics (it reads only W, the statistics and the factors).
+        ``input_grad`` false leaves self.dx unwritten (see backward)."""
         p = self.params(mode, s, s_bwd)
         self.modulate_all(p, recompute_stats)
         if finalize is not None:
@@ -355,7 +372,7 @@ class DenseBlock:
                 self.finalize(finalize)
         self.forward(x)
         catq_block_recon_loss(self.y, y_fp, self.loss, self.dy, self.loss_ws)
-        self.backward(x, p, overlap)
+        self.backward(x, p, overlap, input_grad=input_grad)
         if finalize is not None and overlap:
             self.order("finalize_join", self.side_stream(), torch.cuda.current_stream())
         return self.loss
@@ -514,7 +531,7 @@ class MoEBlock:
         self.modulate_all(self.params(IDENTITY))
         return self.forward(x, out)
 
-    def backward(self, x, p, overlap=True, dy=None, join=True):
+    def backward(self, x, p, overlap=True, dy=None, join=True, input_grad=True):
         """As DenseBlock.backward, with the routed-expert MLP half."""
         c, M, R = self.cfg, self.M, self.R
         h, E, F, k = c.hidden, c.n_experts, c.expert_ffn, c.top_k
@@ -548,8 +565,17 @@ class MoEBlock:
         lbwd("o", self.dh1, self.attn, self.dattn, M)
         catq_aux_attention_bwd(self.desc, self.qkv, self.attn, self.saved, self.dattn, self.dqkv,
                                self.attn_ws)
-        lbwd("qkv", self.dqkv, self.xn1, self.dxn1, M)
-        catq_aux_rmsnorm_bwd(x, self.rstd1, self.dxn1, self.dx, dres=self.dh1)
+        if input_grad:
+            lbwd("qkv", self.dqkv, self.xn1, self.dxn1, M)
+            catq_aux_rmsnorm_bwd(x, self.rstd1, self.dxn1, self.dx, dres=self.dh1)
+        else:
+            L = self.lin["qkv"]
+            if side is not None:
+                self.order("qkv", main, side)
+            with torch.cuda.stream(side if side is not None else main):
+                catq_fakeq_linear_bwd(self.dqkv, self.xn1, L.W_fake, M, L.d_out, L.d_in, L.W,
+                                      L.stats, L.d_mu, L.d_alpha, L.d_delta, p, L.g_mu,
+                                      L.g_alpha, L.g_delta, ws)
         if side is not None and join:
             self.order("join", side, main)
 

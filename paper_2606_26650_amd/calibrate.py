@@ -89,8 +89,10 @@ class BlockCalibrator:
         """One pass over the calibration set at this epoch's time state."""
         mode, s = time_state(self.epoch, self.n_epochs, self.gamma, self.s0)
         for b in range(self.n_batches):
+            # the calibration input is fixed data: no gradient of the block input
             loss = self.blk.step(self.batch(b), self.targets[b], mode=mode, s=s, s_bwd=self.s0,
-                                 recompute_stats=self.step_no == 0, overlap=self.overlap)
+                                 recompute_stats=self.step_no == 0, overlap=self.overlap,
+                                 input_grad=False)
             self.losses.append(loss.clone())
             self.step_no += 1
             lr = linear_lr(self.step_no - 1, self.total_steps, self.lr0)

@@ -105,11 +105,13 @@ class Window:
         return [b.finalize(f) for b, f in zip(self.blocks, bufs)]
 
     def step(self, x, y_fp, mode=SOFT, s=15.0, s_bwd=30.0, recompute_stats=False, overlap=True,
-             finalize=None):
+             finalize=None, input_grad=True):
         """LM+ST of every block -> window forward -> Eq. 7 loss -> backward
         through the blocks in reverse.  Loss stays on the device.
         ``finalize`` (buffers from finalize_buffers) also runs every block's
-        hard ternarisation + packing, on the side stream after LM+ST."""
+        hard ternarisation + packing, on the side stream after LM+ST.
+        ``input_grad`` false skips the gradient of the window input (the
+        first block's dx); the later blocks' input gradients are always formed."""
         p = self.params(mode, s, s_bwd)
         self.modulate_all(p, recompute_stats)
         main = torch.cuda.current_stream()
@@ -127,7 +129,8 @@ class Window:
         n = len(self.blocks)
         for i in range(n - 1, -1, -1):
             dy = None if i == n - 1 else self.blocks[i + 1].dx
-            self.blocks[i].backward(ins[i], p, overlap, dy=dy, join=(i == 0))
+            self.blocks[i].backward(ins[i], p, overlap, dy=dy, join=(i == 0),
+                                    input_grad=input_grad or i > 0)
         if finalize is not None and overlap:
             b0.order("window_finalize_join", b0.side_stream(), main)
         return last.loss

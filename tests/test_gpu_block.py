@@ -216,6 +216,40 @@ def test_overlapped_step_matches_serial(catq, kind):
     assert torch.equal(a[3], b[3]) and torch.equal(a[4], b[4])
 
 
+@pytest.mark.parametrize("kind", ["dense", "moe"])
+@pytest.mark.parametrize("overlap", [False, True])
+def test_step_without_input_gradient(catq, kind, overlap):
+    """A calibrated block's input is fixed data, so the calibration skips
+    the gradient of the block input (Eq. 7 optimises only the factors): the
+    loss and every factor gradient are bit for bit those of the full step,
+    and the input-gradient buffer is left untouched."""
+    import torch
+    if kind == "dense":
+        cfg = sg.small_dense(batch=2, seq=128, hidden=256, n_q=4, n_kv=2, head_dim=64, ffn=384)
+        blk, _, _, xb = _dense_setup(cfg)
+    else:
+        cfg = sg.small_moe(batch=1, seq=96, hidden=256, n_q=4, n_kv=2, head_dim=64, n_experts=8,
+                           top_k=2, expert_ffn=128, router_bias_std=1.0)
+        blk, _, _, xb, _ = _moe_setup(cfg)
+    x = to_dev_bf16(xb)
+    y_fp = blk.new_output()
+    blk.target(x, y_fp)
+    out = []
+    for input_grad in (True, False):
+        blk.dx.fill_(7.0)
+        l = blk.step(x, y_fp, mode=lmst.SOFT, s=15.0, overlap=overlap,
+                     input_grad=input_grad).clone()
+        torch.cuda.synchronize()
+        out.append((l, blk.dx.clone(), [t.clone() for L in blk.lin.values()
+                                        for t in (L.g_mu, L.g_alpha, L.g_delta)]))
+    (la, dxa, ga), (lb, dxb, gb) = out
+    assert torch.equal(la, lb)
+    for u, v in zip(ga, gb):
+        assert torch.equal(u, v)
+    assert not torch.all(dxa == 7.0)
+    assert torch.all(dxb == 7.0)
+
+
 def test_full_size_block_properties(catq):
     """The 1.7B-shaped block at its real size (4 x 2048 tokens): identity
     branch gives loss 0, soft step gives a finite positive loss and finite
