@@ -681,13 +681,31 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
     if (MORE) interleave();
   };
   const int nk = (int)((ke - kb + 63) / 64);
+  // factor epilogue: the weights of a staged part (lane: row lane / 4 of
+  // the part, 16 consecutive columns), loaded one part ahead; the first
+  // part's during the last k tile
+  [[maybe_unused]] uint2 epw[4];
+  [[maybe_unused]] auto epi3_load = [&](int p) {
+    if constexpr (EPI == 3) {
+      constexpr int HP3 = 2, SR3 = 16;
+      const int64_t mrow = m0 + wm * WTM + (p / HP3) * 32 + (p % HP3) * SR3;
+      const int64_t wrow = (int64_t)z * g.M + min(mrow + (lane >> 2), m_lim - 1);
+      const bf16* wsrc = reinterpret_cast<const bf16*>(g.fac.W) + wrow * g.N + n0 + wn * WTN +
+                         (lane & 3) * 16;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) epw[q] = raw4(wsrc + 4 * q);
+    }
+  };
   if (nk > 0) {
     issue(0, kb);
     wait_vmem();
     __syncthreads();
     ldfrag(0, 0, 0);
     for (int kt = 0; kt < nk - 1; ++kt) tile(kt, std::true_type{});
+    if constexpr (EPI == 3) epi3_load(0);
     tile(nk - 1, std::false_type{});
+  } else if constexpr (EPI == 3) {
+    epi3_load(0);
   }
   OutT* C = reinterpret_cast<OutT*>(g.C) + c_off;
   const RT* R = HAS_R ? reinterpret_cast<const RT*>(g.R) : nullptr;
@@ -741,11 +759,94 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
         }
       }
     };
-    // (the factor epilogue holds too many registers to load ahead: there
-    // each part loads its own weights first)
+    if constexpr (EPI == 3) {
+      // Factor epilogue.  Lane l takes row l / 4 of each staged part and 16
+      // consecutive columns, 16 (l % 4) .. +15 of the wave's 64 (which lie in
+      // one half of a 128-weight group), over four 4-column passes: the row's
+      // group scalars are the lane's own, its 16 weights arrive in four 8-byte
+      // loads, and the four terms of the factor gradients are summed over the
+      // lane's 16 weights, then over the row's 4 lanes.  G[m][n] of expert z,
+      // or of the one dense problem (z = 0), unsplit, alpha 1.
+      static_assert(WTN == 64 && SR == 16 && HP == 2 && NW * 64 == 16 * 64,
+                    "factor epilogue lane map");
+      const FacEpi& F = g.fac;
+      const int rr = lane >> 2, cq = (lane & 3) * 16;
+      const int64_t ncol = n0 + wn * WTN + cq;
+#pragma unroll
+      for (int p = 0; p < PARTS; ++p) {
+        const int i = p / HP, h = p % HP;
+        const int64_t mrow = m0 + wm * WTM + i * 32 + h * SR;
+        const int64_t m_c = min(mrow + rr, m_lim - 1);
+        const int64_t wrow = (int64_t)z * g.M + m_c;
+        uint2 wv[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) wv[q] = epw[q];
+        if (p + 1 < PARTS) epi3_load(p + 1);
+        const int64_t grp = wrow * (g.N >> 7) + (ncol >> 7);
+        const GroupScalars gs = group_scalars(F.stats[2 * grp], F.stats[2 * grp + 1],
+                                              F.dmu[grp * F.s[0]], F.dal[grp * F.s[1]],
+                                              F.dde[grp * F.s[2]], F.delta0);
+        // the part's accumulator slab through this wave's staging area
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int row = 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+            if (row / SR == h) st[(row - h * SR) * EP + j * 32 + (lane & 31)] = acc[i][j][r];
+          }
+        float sT = 0.f, s1 = 0.f, sW = 0.f, sD = 0.f;
+        if (mrow + rr < m_lim && F.mode != CATQ_IDENTITY) {
+          const float mu = gs.mu, inv_a = __builtin_amdgcn_rcpf(gs.alpha_div);
+          const float dz = gs.delta * F.st.c2s;
+          const float ed = one_minus_exp_neg(gs.delta * F.st.s4, gs.delta * F.st.s4l);
+          HardThresh th = {0.0, 0.f, 0.f};
+          if (F.mode == CATQ_HARD) th = hard_thresh(gs.delta, gs.alpha_div);
+#pragma unroll 1
+          for (int q = 0; q < 4; ++q) {
+            const f32x4 v = *reinterpret_cast<const f32x4*>(st + rr * EP + cq + 4 * q);
+            const uint2 wq = q == 0 ? wv[0] : (q == 1 ? wv[1] : (q == 2 ? wv[2] : wv[3]));
+            const f32x4 w = widen4(wq);
+            float hc[4];
+            if (F.mode == CATQ_HARD) {
+              const float w4[4] = {w[0], w[1], w[2], w[3]};
+              hard_codes_n<4>(w4, mu, th, hc);
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const float xs = (w[e] - mu) * inv_a;
+              float fp = 0.f, fwp = 1.f, fdp = 0.f;
+              if (!F.ste) transition_parts_z(xs, F.st.c2s, dz, ed, fp, fwp, fdp);
+              const float T = (F.mode == CATQ_HARD) ? hc[e] : fp;
+              sT = fmaf(v[e], T, sT);
+              const float gf = v[e] * fwp;
+              s1 += gf;
+              sW = fmaf(gf, xs, sW);
+              sD = fmaf(v[e], fdp, sD);
+            }
+          }
+        }
+#pragma unroll
+        for (int mk = 1; mk < 4; mk <<= 1) {
+          sT += __shfl_xor(sT, mk, 64);
+          s1 += __shfl_xor(s1, mk, 64);
+          sW += __shfl_xor(sW, mk, 64);
+          sD += __shfl_xor(sD, mk, 64);
+        }
+        if ((lane & 3) == 0) {
+          // [tile row][wave column block = quarter of the tile][term]; the
+          // row's 64 columns of this wave are half of one group
+          float* d = fsum + ((int)(mrow - m0 + rr) * 4 + wn) * 4;
+          d[0] = sT;
+          d[1] = s1;
+          d[2] = sW;
+          d[3] = sD;
+        }
+      }
+    }
+    // (the factor epilogue has its own loop above)
     if constexpr (EPI != 3) load_part(0, 0);
 #pragma unroll
-    for (int p = 0; p < PARTS; ++p) {
+    for (int p = 0; p < (EPI == 3 ? 0 : PARTS); ++p) {
       const int i = p / HP, h = p % HP;
       {
         const int64_t mrow = m0 + wm * WTM + i * 32 + h * SR;
@@ -883,7 +984,10 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
       for (int t = tid; t < BM * 2; t += NW * 64) {
         const int row = t >> 1, gt = t & 1;
         const float* a0 = fsum + (row * 4 + 2 * gt) * 4;
-        const float sT = a0[0] + a0[4], s1 = a0[1] + a0[5], sW = a0[2] + a0[6], sD = a0[3] + a0[7];
+        // the constant factors of f (k2, soft only), f_W and f_Delta (sk4)
+        const FacScale k = fac_scale(F.mode, F.ste, F.st);
+        const float sT = (a0[0] + a0[4]) * k.f, s1 = (a0[1] + a0[5]) * k.w;
+        const float sW = (a0[2] + a0[6]) * k.w, sD = (a0[3] + a0[7]) * k.d;
         const int64_t grp = ((int64_t)z * g.M + m0 + row) * (g.N >> 7) + (n0 >> 7) + gt;
         const float alpha0 = F.stats[2 * grp + 1];
         const GroupScalars gs = group_scalars(F.stats[2 * grp], alpha0, F.dmu[grp * F.s[0]],

@@ -339,26 +339,27 @@ __global__ __launch_bounds__(256) void lmst_bwd_kernel(BwdArgs a) {
   float ST = 0.f, SW = 0.f, S1 = 0.f, SD = 0.f;
   if (a.mode != CATQ_IDENTITY) {
     const float inv_a = 1.0f / gs.alpha_div;
+    const float dz = gs.delta * a.st.c2s;
     const float ED = one_minus_exp_neg(gs.delta * a.st.s4, gs.delta * a.st.s4l);
     float hc[8];
     if (a.mode == CATQ_HARD) hard_codes8(w, gs.mu, hard_thresh(gs.delta, gs.alpha_div), hc);
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       float xs = (w[j] - gs.mu) * inv_a;
-      float f, fW, fD;
+      float fp, fwp, fdp;
       if (a.ste) {
-        fW = 1.0f;
-        fD = 0.0f;
-        f = 0.0f;
+        fwp = 1.0f;
+        fdp = 0.0f;
+        fp = 0.0f;
       } else {
-        transition_parts(xs, gs.delta, ED, a.st, f, fW, fD);
+        transition_parts_z(xs, a.st.c2s, dz, ED, fp, fwp, fdp);
       }
-      float T = (a.mode == CATQ_HARD) ? hc[j] : f;
+      float T = (a.mode == CATQ_HARD) ? hc[j] : fp;
       ST = fmaf(G[j], T, ST);
-      float gf = G[j] * fW;
+      float gf = G[j] * fwp;
       S1 += gf;
       SW = fmaf(gf, xs, SW);
-      SD = fmaf(G[j], fD, SD);
+      SD = fmaf(G[j], fdp, SD);
     }
   }
   for (int m = L >> 1; m >= 1; m >>= 1) {
@@ -368,6 +369,12 @@ __global__ __launch_bounds__(256) void lmst_bwd_kernel(BwdArgs a) {
     SD += __shfl_xor(SD, m, 64);
   }
   if (lane_in_g == 0) {
+    // the constant factors of f (k2, soft only), f_W and f_Delta (sk4)
+    const FacScale k = fac_scale(a.mode, a.ste, a.st);
+    S1 *= k.w;
+    SW *= k.w;
+    SD *= k.d;
+    ST *= k.f;
     float v[3];
     v[0] = alpha0 * (-S1);
     v[1] = alpha0 * (ST - SW);

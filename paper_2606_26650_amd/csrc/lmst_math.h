@@ -197,6 +197,46 @@ __device__ __forceinline__ float transition_f(float xs, float delta, float ED, c
   return copysignf(F, xs);
 }
 
+// f, f_W and f_Delta without their constant factors, in the base-2 exponent
+// domain of soft_value: with z = xs * c2s (c2s = 2 s log2 e), y = |z|,
+// dz = Delta * c2s and ed = E_Delta,
+//   f = k2 * fp,   f_W = sk4 * fwp,   f_Delta = sk4 * fdp,
+// 1/(1 + q_a) and 1/(1 + q_b) from one reciprocal of their product.  The
+// factor-gradient sums apply k2 and sk4 once per group.
+__device__ __forceinline__ void transition_parts_z(float xs, float c2s, float dz, float ed,
+                                                   float& fp, float& fwp, float& fdp) {
+  const float z = xs * c2s;
+  const float y = fabsf(z);
+  const float d = y - dz;
+  const float qa = __builtin_amdgcn_exp2f(-fabsf(d));
+  const float T = __builtin_amdgcn_exp2f(-(y + y));
+  const float E = one_minus_exp2_neg2(y, T);
+  const bool ge = d >= 0.0f;
+  const float eb = ge ? ed : E;
+  const float qb = fmaf(-qa, eb, qa);
+  const float opa = 1.0f + qa, opb = 1.0f + qb;
+  const float rden = __builtin_amdgcn_rcpf(opa * opb);
+  const float num = ge ? E : qa * E;
+  fp = copysignf(num * rden, xs);
+  const float ra = opb * rden, rb = opa * rden;  // 1/(1 + q_a), 1/(1 + q_b)
+  fwp = fmaf(qa * ra, ra, (qb * rb) * rb);
+  const float om = ge ? E : ed;  // 1 - q_a q_b / ... (see transition_parts)
+  fdp = copysignf((qa * eb) * om * (rden * rden), -xs);
+}
+
+// Scales of the per-group sums of transition_parts_z: f is the hard code
+// (HARD, no scale) or k2 fp; f_W is 1 under the straight-through estimator.
+struct FacScale {
+  float f, w, d;
+};
+__device__ __forceinline__ FacScale fac_scale(int mode, int ste, const StConst& c) {
+  FacScale k;
+  k.f = (mode == CATQ_SOFT) ? c.k2 : 1.0f;
+  k.w = ste ? 1.0f : c.sk4;
+  k.d = c.sk4;
+  return k;
+}
+
 // f, f_W and f_Delta together (backward).
 __device__ __forceinline__ void transition_parts(float xs, float delta, float ED, const StConst& c,
                                                  float& f, float& fW, float& fD) {
