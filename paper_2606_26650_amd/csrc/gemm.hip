@@ -781,7 +781,6 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
         uint2 wv[4];
 #pragma unroll
         for (int q = 0; q < 4; ++q) wv[q] = epw[q];
-        if (p + 1 < PARTS) epi3_load(p + 1);
         const int64_t grp = wrow * (g.N >> 7) + (ncol >> 7);
         const GroupScalars gs = group_scalars(F.stats[2 * grp], F.stats[2 * grp + 1],
                                               F.dmu[grp * F.s[0]], F.dal[grp * F.s[1]],
@@ -794,35 +793,46 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
             const int row = 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
             if (row / SR == h) st[(row - h * SR) * EP + j * 32 + (lane & 31)] = acc[i][j][r];
           }
+        // the next part's weights, in flight while this part is processed
+        if (p + 1 < PARTS) epi3_load(p + 1);
         float sT = 0.f, s1 = 0.f, sW = 0.f, sD = 0.f;
         if (mrow + rr < m_lim && F.mode != CATQ_IDENTITY) {
           const float mu = gs.mu, inv_a = __builtin_amdgcn_rcpf(gs.alpha_div);
           const float dz = gs.delta * F.st.c2s;
           const float ed = one_minus_exp_neg(gs.delta * F.st.s4, gs.delta * F.st.s4l);
-          HardThresh th = {0.0, 0.f, 0.f};
-          if (F.mode == CATQ_HARD) th = hard_thresh(gs.delta, gs.alpha_div);
-#pragma unroll 1
-          for (int q = 0; q < 4; ++q) {
+          // one pass: 4 weights (rotated into wv[0]) against 4 G values
+          auto pass = [&](int q, auto hard_c) {
+            constexpr bool HARD = decltype(hard_c)::value;
             const f32x4 v = *reinterpret_cast<const f32x4*>(st + rr * EP + cq + 4 * q);
-            const uint2 wq = q == 0 ? wv[0] : (q == 1 ? wv[1] : (q == 2 ? wv[2] : wv[3]));
-            const f32x4 w = widen4(wq);
+            const f32x4 w = widen4(wv[0]);
+            // the next pass's weights into wv[0] (registers rotated: no
+            // dynamically indexed array)
+            wv[0] = wv[1];
+            wv[1] = wv[2];
+            wv[2] = wv[3];
             float hc[4];
-            if (F.mode == CATQ_HARD) {
+            if constexpr (HARD) {
               const float w4[4] = {w[0], w[1], w[2], w[3]};
-              hard_codes_n<4>(w4, mu, th, hc);
+              hard_codes_n<4>(w4, mu, hard_thresh(gs.delta, gs.alpha_div), hc);
             }
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
               const float xs = (w[e] - mu) * inv_a;
               float fp = 0.f, fwp = 1.f, fdp = 0.f;
               if (!F.ste) transition_parts_z(xs, F.st.c2s, dz, ed, fp, fwp, fdp);
-              const float T = (F.mode == CATQ_HARD) ? hc[e] : fp;
-              sT = fmaf(v[e], T, sT);
+              sT = fmaf(v[e], HARD ? hc[e] : fp, sT);
               const float gf = v[e] * fwp;
               s1 += gf;
               sW = fmaf(gf, xs, sW);
               sD = fmaf(v[e], fdp, sD);
             }
+          };
+          if (F.mode == CATQ_HARD) {
+#pragma unroll 1
+            for (int q = 0; q < 4; ++q) pass(q, std::true_type{});
+          } else {
+#pragma unroll 1
+            for (int q = 0; q < 4; ++q) pass(q, std::false_type{});
           }
         }
 #pragma unroll
