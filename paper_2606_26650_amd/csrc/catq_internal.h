@@ -210,6 +210,15 @@ __device__ __forceinline__ void dma4_buf(i32x4_rsrc rsrc, uint32_t voff, const v
 }
 #pragma clang diagnostic pop
 
+// wait until at most N vector memory operations of this wave are in flight
+// (loads complete in issue order: the N newest may still be outstanding)
+template <int N>
+__device__ __forceinline__ void wait_vmem_n() {
+#if defined(__HIP_DEVICE_COMPILE__)
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+#endif
+}
+
 __device__ __forceinline__ void wait_vmem() {
 #if defined(__HIP_DEVICE_COMPILE__)
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");

@@ -550,7 +550,7 @@ __device__ __forceinline__ bool group_tile(const int64_t* off, int E, int t, int
 }
 
 template <int BM, int BN, int WGM, int WGN, bool AKM, bool BKM, typename OutT, typename RT,
-          bool HAS_R, int EPI = 0>
+          bool HAS_R, int EPI = 0, int SB = 2>
 __global__ __launch_bounds__(WGM* WGN * 64, 1)
     __attribute__((amdgpu_waves_per_eu(1, (WGM * WGN + 3) / 4))) void gemm_dma_kernel(GemmLaunch L) {
 #if defined(__HIP_DEVICE_COMPILE__)
@@ -560,10 +560,13 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
   static_assert(FM >= 1 && FN >= 1 && FM * FN >= FM + FN, "bad tile");
   using OA = std::conditional_t<AKM, DmaOpKM<BM, NW>, DmaOpNT<BM, NW>>;
   using OB = std::conditional_t<BKM, DmaOpKM<BN, NW>, DmaOpNT<BN, NW>>;
-  // one LDS allocation: the two stages of A, then the two of B (the
-  // epilogue stages the output through all of it)
+  // one LDS allocation: the two stages of A, then the SB of B (the epilogue
+  // stages the output through the first two stages' worth of it).  SB = 3
+  // puts B's copies two k tiles ahead, for B streamed from HBM once (a large
+  // weight, or an expert's weight used by one row tile)
+  static_assert(SB == 2 || SB == 3, "two or three B stages");
   constexpr int LDS_SLOTS = 2 * (BM + BN) * 8;
-  __shared__ uint4 smem[LDS_SLOTS];
+  __shared__ uint4 smem[(2 * BM + SB * BN) * 8];
   auto sA = [&](int buf) { return smem + buf * (BM * 8); };
   auto sB = [&](int buf) { return smem + 2 * BM * 8 + buf * (BN * 8); };
   const GemmArgs& g = L.g;
@@ -622,16 +625,14 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
   else
     ob.init(Bb, g.ldb, n0, g.N, wave, lane);
   bf16x8 fa[2][FM], fb[2][FN];
-  auto ldfrag = [&](int buf, int kk, int slot) {
+  auto ldfrag = [&](int kt, int kk, int slot) {
 #pragma unroll
-    for (int i = 0; i < FM; ++i) fa[slot][i] = oa.frag(sA(buf), wm * WTM + 32 * i, kk, lane);
+    for (int i = 0; i < FM; ++i) fa[slot][i] = oa.frag(sA(kt & 1), wm * WTM + 32 * i, kk, lane);
 #pragma unroll
-    for (int j = 0; j < FN; ++j) fb[slot][j] = ob.frag(sB(buf), wn * WTN + 32 * j, kk, lane);
+    for (int j = 0; j < FN; ++j) fb[slot][j] = ob.frag(sB(kt % SB), wn * WTN + 32 * j, kk, lane);
   };
-  auto issue = [&](int buf, int64_t k0) {
-    oa.issue(sA(buf), g.lda, k0, ke, wave);
-    ob.issue(sB(buf), g.ldb, k0, ke, wave);
-  };
+  auto issueA = [&](int kt) { oa.issue(sA(kt & 1), g.lda, kb + (int64_t)kt * 64, ke, wave); };
+  auto issueB = [&](int kt) { ob.issue(sB(kt % SB), g.ldb, kb + (int64_t)kt * 64, ke, wave); };
   f32x16 acc[FM][FN];
 #pragma unroll
   for (int i = 0; i < FM; ++i)
@@ -664,23 +665,31 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
   // interleaved, barrier, then sub-step 3 overlapped with the next tile's
   // first reads.  MORE is false only for the last tile (no branches inside
   // the steady-state body, so the interleaving spans it whole).
+  const int nk = (int)((ke - kb + 63) / 64);
   auto tile = [&](int kt, auto more_c) {
     constexpr bool MORE = decltype(more_c)::value;
-    const int buf = kt & 1;
-    if (MORE) issue(buf ^ 1, kb + (int64_t)(kt + 1) * 64);
+    // copies of tile kt+1 (A; and B with two stages) or kt+2 (B, three
+    // stages) into the stages tile kt-1 used; B's copies are issued last, so
+    // with three stages waiting for all but B's newest finishes tile kt+1
+    if (MORE) issueA(kt + 1);
+    if (SB == 2 && MORE) issueB(kt + 1);
+    const bool deep = SB == 3 && kt + 2 < nk;
+    if (deep) issueB(kt + 2);
 #pragma unroll
     for (int kk = 0; kk < 3; ++kk) {
-      ldfrag(buf, kk + 1, (kk & 1) ^ 1);
+      ldfrag(kt, kk + 1, (kk & 1) ^ 1);
       mfmas(kk & 1);
       interleave();
     }
-    wait_vmem();
+    if (deep)
+      wait_vmem_n<OB::NI>();
+    else
+      wait_vmem();
     __syncthreads();
-    if (MORE) ldfrag(buf ^ 1, 0, 0);
+    if (MORE) ldfrag(kt + 1, 0, 0);
     mfmas(1);
     if (MORE) interleave();
   };
-  const int nk = (int)((ke - kb + 63) / 64);
   // factor epilogue: the weights of a staged part (lane: row lane / 4 of
   // the part, 16 consecutive columns), loaded one part ahead; the first
   // part's during the last k tile
@@ -697,8 +706,14 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
     }
   };
   if (nk > 0) {
-    issue(0, kb);
-    wait_vmem();
+    issueA(0);
+    issueB(0);
+    if (SB == 3 && nk > 1) {
+      issueB(1);
+      wait_vmem_n<OB::NI>();
+    } else {
+      wait_vmem();
+    }
     __syncthreads();
     ldfrag(0, 0, 0);
     for (int kt = 0; kt < nk - 1; ++kt) tile(kt, std::true_type{});
@@ -1151,7 +1166,7 @@ static void launch_cfg(GemmLaunch& L, hipStream_t stream) {
 }
 
 template <int BM, int BN, int WGM, int WGN, bool AKM, bool BKM, typename OutT, typename RT,
-          int EPI = 0>
+          int EPI = 0, int SB = 2>
 static void launch_dma(GemmLaunch& L, hipStream_t stream) {
   const GemmArgs& g = L.g;
   // grouped rows: at most ceil(M/BM) + E m-tiles over all experts together
@@ -1160,11 +1175,11 @@ static void launch_dma(GemmLaunch& L, hipStream_t stream) {
   dim3 grid((unsigned)(L.tiles_m * L.tiles_n * (g.group_mode == 2 ? g.n_groups : L.ksplit)));
   dim3 block(WGM * WGN * 64);
   char tag[112];
-  std::snprintf(tag, sizeof(tag), "gemm_dma_kernel<%d, %d, %d, %d, %s%s, %s, %s, %s%s%s>", BM, BN,
-                WGM, WGN, AKM ? "k" : "n", BKM ? "k" : "t", tname<OutT>(), tname<RT>(),
+  std::snprintf(tag, sizeof(tag), "gemm_dma_kernel<%d, %d, %d, %d, %s%s, %s, %s, %s%s%s%s>", BM,
+                BN, WGM, WGN, AKM ? "k" : "n", BKM ? "k" : "t", tname<OutT>(), tname<RT>(),
                 g.R ? "true" : "false",
                 EPI == 1 ? ", swiglu" : (EPI == 2 ? ", swiglu_bwd" : (EPI == 3 ? ", factor_grads" : "")),
-                g.group_mode ? ", experts" : "");
+                g.group_mode ? ", experts" : "", SB == 3 ? ", 3 B stages" : "");
   double flops, bytes;
   gemm_work(L, (int)sizeof(OutT), flops, bytes);
   if (EPI == 1) bytes += (double)g.M * (double)(g.N / 2) * 2.0;          // a written
@@ -1175,11 +1190,11 @@ static void launch_dma(GemmLaunch& L, hipStream_t stream) {
   }
   if (g.R)
     CATQ_TRACED(stream, tag, flops, bytes, g.M, g.N, g.K,
-                hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WGM, WGN, AKM, BKM, OutT, RT, true, EPI>),
+                hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WGM, WGN, AKM, BKM, OutT, RT, true, EPI, SB>),
                                    grid, block, 0, stream, L));
   else
     CATQ_TRACED(stream, tag, flops, bytes, g.M, g.N, g.K,
-                hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WGM, WGN, AKM, BKM, OutT, RT, false, EPI>),
+                hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WGM, WGN, AKM, BKM, OutT, RT, false, EPI, SB>),
                                    grid, block, 0, stream, L));
 }
 
@@ -1205,8 +1220,15 @@ static void launch_bf16(GemmLaunch& L, hipStream_t stream) {
   if (g.group_mode == 1 && g.N >= 256 && dma_ok(L, A_T, B_T, 256, 256)) {
     // routed experts' rows: 256-row tiles on 16 waves, although each
     // expert's last tile is partly empty (with ~256 rows per expert, 128-row
-    // tiles on 8 waves waste less but measured 25% slower)
-    launch_dma<256, 256, 4, 4, A_T == 1, B_T == 1, OutT, RT>(L, stream);
+    // tiles on 8 waves waste less but measured 25% slower).  In the forward
+    // each expert's weight streams from HBM for about one row tile: three B
+    // stages (copies two k tiles ahead; bit-identical; on the 235B-A22B-
+    // shaped gate|up experts 1.17 -> 0.98 ms alone, 1.10 -> 1.09 ms in the
+    // calibration step)
+    if (A_T == 0 && B_T == 0)
+      launch_dma<256, 256, 4, 4, false, false, OutT, RT, 0, 3>(L, stream);
+    else
+      launch_dma<256, 256, 4, 4, A_T == 1, B_T == 1, OutT, RT>(L, stream);
     return;
   }
   if (g.group_mode == 2 && dma_ok(L, A_T, B_T, 256, 256)) {
@@ -1316,7 +1338,13 @@ catq_status gemm_run_epi(const GemmArgs& a, int a_t, int b_t, hipStream_t stream
     // A [M][K] tokens (K-contiguous), B the fused weight [N][K]
     if (!(shape && a_t == 0 && b_t == 0 && a.M >= 256 && a.N >= 256 && dma_ok(L, 0, 0, 256, 256)))
       return CATQ_ERR_VALUE;
-    launch_dma<256, 256, 4, 4, false, false, bf16, bf16, 1>(L, stream);
+    // a weight of more than 128 MB streams from HBM: three B stages
+    // (bit-identical; 2.47 -> 2.39 ms on the 14B-shaped gate|up in the
+    // calibration step)
+    if ((double)a.N * (double)a.K * 2.0 > 128.0 * (1 << 20))
+      launch_dma<256, 256, 4, 4, false, false, bf16, bf16, 1, 3>(L, stream);
+    else
+      launch_dma<256, 256, 4, 4, false, false, bf16, bf16, 1>(L, stream);
   } else {
     // dX-shaped: A = dY [M][K] (K-contiguous), B = W_fake [K][N] (K-major)
     if (!(shape && a_t == 0 && b_t == 1 && a.M >= 256 && a.N >= 256 && dma_ok(L, 0, 1, 256, 256)))
