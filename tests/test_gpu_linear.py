@@ -297,6 +297,30 @@ def test_full_size_qkv_gemm_sampled(catq):
     assert np.all(np.abs(got - ref) <= 2.0 ** -8 * np.abs(ref) + 1e-3 * np.abs(ref).max())
 
 
+def test_streamed_weight_fwd_sampled(catq):
+    """Forward product whose weight exceeds 128 MB (the down projection of
+    the 14B-shaped block, ragged in both output extents: 2011 x 5080 over
+    17408 inputs), fp32 output with an fp32 residual: sampled outputs, the
+    last row and column included, against float64 dot products."""
+    import torch
+    M, N, K = 2011, 5080, 17408
+    xb, wb = _xw(11, M, N, K)
+    r = sg.bf16_bits_to_f32(sg.normal_bf16(12, "Y", (M, N)))
+    X, W, R = to_dev_bf16(xb), to_dev_bf16(wb), to_dev_f32(r)
+    Y = torch.empty(M, N, dtype=torch.float32, device="cuda")
+    catq.catq_fakeq_linear_fwd(X, W, Y, M, N, K, residual=R)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(1)
+    mi = np.concatenate([rng.integers(0, M, 4096), [M - 1] * 64, np.arange(64)])
+    ni = np.concatenate([rng.integers(0, N, 4096), np.arange(64), [N - 1] * 64])
+    Xo, Wo = f64(xb[mi]), f64(wb[ni])
+    ref = np.einsum("ij,ij->i", Xo, Wo) + r[mi, ni]
+    mag = np.einsum("ij,ij->i", np.abs(Xo), np.abs(Wo))
+    got = host(Y)[mi, ni]
+    # fp32 accumulation of exact bf16 products over 17408 terms
+    assert np.all(np.abs(got - ref) <= 2.0 ** -14 * mag + 2.0 ** -20 * np.abs(ref))
+
+
 def test_full_size_dw_gemm_sampled(catq):
     """Weight gradient of the down projection at full size (G = dY^T X over
     8192 tokens, N=2048, K=6144) on sampled entries; exercises split-K."""
