@@ -19,9 +19,10 @@ final hard ternarisation with 2-bit packing of every weight runs once after
 the last step.  K = 10 is the 10-step calibration of the workload.  The
 full-precision target is computed before timing (it does not change during
 calibration); inputs are resident in HBM when the timed region starts.  The
-step runs on two streams: each linear's weight-gradient half (G = dY^T X and
-the factor gradients) goes to a side stream and overlaps the input-gradient
-chain (--no-overlap: one stream).
+step runs on the block's default schedule: one stream for a dense block, two
+for a routed-expert block, where each linear's weight-gradient half (G =
+dY^T X and the factor gradients) goes to a side stream and overlaps the
+input-gradient chain (--overlap, --no-overlap: force two streams or one).
 
 Prints one JSON line.  ``value`` = K / (timed seconds), in block-steps/s.  A
 kernel pass then repeats the same calibration on one stream with a HIP event
@@ -57,9 +58,13 @@ def parse():
     ap.add_argument("--copy-gib", type=float, default=0.0,
                     help="only run a plain device copy of this size (counter calibration)")
     ap.add_argument("--breakdown", action="store_true", help="print the per-kernel table")
-    ap.add_argument("--no-overlap", action="store_true",
-                    help="run the step on one stream (no side stream for the weight-gradient "
-                         "halves and the finalize)")
+    sched = ap.add_mutually_exclusive_group()
+    sched.add_argument("--no-overlap", action="store_true",
+                       help="run the step on one stream (no side stream for the weight-gradient "
+                            "halves and the finalize)")
+    sched.add_argument("--overlap", action="store_true",
+                       help="run the step on two streams (weight-gradient halves and the "
+                            "finalize on a side stream)")
     ap.add_argument("--ternary", type=int, default=0, metavar="M",
                     help="only time the packed-ternary decode layers of a Qwen3-14B-shaped "
                          "block at M tokens (deployment on the 2-bit storage)")
@@ -348,7 +353,9 @@ def main():
     from paper_2606_26650_amd.calibrate import BlockCalibrator
     x = bf16_tensor(xb)
     # the full-precision target is computed here, once (not timed)
-    cal = BlockCalibrator(blk, x, args.steps, overlap=not args.no_overlap)
+    cal = BlockCalibrator(blk, x, args.steps,
+                          overlap=True if args.overlap else (False if args.no_overlap else None))
+    overlap = cal.overlap
     # the final ternarisation writes the 2-bit storage directly (no int8 codes)
     fin = blk.finalize_buffers(codes=False)
 
@@ -361,7 +368,7 @@ def main():
 
     for _ in range(args.warmup):
         blk.step(x, cal.targets[0], mode=cq.SOFT, s=15.0, s_bwd=30.0,
-                 overlap=not args.no_overlap)
+                 overlap=overlap)
     torch.cuda.synchronize()
     # timed pass: the production schedule, no per-launch instrumentation
     t0 = time.perf_counter()
@@ -438,7 +445,7 @@ def main():
             "flops_per_launch": dom["flops"] / dom["n"],
             "traffic": counted_traffic(dom_tag, key),
         },
-        "schedule": ("two streams" if not args.no_overlap else "one stream") +
+        "schedule": ("two streams" if overlap else "one stream") +
                     ", launches issued per step",
         "kernel_pass": {"ms_per_step": kernel_pass_ms, "streams": 1, "steps": args.steps,
                         "instrumented": "HIP event pair per launch"},

@@ -141,6 +141,12 @@ class DenseBlock:
     """Pre-norm decoder block (RMSNorm, fused q|k|v, QK-norm, RoPE, causal GQA
     attention, o, residual, RMSNorm, fused gate|up, SwiGLU, down, residual)."""
 
+    # Schedule of a step when the caller names none: one stream.  Every
+    # product of a dense block fills the chip on its own, and two of them at
+    # once on two streams share the caches and ran the calibration step
+    # 1-3% slower (14B- and 1.7B-shaped blocks).
+    overlap_default = False
+
     def __init__(self, cfg, weights: dict, g: int = 128, a8: bool = False):
         """a8: the W1.58A8 setting -- the inputs of the four linears and Q, K,
         V of the attention products are fake-quantized to 8 bits in the
@@ -354,13 +360,17 @@ class DenseBlock:
             self.order("join", side, main)
 
     # ------------------------------------------------------------------- step
-    def step(self, x, y_fp, mode=SOFT, s=15.0, s_bwd=30.0, recompute_stats=False, overlap=True,
+    def step(self, x, y_fp, mode=SOFT, s=15.0, s_bwd=30.0, recompute_stats=False, overlap=None,
              finalize=None, input_grad=True):
         """LM+ST -> forward -> loss -> backward.  Loss stays on the device.
-        ``finalize`` (buffers from finalize_buffers) also runs the hard
-        ternarisation + packing, on the side stream once LM+ST has the
-        statistics (it reads only W, the statistics and the factors).
-        ``input_grad`` false leaves self.dx unwritten (see backward)."""
+        ``overlap`` (None: the block's overlap_default) puts the
+        weight-gradient halves on the side stream.  ``finalize`` (buffers
+        from finalize_buffers) also runs the hard ternarisation + packing,
+        on the side stream (with overlap) once LM+ST has the statistics (it
+        reads only W, the statistics and the factors).  ``input_grad`` false
+        leaves self.dx unwritten (see backward)."""
+        if overlap is None:
+            overlap = self.overlap_default
         p = self.params(mode, s, s_bwd)
         self.modulate_all(p, recompute_stats)
         if finalize is not None:
@@ -431,6 +441,12 @@ class DenseBlock:
 class MoEBlock:
     """Decoder block whose MLP routes every token to its top-k experts (router
     logits given, left unquantised); attention half as in DenseBlock."""
+
+    # Two streams by default: the experts' weight-gradient products, with the
+    # factor gradients in their vector-bound epilogues, overlap the
+    # input-gradient chain (about 1% faster than one stream on the
+    # 235B-A22B-shaped block, even and skewed expert loads).
+    overlap_default = True
 
     def __init__(self, cfg, weights: dict, logits: np.ndarray, g: int = 128):
         self.cfg = c = cfg
@@ -599,8 +615,8 @@ class MoEBlock:
 
 
 class StepGraph:
-    """One calibration step (both streams) captured as a HIP graph and
-    replayed: the step's ~35 launches then cost one graph launch.  Inputs
+    """One calibration step (on one stream or both, as ``step_kw`` asks)
+    captured as a HIP graph and replayed: the step's ~35 launches then cost one graph launch.  Inputs
     and outputs are the captured buffers: change them in place between
     replays (the factors are updated in place by the optimiser).  The step
     is run once eagerly first, so the side stream, the events and the

@@ -54,9 +54,11 @@ class BlockCalibrator:
     are computed once (identity branch) and kept on the device."""
 
     def __init__(self, block, x_all: torch.Tensor, n_epochs: int, gamma: float = 0.8,
-                 s0: float = 30.0, lr0: float = 1e-3, overlap: bool = True):
+                 s0: float = 30.0, lr0: float = 1e-3, overlap: bool | None = None):
         self.blk = block
-        self.overlap = overlap    # the step's side stream (see the block drivers)
+        # the step's side stream (see the block drivers); None: the driver's
+        # overlap_default
+        self.overlap = block.overlap_default if overlap is None else overlap
         cfg = block.cfg
         self.tok_per_batch = cfg.batch * cfg.seq
         if x_all.shape[0] % self.tok_per_batch:

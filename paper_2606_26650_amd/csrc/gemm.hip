@@ -1214,6 +1214,19 @@ static bool dma_ok(const GemmLaunch& L, int a_t, int b_t, int bm, int bn) {
          (b_t == 0 || g.N % bn == 0);
 }
 
+// A dense product on 256 x 256 tiles.  A forward product whose weight (B,
+// K-contiguous) exceeds 128 MB streams it from HBM: three B stages
+// (bit-identical; the 14B-shaped down projection with its residual, 1.42 ->
+// 1.38 ms in the calibration step).
+template <int A_T, int B_T, typename OutT, typename RT>
+static void launch_dense256(GemmLaunch& L, hipStream_t stream) {
+  const GemmArgs& g = L.g;
+  if (A_T == 0 && B_T == 0 && L.ksplit <= 1 && (double)g.N * (double)g.K * 2.0 > 128.0 * (1 << 20))
+    launch_dma<256, 256, 4, 4, false, false, OutT, RT, 0, 3>(L, stream);
+  else
+    launch_dma<256, 256, 4, 4, A_T == 1, B_T == 1, OutT, RT>(L, stream);
+}
+
 template <int A_T, int B_T, typename OutT, typename RT>
 static void launch_bf16(GemmLaunch& L, hipStream_t stream) {
   const GemmArgs& g = L.g;
@@ -1241,16 +1254,38 @@ static void launch_bf16(GemmLaunch& L, hipStream_t stream) {
   const int64_t t256 = ((g.M + 255) / 256) * ((g.N + 255) / 256) * L.ksplit;
   if (g.group_mode == 0 && g.M >= 256 && g.N >= 256 && t256 >= 160 &&
       dma_ok(L, A_T, B_T, 256, 256)) {
-    // a forward product whose weight (B, K-contiguous) exceeds 128 MB streams
-    // it from HBM: three B stages (bit-identical; the 14B-shaped down
-    // projection with its residual, 1.42 -> 1.38 ms in the calibration step)
-    if constexpr (A_T == 0 && B_T == 0) {
-      if (L.ksplit <= 1 && (double)g.N * (double)g.K * 2.0 > 128.0 * (1 << 20)) {
-        launch_dma<256, 256, 4, 4, false, false, OutT, RT, 0, 3>(L, stream);
-        return;
+    // One workgroup of the 256 x 256 kernel fills a compute unit, so a last
+    // round of a quarter to three quarters of the 256 units leaves the rest
+    // idle (8192 x 5120 outputs: 640 tiles, 2.5 rounds).  Then the columns
+    // past the last whole round go to the 128 x 128 kernel as a launch of
+    // their own (two workgroups per unit, one round at most).  Both kernels
+    // accumulate an output over K in the same order, so the bits do not
+    // change; in the 14B-shaped calibration step the five such products
+    // take 0.45 ms less.
+    if (L.ksplit <= 1) {
+      const int tm = (int)((g.M + 255) / 256), tn = (int)((g.N + 255) / 256);
+      const int rem = (tm * tn) % 256;
+      int h = 0;  // column tiles of the head: the most that make whole rounds
+      if (rem >= 64 && rem <= 192)
+        for (int c = tn - 1; c >= 1 && h == 0; --c)
+          if ((tm * c) % 256 == 0) h = c;
+      if (h > 0) {
+        const int64_t nh = (int64_t)h * 256;
+        GemmLaunch H = L, T = L;
+        H.g.N = nh;
+        T.g.N = g.N - nh;
+        T.g.B = reinterpret_cast<const bf16*>(g.B) + (B_T ? nh : nh * g.ldb);
+        T.g.C = reinterpret_cast<OutT*>(g.C) + nh;
+        if (g.R) T.g.R = reinterpret_cast<const RT*>(g.R) + nh;
+        const int64_t t128 = ((g.M + 127) / 128) * ((T.g.N + 127) / 128);
+        if (t128 <= 512 && dma_ok(T, A_T, B_T, 128, 128)) {
+          launch_dense256<A_T, B_T, OutT, RT>(H, stream);
+          launch_dma<128, 128, 2, 2, A_T == 1, B_T == 1, OutT, RT>(T, stream);
+          return;
+        }
       }
     }
-    launch_dma<256, 256, 4, 4, A_T == 1, B_T == 1, OutT, RT>(L, stream);
+    launch_dense256<A_T, B_T, OutT, RT>(L, stream);
     return;
   }
   if (g.group_mode == 0 && dma_ok(L, A_T, B_T, 128, 128)) {

@@ -104,14 +104,22 @@ class Window:
         """Hard codes, group scales and 2-bit packing of every block."""
         return [b.finalize(f) for b, f in zip(self.blocks, bufs)]
 
-    def step(self, x, y_fp, mode=SOFT, s=15.0, s_bwd=30.0, recompute_stats=False, overlap=True,
+    @property
+    def overlap_default(self):
+        """The step's default schedule: that of the window's blocks."""
+        return self.blocks[0].overlap_default
+
+    def step(self, x, y_fp, mode=SOFT, s=15.0, s_bwd=30.0, recompute_stats=False, overlap=None,
              finalize=None, input_grad=True):
         """LM+ST of every block -> window forward -> Eq. 7 loss -> backward
         through the blocks in reverse.  Loss stays on the device.
         ``finalize`` (buffers from finalize_buffers) also runs every block's
         hard ternarisation + packing, on the side stream after LM+ST.
         ``input_grad`` false skips the gradient of the window input (the
-        first block's dx); the later blocks' input gradients are always formed."""
+        first block's dx); the later blocks' input gradients are always formed.
+        ``overlap`` None takes overlap_default."""
+        if overlap is None:
+            overlap = self.overlap_default
         p = self.params(mode, s, s_bwd)
         self.modulate_all(p, recompute_stats)
         main = torch.cuda.current_stream()

@@ -1,4 +1,4 @@
-"""The calibration step captured as a HIP graph (both streams) and replayed:
+"""The calibration step captured as a HIP graph (one stream, or both) and replayed:
 every replay equals the eager step bit for bit, also after other eager work
 has reused the same buffers in between (the captured kernels must not depend
 on state that only the capture saw)."""
@@ -18,8 +18,8 @@ def _outputs(blk, fin):
             [fin["_flat"]["packed"].clone(), fin["_flat"]["alpha"].clone()])
 
 
-@pytest.mark.parametrize("kind", ["dense", "moe"])
-def test_graph_replays_match_eager(catq, kind):
+@pytest.mark.parametrize("kind,overlap", [("dense", False), ("dense", True), ("moe", True)])
+def test_graph_replays_match_eager(catq, kind, overlap):
     import torch
     from paper_2606_26650_amd.block import DenseBlock, MoEBlock, StepGraph
     if kind == "dense":
@@ -35,14 +35,15 @@ def test_graph_replays_match_eager(catq, kind):
     y_fp = blk.new_output()
     blk.target(x, y_fp)
     fin = blk.finalize_buffers()
-    kw = dict(mode=lmst.SOFT, s=15.0, s_bwd=30.0, recompute_stats=True, finalize=fin)
+    kw = dict(mode=lmst.SOFT, s=15.0, s_bwd=30.0, recompute_stats=True, finalize=fin,
+              overlap=overlap)
     blk.step(x, y_fp, **kw)
     torch.cuda.synchronize()
     ref = _outputs(blk, fin)
     g = StepGraph(blk, x, y_fp, **kw)
     for r in range(3):
         # other eager work on the same buffers between replays
-        blk.step(x, y_fp, mode=lmst.HARD, s_bwd=30.0)
+        blk.step(x, y_fp, mode=lmst.HARD, s_bwd=30.0, overlap=overlap)
         torch.cuda.synchronize()
         g.replay()
         torch.cuda.synchronize()
@@ -60,7 +61,7 @@ def test_graph_replay_of_a_window(catq):
     x = to_dev_bf16(sg.activations(cfg, 0))
     y_fp = win.new_output()
     win.target(x, y_fp)
-    kw = dict(mode=lmst.SOFT, s=7.5, s_bwd=30.0)
+    kw = dict(mode=lmst.SOFT, s=7.5, s_bwd=30.0, overlap=True)
     win.step(x, y_fp, **kw)
     torch.cuda.synchronize()
     ref = [win.loss.clone(), win.dx.clone().view(torch.int16)] + \

@@ -321,6 +321,40 @@ def test_streamed_weight_fwd_sampled(catq):
     assert np.all(np.abs(got - ref) <= 2.0 ** -14 * mag + 2.0 ** -20 * np.abs(ref))
 
 
+@pytest.mark.parametrize("out_f32", [False, True])
+def test_partial_last_round_split(catq, out_f32):
+    """8192 x 5120 outputs are 640 tiles of 256 x 256, 2.5 rounds of the 256
+    compute units: the columns past the second round run as a 128 x 128
+    launch of their own.  The whole output against float64 (with a residual
+    in the fp32 case), and the split-off columns bit for bit against the
+    same columns from an unsplit launch (the weight's rows 1024.., 512 tiles,
+    whole rounds)."""
+    import torch
+    M, N, K = 8192, 5120, 192
+    xb, wb = _xw(13, M, N, K)
+    X, W = to_dev_bf16(xb), to_dev_bf16(wb)
+    dt = torch.float32 if out_f32 else torch.bfloat16
+    rb = sg.normal_bf16(14, "Y", (M, N)) if out_f32 else None
+    R = to_dev_bf16(rb) if out_f32 else None
+    Y = torch.empty(M, N, dtype=dt, device="cuda")
+    catq.catq_fakeq_linear_fwd(X, W, Y, M, N, K, residual=R)
+    Y2 = torch.empty(M, N - 1024, dtype=dt, device="cuda")
+    catq.catq_fakeq_linear_fwd(X, W[1024:].contiguous(), Y2, M, N - 1024, K,
+                               residual=R[:, 1024:].contiguous() if out_f32 else None)
+    torch.cuda.synchronize()
+    assert torch.equal(Y[:, 4096:], Y2[:, 3072:])
+    ref = f64(xb) @ f64(wb).T
+    if out_f32:
+        ref += f64(rb)
+    assert max_norm_err(host(Y), ref) <= (1e-5 if out_f32 else 4e-3)
+
+
+def test_partial_last_round_split_dx(catq):
+    """The input gradient of a 256 -> 5120 linear over 8192 tokens (8192 x
+    5120 outputs, K-major weight): split as the forward above."""
+    _bwd_case(catq, 8192, 256, 5120, catq.SOFT)
+
+
 def test_full_size_dw_gemm_sampled(catq):
     """Weight gradient of the down projection at full size (G = dY^T X over
     8192 tokens, N=2048, K=6144) on sampled entries; exercises split-K."""
