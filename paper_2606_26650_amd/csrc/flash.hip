@@ -273,94 +273,128 @@ __global__ __launch_bounds__(fa::NT, 2) void flash_fwd_kernel(FaArgs a) {
   const int wave_first = q0 + 32 * w, wave_last = wave_first + 31;
   fa::TrOffsets<D> tro;
   tro.init(lane);
-  auto issue = [&](int buf, int k0) {
-    fa::dma_tile<D>(Kb, D, k0, a.S, sK[buf], w, lane);
-    fa::dma_tile<D>(Vb, D, k0, a.S, sV[buf], w, lane);
+  // K and V rows by buffer copies (one set of lane offsets for both; rows
+  // past the sequence read as zero, their keys are masked)
+  fa::TileCopy<D> tcp;
+  tcp.init(D, w, lane);
+  auto issueK = [&](int buf, int k0) { tcp.issue(Kb, D, k0, a.S, sK[buf], w); };
+  auto issueV = [&](int buf, int k0) { tcp.issue(Vb, D, k0, a.S, sV[buf], w); };
+  // S^T of one key tile (K rows in `kl`) for the two 32-key blocks: two
+  // independent accumulation chains, each fragment read one step ahead of
+  // its products
+  auto scores = [&](const uint4* kl, f32x16 (&s)[2]) {
+    s[0] = fa::zero16();
+    s[1] = fa::zero16();
+    bf16x8 fr[2][2];
+    fr[0][0] = fa::tfrag_row<D>(kl, l32, g);
+    fr[0][1] = fa::tfrag_row<D>(kl, 32 + l32, g);
+#pragma unroll
+    for (int t = 0; t < C::KS; ++t) {
+      if (t + 1 < C::KS) {
+        fr[(t + 1) & 1][0] = fa::tfrag_row<D>(kl, l32, 2 * (t + 1) + g);
+        fr[(t + 1) & 1][1] = fa::tfrag_row<D>(kl, 32 + l32, 2 * (t + 1) + g);
+      }
+      s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[t & 1][0], qf[t], s[0], 0, 0, 0);
+      s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[t & 1][1], qf[t], s[1], 0, 0, 0);
+    }
   };
-  issue(0, 0);
+  // Online softmax of one (masked) score tile, first half: the tile max of
+  // the raw scores (the scale c > 0 commutes with it), the new running max
+  // (msafe: 0 for a lane whose query lies past the sequence end, which sees
+  // only masked keys) and the rescale factor of the old sums.  alpha == 1
+  // exactly unless the running max moved: O is rescaled only when it moved
+  // for some lane of the wave.
+  auto tile_max = [&](f32x16 (&s)[2], float& msafe, float& alpha) {
+    float mt = -INFINITY;
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[sb][r]);
+    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+    const float mn = fmaxf(m, mt * a.c);
+    msafe = (mn == -INFINITY) ? 0.f : mn;
+    alpha = __builtin_amdgcn_exp2f(m - msafe);
+    const bool moved = mn != m;
+    m = mn;
+    if (__any(moved)) {
+#pragma unroll
+      for (int i = 0; i < C::DB; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[i][r] *= alpha;
+    }
+  };
+  // second half: P = 2^(c s - m), packed as the bf16 operand of the
+  // products, O^T += V^T P^T (V^T fragments by transpose reads of the V rows
+  // in `vl`), l = alpha l + rowsum P
+  auto accumulate = [&](f32x16 (&s)[2], const uint4* vl, float msafe, float alpha) {
+    float rs = 0.f;
+    bf16x8 pk[4];
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float p = __builtin_amdgcn_exp2f(fmaf(s[sb][r], a.c, -msafe));
+        s[sb][r] = p;
+        rs += p;
+      }
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) pk[2 * sb + hh] = fa::pack8(s[sb], hh);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int i = 0; i < C::DB; ++i)
+        o[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa::tr_read<D>(vl, tro, i, j), pk[j], o[i], 0,
+                                                       0, 0);
+    rs += __shfl_xor(rs, 32, 64);
+    l = l * alpha + rs;
+  };
+
+  // Software pipeline over key tiles: K runs one tile ahead of V, so while
+  // the exponentials of tile kt run on the vector ALUs the scores of tile
+  // kt+1 go to the matrix cores.  Prologue: K and V of tile 0, K of tile 1,
+  // the scores of tile 0 (every wave reads tile 0: wave_last >= 31).
+  issueK(0, 0);
+  issueV(0, 0);
+  if (nkt > 1) issueK(1, fa::BK);
   wait_vmem();
+  __syncthreads();
+  f32x16 sc[2];
+  scores(sK[0], sc);
+  // every wave has read K of tile 0 before tile 2 takes its buffer
   __syncthreads();
   for (int kt = 0; kt < nkt; ++kt) {
     const int k0 = kt * fa::BK, buf = kt & 1;
-    // the next tile lands in the buffer every wave finished reading before
-    // the previous barrier
-    if (kt + 1 < nkt) issue(buf ^ 1, k0 + fa::BK);
+    // V of tile kt+1 into the buffer V of tile kt-1 left, K of tile kt+2
+    // into that of tile kt (both read before the previous barrier)
+    if (kt + 1 < nkt) issueV(buf ^ 1, k0 + fa::BK);
+    if (kt + 2 < nkt) issueK(buf, k0 + 2 * fa::BK);
     if (k0 <= wave_last) {
-      // S^T for the two 32-key blocks: two independent accumulation chains,
-      // each fragment read one step ahead of its products
-      f32x16 s[2];
-      s[0] = fa::zero16();
-      s[1] = fa::zero16();
-      {
-        bf16x8 fr[2][2];
-        fr[0][0] = fa::tfrag_row<D>(sK[buf], l32, g);
-        fr[0][1] = fa::tfrag_row<D>(sK[buf], 32 + l32, g);
-#pragma unroll
-        for (int t = 0; t < C::KS; ++t) {
-          if (t + 1 < C::KS) {
-            fr[(t + 1) & 1][0] = fa::tfrag_row<D>(sK[buf], l32, 2 * (t + 1) + g);
-            fr[(t + 1) & 1][1] = fa::tfrag_row<D>(sK[buf], 32 + l32, 2 * (t + 1) + g);
-          }
-          s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[t & 1][0], qf[t], s[0], 0, 0, 0);
-          s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[t & 1][1], qf[t], s[1], 0, 0, 0);
-        }
-      }
-      // causal / length mask, only on tiles that cross the wave's diagonal or
-      // the sequence end; then the tile max of the raw scores (the scale c > 0
-      // commutes with the max)
-      float mt = -INFINITY;
-      if (k0 + fa::BK - 1 > wave_first || k0 + fa::BK > a.S) {
+      // A tile followed by another of the same wave lies wholly below the
+      // wave's diagonal and inside the sequence (the next tile starts at or
+      // before wave_last < S; tile starts are multiples of 64, wave starts
+      // of 32): only the wave's last tile may need the causal / length mask.
+      const bool next = kt + 1 < nkt && k0 + fa::BK <= wave_last;
+      if (!next && (k0 + fa::BK - 1 > wave_first || k0 + fa::BK > a.S)) {
 #pragma unroll
         for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int key = k0 + sb * 32 + fa::acc_row(r, g);
-            if (key > qme || key >= a.S) s[sb][r] = -INFINITY;
-            mt = fmaxf(mt, s[sb][r]);
+            if (key > qme || key >= a.S) sc[sb][r] = -INFINITY;
           }
-      } else {
-#pragma unroll
-        for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[sb][r]);
       }
-      mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-      const float mn = fmaxf(m, mt * a.c);
-      // a lane whose query lies past the sequence end sees only masked keys
-      const float msafe = (mn == -INFINITY) ? 0.f : mn;
-      const float alpha = __builtin_amdgcn_exp2f(m - msafe);
-      // alpha == 1 exactly unless the running max moved: skip the rescale when
-      // it moved for no lane of the wave
-      if (__any(mn != m)) {
-#pragma unroll
-        for (int i = 0; i < C::DB; ++i)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) o[i][r] *= alpha;
-      }
-      m = mn;
-      // per 32-key block: P, then O^T += V^T P^T (V^T fragments by transpose
-      // reads of the V rows); the exponentials of the second block are
-      // independent of the first block's products and can overlap them
-      float rs = 0.f;
-#pragma unroll
-      for (int sb = 0; sb < 2; ++sb) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float p = __builtin_amdgcn_exp2f(fmaf(s[sb][r], a.c, -msafe));
-          s[sb][r] = p;
-          rs += p;
-        }
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const bf16x8 pf = fa::pack8(s[sb], hh);
-#pragma unroll
-          for (int i = 0; i < C::DB; ++i)
-            o[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                fa::tr_read<D>(sV[buf], tro, i, 2 * sb + hh), pf, o[i], 0, 0, 0);
-        }
-      }
-      rs += __shfl_xor(rs, 32, 64);
-      l = l * alpha + rs;
+      float msafe, alpha;
+      tile_max(sc, msafe, alpha);
+      // One basic block: the next tile's scores beside this tile's
+      // exponentials, then this tile's products.  On the wave's last tile
+      // the scores read the other K buffer (a stale tile, or none filled
+      // since) and are discarded: the wave skips every later tile.
+      f32x16 sn[2];
+      scores(sK[buf ^ 1], sn);
+      accumulate(sc, sV[buf], msafe, alpha);
+      sc[0] = sn[0];
+      sc[1] = sn[1];
     }
     wait_vmem();
     __syncthreads();
