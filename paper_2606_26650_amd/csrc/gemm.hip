@@ -699,8 +699,8 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
       constexpr int HP3 = 2, SR3 = 16;
       const int64_t mrow = m0 + wm * WTM + (p / HP3) * 32 + (p % HP3) * SR3;
       const int64_t wrow = (int64_t)z * g.M + min(mrow + (lane >> 2), m_lim - 1);
-      const bf16* wsrc = reinterpret_cast<const bf16*>(g.fac.W) + wrow * g.N + n0 + wn * WTN +
-                         (lane & 3) * 16;
+      const bf16* wsrc = reinterpret_cast<const bf16*>(g.fac.W) + wrow * g.fac.ldw + n0 +
+                         wn * WTN + (lane & 3) * 16;
 #pragma unroll
       for (int q = 0; q < 4; ++q) epw[q] = raw4(wsrc + 4 * q);
     }
@@ -736,15 +736,17 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
     constexpr int EP = WTN + 8;
     constexpr int LPR = WTN / 4, RPP = 64 / LPR;  // lanes per row, rows per pass
     // rows staged per LDS round trip: the whole 32-row slab when every wave's
-    // share fits in the operand buffers, else half of it (16 waves)
-    constexpr int SR = (NW * 32 * EP * 4 <= LDS_SLOTS * 16) ? 32 : 16;
+    // share fits in the operand buffers, else half of it (16 waves; and the
+    // factor epilogue, whose lane map takes 16-row parts)
+    constexpr int SR = (EPI != 3 && NW * 32 * EP * 4 <= LDS_SLOTS * 16) ? 32 : 16;
     constexpr int NP = SR / RPP;                  // passes per staged part
     static_assert(NW * SR * EP * 4 <= LDS_SLOTS * 16, "epilogue staging");
     float* st = reinterpret_cast<float*>(smem) + wave * (SR * EP);
     // factor epilogue: the half-group sums of every tile row, past the staging
+    // ([tile row][wave column block][term]; a 64-column block is half a group)
     [[maybe_unused]] float* fsum = reinterpret_cast<float*>(smem) + NW * SR * EP;
-    static_assert(EPI != 3 || (BN == 256 && WTN == 64 &&
-                               (NW * SR * EP + BM * 4 * 4) * 4 <= LDS_SLOTS * 16),
+    static_assert(EPI != 3 || (BN % 128 == 0 && WTN == 64 &&
+                               (NW * SR * EP + BM * WGN * 4) * 4 <= LDS_SLOTS * 16),
                   "factor epilogue layout");
     const int cc = (lane % LPR) * 4;
     const int64_t n = n0 + wn * WTN + cc;
@@ -768,9 +770,6 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
           uvb[slot][q] = raw4(gu + g.N + n_c);
         } else if constexpr (EPI == 0 && HAS_R) {
           rvb[slot][q] = raw4(R + m_c * g.ldr + n_c);
-        } else if constexpr (EPI == 3) {
-          gvb[slot][q] = raw4(reinterpret_cast<const bf16*>(g.fac.W) +
-                              ((int64_t)z * g.M + m_c) * g.N + n_c);
         }
       }
     };
@@ -782,8 +781,7 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
       // loads, and the four terms of the factor gradients are summed over the
       // lane's 16 weights, then over the row's 4 lanes.  G[m][n] of expert z,
       // or of the one dense problem (z = 0), unsplit, alpha 1.
-      static_assert(WTN == 64 && SR == 16 && HP == 2 && NW * 64 == 16 * 64,
-                    "factor epilogue lane map");
+      static_assert(WTN == 64 && SR == 16 && HP == 2, "factor epilogue lane map");
       const FacEpi& F = g.fac;
       const int rr = lane >> 2, cq = (lane & 3) * 16;
       const int64_t ncol = n0 + wn * WTN + cq;
@@ -796,7 +794,7 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
         uint2 wv[4];
 #pragma unroll
         for (int q = 0; q < 4; ++q) wv[q] = epw[q];
-        const int64_t grp = wrow * (g.N >> 7) + (ncol >> 7);
+        const int64_t grp = wrow * (F.ldw >> 7) + (ncol >> 7);
         const GroupScalars gs = group_scalars(F.stats[2 * grp], F.stats[2 * grp + 1],
                                               F.dmu[grp * F.s[0]], F.dal[grp * F.s[1]],
                                               F.dde[grp * F.s[2]], F.delta0);
@@ -858,9 +856,9 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
           sD += __shfl_xor(sD, mk, 64);
         }
         if ((lane & 3) == 0) {
-          // [tile row][wave column block = quarter of the tile][term]; the
-          // row's 64 columns of this wave are half of one group
-          float* d = fsum + ((int)(mrow - m0 + rr) * 4 + wn) * 4;
+          // [tile row][wave column block][term]; the row's 64 columns of
+          // this wave are half of one group
+          float* d = fsum + ((int)(mrow - m0 + rr) * WGN + wn) * 4;
           d[0] = sT;
           d[1] = s1;
           d[2] = sW;
@@ -875,31 +873,10 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
       const int i = p / HP, h = p % HP;
       {
         const int64_t mrow = m0 + wm * WTM + i * 32 + h * SR;
-        if constexpr (EPI == 3)
-          load_part(p, p & 1);
-        else if (p + 1 < PARTS)
-          load_part(p + 1, (p + 1) & 1);
+        if (p + 1 < PARTS) load_part(p + 1, (p + 1) & 1);
         [[maybe_unused]] auto& rv = rvb[p & 1];
         [[maybe_unused]] auto& gv = gvb[p & 1];
         [[maybe_unused]] auto& uv = uvb[p & 1];
-        // factor epilogue: lane l holds the group scalars of the part's row
-        // l % SR (its 64 columns lie in one group), handed to the lanes of
-        // that row by shuffles in each pass
-        [[maybe_unused]] float p_mu = 0.f, p_inva = 0.f, p_delta = 0.f, p_ed = 0.f;
-        [[maybe_unused]] HardThresh p_th = {0.0, 0.f, 0.f};
-        if constexpr (EPI == 3) {
-          const FacEpi& F = g.fac;
-          const int64_t wrow = (int64_t)z * g.M + min(mrow + (lane % SR), m_lim - 1);
-          const int64_t grp = wrow * (g.N >> 7) + (n_c >> 7);
-          const GroupScalars gs =
-              group_scalars(F.stats[2 * grp], F.stats[2 * grp + 1], F.dmu[grp * F.s[0]],
-                            F.dal[grp * F.s[1]], F.dde[grp * F.s[2]], F.delta0);
-          p_mu = gs.mu;
-          p_inva = 1.0f / gs.alpha_div;
-          p_delta = gs.delta;
-          p_ed = one_minus_exp_neg(gs.delta * F.st.s4, gs.delta * F.st.s4l);
-          p_th = hard_thresh(gs.delta, gs.alpha_div);
-        }
 #pragma unroll
         for (int j = 0; j < FN; ++j)
 #pragma unroll
@@ -912,58 +889,6 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
           const int rr = q * RPP + lane / LPR;
           const int64_t m = mrow + rr;
           f32x4 v = *reinterpret_cast<const f32x4*>(st + rr * EP + cc);
-          if constexpr (EPI == 3) {
-            // G[m][n..n+3] of expert z, or of the one dense problem (z = 0),
-            // unsplit, alpha 1: the four terms of the factor gradients over
-            // these weights, summed over the 16 lanes of the row's 64
-            // columns (half of a 128-weight group)
-            const FacEpi& F = g.fac;
-            float sT = 0.f, s1 = 0.f, sW = 0.f, sD = 0.f;
-            // this row's group scalars from the lane that holds them
-            const int src = q * RPP + lane / LPR;
-            const float mu = __shfl(p_mu, src, 64), inv_a = __shfl(p_inva, src, 64);
-            const float delta = __shfl(p_delta, src, 64), ED = __shfl(p_ed, src, 64);
-            if (m < m_lim && n < g.N && F.mode != CATQ_IDENTITY) {
-              const f32x4 w = widen4(gv[q]);
-              float hc[4];
-              if (F.mode == CATQ_HARD) {
-                HardThresh th;
-                th.theta = __shfl(p_th.theta, src, 64);
-                th.hi = __shfl(p_th.hi, src, 64);
-                th.lo = __shfl(p_th.lo, src, 64);
-                const float w4[4] = {w[0], w[1], w[2], w[3]};
-                hard_codes_n<4>(w4, mu, th, hc);
-              }
-#pragma unroll
-              for (int e = 0; e < 4; ++e) {
-                const float xs = (w[e] - mu) * inv_a;
-                float f = 0.f, fW = 1.f, fD = 0.f;
-                if (!F.ste) transition_parts(xs, delta, ED, F.st, f, fW, fD);
-                const float T = (F.mode == CATQ_HARD) ? hc[e] : f;
-                sT = fmaf(v[e], T, sT);
-                const float gf = v[e] * fW;
-                s1 += gf;
-                sW = fmaf(gf, xs, sW);
-                sD = fmaf(v[e], fD, sD);
-              }
-            }
-#pragma unroll
-            for (int mk = 1; mk < 16; mk <<= 1) {
-              sT += __shfl_xor(sT, mk, 64);
-              s1 += __shfl_xor(s1, mk, 64);
-              sW += __shfl_xor(sW, mk, 64);
-              sD += __shfl_xor(sD, mk, 64);
-            }
-            if ((lane & 15) == 0) {
-              // [tile row][group of the tile][half of the group][term]
-              float* d = fsum + ((int)(mrow - m0 + rr) * 4 + wn) * 4;
-              d[0] = sT;
-              d[1] = s1;
-              d[2] = sW;
-              d[3] = sD;
-            }
-            continue;
-          }
           if (m < m_lim && n < g.N) {
             v *= g.alpha;
             if constexpr (EPI == 1) {
@@ -1006,14 +931,15 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
       // (the separate factor-gradient kernel's formulas)
       __syncthreads();
       const FacEpi& F = g.fac;
-      for (int t = tid; t < BM * 2; t += NW * 64) {
-        const int row = t >> 1, gt = t & 1;
-        const float* a0 = fsum + (row * 4 + 2 * gt) * 4;
+      constexpr int GPT = BN / 128;  // groups per tile row
+      for (int t = tid; t < BM * GPT; t += NW * 64) {
+        const int row = t / GPT, gt = t % GPT;
+        const float* a0 = fsum + (row * WGN + 2 * gt) * 4;
         // the constant factors of f (k2, soft only), f_W and f_Delta (sk4)
         const FacScale k = fac_scale(F.mode, F.ste, F.st);
         const float sT = (a0[0] + a0[4]) * k.f, s1 = (a0[1] + a0[5]) * k.w;
         const float sW = (a0[2] + a0[6]) * k.w, sD = (a0[3] + a0[7]) * k.d;
-        const int64_t grp = ((int64_t)z * g.M + m0 + row) * (g.N >> 7) + (n0 >> 7) + gt;
+        const int64_t grp = ((int64_t)z * g.M + m0 + row) * (F.ldw >> 7) + (n0 >> 7) + gt;
         const float alpha0 = F.stats[2 * grp + 1];
         const GroupScalars gs = group_scalars(F.stats[2 * grp], alpha0, F.dmu[grp * F.s[0]],
                                               F.dal[grp * F.s[1]], F.dde[grp * F.s[2]], F.delta0);
@@ -1415,8 +1341,45 @@ catq_status gemm_run_factor(const GemmArgs& a, hipStream_t stream) {
   const bool shape = a.M > 0 && a.N > 0 && a.M % 256 == 0 && a.N % 256 == 0 && a.alpha == 1.0f &&
                      a.R == nullptr && a.c_gs == 0 && a.ldc % 4 == 0 && aligned16(a.C) &&
                      a.fac.W != nullptr && (reinterpret_cast<uintptr_t>(a.fac.W) & 7) == 0 &&
-                     dma_ok(L, 1, 1, 256, 256);
+                     a.fac.ldw == a.N && dma_ok(L, 1, 1, 256, 256);
   if (!shape) return CATQ_ERR_VALUE;
+  if (a.group_mode == 0) {
+    // A partial last round of a quarter to three quarters of the 256
+    // compute units (5120 x 17408: 1360 tiles, 5.3 rounds): the columns past
+    // the last whole round run as a 128 x 128 launch of their own (two
+    // workgroups per unit, one round at most), with the weights, group
+    // arrays and outputs taken from that column on (the row pitch of W, and
+    // so the group numbering, stays the whole d_in)
+    const int tm = (int)(a.M / 256), tn = (int)(a.N / 256);
+    const int rem = (tm * tn) % 256;
+    int h = 0;
+    if (rem >= 64 && rem <= 192)
+      for (int c = tn - 1; c >= 1 && h == 0; --c)
+        if ((tm * c) % 256 == 0) h = c;
+    if (h > 0) {
+      const int64_t nh = (int64_t)h * 256, gsh = nh / 128;
+      GemmLaunch H = L, T = L;
+      H.g.N = nh;
+      T.g.N = a.N - nh;
+      T.g.B = reinterpret_cast<const bf16*>(a.B) + nh;
+      FacEpi& F = T.g.fac;
+      F.W = reinterpret_cast<const bf16*>(F.W) + nh;
+      F.stats += 2 * gsh;
+      F.dmu += gsh * F.s[0];
+      F.dal += gsh * F.s[1];
+      F.dde += gsh * F.s[2];
+      for (int k = 0; k < 3; ++k)
+        if (F.s[k] == 1) F.out[k] += gsh;
+      if (F.ws != nullptr) F.ws += gsh;
+      const int64_t t128 = (a.M / 128) * (T.g.N / 128);
+      if (t128 <= 512 && dma_ok(T, 1, 1, 128, 128)) {
+        launch_dma<256, 256, 4, 4, true, true, float, float, 3>(H, stream);
+        launch_dma<128, 128, 2, 2, true, true, float, float, 3>(T, stream);
+        CATQ_CHECK_LAUNCH("gemm factor epilogue");
+        return CATQ_OK;
+      }
+    }
+  }
   launch_dma<256, 256, 4, 4, true, true, float, float, 3>(L, stream);
   CATQ_CHECK_LAUNCH("gemm factor epilogue");
   return CATQ_OK;

@@ -66,7 +66,8 @@ struct StConst {
 // learnable factors of every 128-weight group of W (the reductions of
 // Sec. 2.3), as the separate factor-gradient kernel computes them from G.
 struct FacEpi {
-  const void* W;          // bf16 weights [E][rows][d_in] (E = 1 when dense)
+  const void* W;          // bf16 weights [E][rows][ldw] (E = 1 when dense)
+  int64_t ldw;            // row pitch of W (d_in; a column range of G keeps it)
   const float* stats;     // [n_groups][2] mu0, alpha0
   const float* dmu;
   const float* dal;

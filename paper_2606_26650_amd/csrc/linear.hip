@@ -263,6 +263,7 @@ extern "C" catq_status catq_fakeq_linear_bwd(
     f.c_gs = 0;  // C is only an aligned dummy
     FacEpi& fe = f.fac;
     fe.W = W;
+    fe.ldw = K;
     fe.stats = stats;
     fe.dmu = d_mu;
     fe.dal = d_alpha;

@@ -222,6 +222,23 @@ def test_dense_factor_epilogue(catq, M, N, K, fused, mode, s_bwd, strides):
     no dW_fake requested); other shapes take the two-pass path.  Both against
     the oracle and against the separate factor-gradient kernel on the
     materialised G (requested through dW_fake)."""
+    _dense_factor_case(catq, M, N, K, fused, mode, s_bwd, strides)
+
+
+@pytest.mark.parametrize("mode,s_bwd,strides", [
+    (lmst.SOFT, 30.0, (1, 1, 1)), (lmst.HARD, 30.0, (1, 1, 1)), (lmst.SOFT, 30.0, (0, 1, 0))])
+def test_dense_factor_epilogue_partial_round(catq, mode, s_bwd, strides):
+    """A 2048 x 10240 gradient is 320 tiles of 256 x 256, a quarter of a
+    second round: its last 2048 columns run as a 128 x 128 factor-epilogue
+    launch of their own (weights, group arrays and outputs from that column
+    on), the rest on 256 x 256 tiles.  Oracle parity as above, shared factors
+    included."""
+    tags = _dense_factor_case(catq, 256, 2048, 10240, True, mode, s_bwd, strides)
+    assert any(t.startswith("gemm_dma_kernel<128, 128") and "factor_grads" in t for t in tags), tags
+    assert any(t.startswith("gemm_dma_kernel<256, 256") and "factor_grads" in t for t in tags), tags
+
+
+def _dense_factor_case(catq, M, N, K, fused, mode, s_bwd, strides):
     import torch
     xb = sg.normal_bf16(11, "X", (M, K))
     wb = sg.normal_bf16(11, "W", (N, K), std=0.02)
@@ -264,6 +281,8 @@ def test_dense_factor_epilogue(catq, M, N, K, fused, mode, s_bwd, strides):
         assert torch.isfinite(a).all()
         assert max_norm_err(host(a), r) <= 2e-2
         assert max_norm_err(host(a), host(b)) <= 1e-4
+    return tags
+
 
 def test_fp32_linear(catq):
     import torch
