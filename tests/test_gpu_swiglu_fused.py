@@ -95,6 +95,7 @@ def _down(catq, M, N, F, seed):
 
 @pytest.mark.parametrize("M,N,F", [(4096, 512, 4096),      # fused
                                    (4141, 256, 4096),      # fused, ragged M
+                                   (2048, 256, 10240),     # fused, 1.25 rounds of tiles
                                    (4096, 256, 4104),      # separate (F % 256)
                                    (512, 256, 384)])       # separate (small)
 def test_down_swiglu_bwd_fused(catq, M, N, F):
