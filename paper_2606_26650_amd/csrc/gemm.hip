@@ -782,22 +782,43 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
       // lane's 16 weights, then over the row's 4 lanes.  G[m][n] of expert z,
       // or of the one dense problem (z = 0), unsplit, alpha 1.
       static_assert(WTN == 64 && SR == 16 && HP == 2, "factor epilogue lane map");
+      constexpr int GPT = BN / 128;  // groups per tile row
+      static_assert(BM * GPT <= NW * 64, "one reduced group per thread");
       const FacEpi& F = g.fac;
       const int rr = lane >> 2, cq = (lane & 3) * 16;
       const int64_t ncol = n0 + wn * WTN + cq;
+      // The raw group scalars (mu0, alpha0 and the three factors) of a part's
+      // row, loaded one part ahead, and those of the group this thread
+      // reduces at the end, loaded with the last part: with a few k tiles
+      // per tile (routed experts: ~256 rows) these loads' latency is
+      // otherwise exposed.
+      auto raw_scalars = [&](int64_t grp, float (&r)[5]) {
+        r[0] = F.stats[2 * grp];
+        r[1] = F.stats[2 * grp + 1];
+        r[2] = F.dmu[grp * F.s[0]];
+        r[3] = F.dal[grp * F.s[1]];
+        r[4] = F.dde[grp * F.s[2]];
+      };
+      auto part_group = [&](int p) {
+        const int64_t mrow = m0 + wm * WTM + (p / HP) * 32 + (p % HP) * SR;
+        return ((int64_t)z * g.M + min(mrow + rr, m_lim - 1)) * (F.ldw >> 7) + (ncol >> 7);
+      };
+      const int ft = min(tid, BM * GPT - 1), frow = ft / GPT, fgt = ft % GPT;
+      const int64_t fgrp = ((int64_t)z * g.M + m0 + frow) * (F.ldw >> 7) + (n0 >> 7) + fgt;
+      float gsf[5], gsc[5], gsn[5];
+      raw_scalars(part_group(0), gsc);
 #pragma unroll
       for (int p = 0; p < PARTS; ++p) {
         const int i = p / HP, h = p % HP;
         const int64_t mrow = m0 + wm * WTM + i * 32 + h * SR;
-        const int64_t m_c = min(mrow + rr, m_lim - 1);
-        const int64_t wrow = (int64_t)z * g.M + m_c;
         uint2 wv[4];
 #pragma unroll
         for (int q = 0; q < 4; ++q) wv[q] = epw[q];
-        const int64_t grp = wrow * (F.ldw >> 7) + (ncol >> 7);
-        const GroupScalars gs = group_scalars(F.stats[2 * grp], F.stats[2 * grp + 1],
-                                              F.dmu[grp * F.s[0]], F.dal[grp * F.s[1]],
-                                              F.dde[grp * F.s[2]], F.delta0);
+        const GroupScalars gs = group_scalars(gsc[0], gsc[1], gsc[2], gsc[3], gsc[4], F.delta0);
+        if (p + 1 < PARTS)
+          raw_scalars(part_group(p + 1), gsn);
+        else
+          raw_scalars(fgrp, gsf);
         // the part's accumulator slab through this wave's staging area
 #pragma unroll
         for (int j = 0; j < FN; ++j)
@@ -864,11 +885,40 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
           d[2] = sW;
           d[3] = sD;
         }
+        if (p + 1 < PARTS) {
+#pragma unroll
+          for (int k = 0; k < 5; ++k) gsc[k] = gsn[k];
+        }
+      }
+      // both halves of each group in order, then the three factor gradients
+      // (the separate factor-gradient kernel's formulas)
+      __syncthreads();
+      if (tid < BM * GPT) {
+        const int row = frow, gt = fgt;
+        const float* a0 = fsum + (row * WGN + 2 * gt) * 4;
+        // the constant factors of f (k2, soft only), f_W and f_Delta (sk4)
+        const FacScale k = fac_scale(F.mode, F.ste, F.st);
+        const float sT = (a0[0] + a0[4]) * k.f, s1 = (a0[1] + a0[5]) * k.w;
+        const float sW = (a0[2] + a0[6]) * k.w, sD = (a0[3] + a0[7]) * k.d;
+        const int64_t grp = fgrp;
+        const float alpha0 = gsf[1];
+        const GroupScalars gs = group_scalars(gsf[0], alpha0, gsf[2], gsf[3], gsf[4], F.delta0);
+        float o[3];
+        o[0] = alpha0 * (-s1);
+        o[1] = alpha0 * (sT - sW);
+        o[2] = F.delta0 * (gs.alpha * sD);
+#pragma unroll
+        for (int k = 0; k < 3; ++k) {
+          if (F.s[k] == 1)
+            F.out[k][grp] = o[k];
+          else
+            F.ws[k * F.n_groups + grp] = o[k];
+        }
       }
     }
     // (the factor epilogue has its own loop above)
     if constexpr (EPI != 3) load_part(0, 0);
-#pragma unroll
+  #pragma unroll
     for (int p = 0; p < (EPI == 3 ? 0 : PARTS); ++p) {
       const int i = p / HP, h = p % HP;
       {
@@ -877,14 +927,14 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
         [[maybe_unused]] auto& rv = rvb[p & 1];
         [[maybe_unused]] auto& gv = gvb[p & 1];
         [[maybe_unused]] auto& uv = uvb[p & 1];
-#pragma unroll
+  #pragma unroll
         for (int j = 0; j < FN; ++j)
-#pragma unroll
+  #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int row = 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
             if (row / SR == h) st[(row - h * SR) * EP + j * 32 + (lane & 31)] = acc[i][j][r];
           }
-#pragma unroll
+  #pragma unroll
         for (int q = 0; q < NP; ++q) {
           const int rr = q * RPP + lane / LPR;
           const int64_t m = mrow + rr;
@@ -909,7 +959,7 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
               bf16* dgu = reinterpret_cast<bf16*>(g.aux1) + m * g.ld_aux;
               const f32x4 gg = widen4(gv[q]), uu = widen4(uv[q]);
               f32x4 dg, du;
-#pragma unroll
+  #pragma unroll
               for (int e = 0; e < 4; ++e) {
                 float a_, b_;
                 swiglu1_bwd(gg[e], uu[e], bf16_round_f(v[e]), a_, b_);
@@ -923,36 +973,6 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
               store4f(C + m * g.ldc + n, v);
             }
           }
-        }
-      }
-    }
-    if constexpr (EPI == 3) {
-      // both halves of each group in order, then the three factor gradients
-      // (the separate factor-gradient kernel's formulas)
-      __syncthreads();
-      const FacEpi& F = g.fac;
-      constexpr int GPT = BN / 128;  // groups per tile row
-      for (int t = tid; t < BM * GPT; t += NW * 64) {
-        const int row = t / GPT, gt = t % GPT;
-        const float* a0 = fsum + (row * WGN + 2 * gt) * 4;
-        // the constant factors of f (k2, soft only), f_W and f_Delta (sk4)
-        const FacScale k = fac_scale(F.mode, F.ste, F.st);
-        const float sT = (a0[0] + a0[4]) * k.f, s1 = (a0[1] + a0[5]) * k.w;
-        const float sW = (a0[2] + a0[6]) * k.w, sD = (a0[3] + a0[7]) * k.d;
-        const int64_t grp = ((int64_t)z * g.M + m0 + row) * (F.ldw >> 7) + (n0 >> 7) + gt;
-        const float alpha0 = F.stats[2 * grp + 1];
-        const GroupScalars gs = group_scalars(F.stats[2 * grp], alpha0, F.dmu[grp * F.s[0]],
-                                              F.dal[grp * F.s[1]], F.dde[grp * F.s[2]], F.delta0);
-        float o[3];
-        o[0] = alpha0 * (-s1);
-        o[1] = alpha0 * (sT - sW);
-        o[2] = F.delta0 * (gs.alpha * sD);
-#pragma unroll
-        for (int k = 0; k < 3; ++k) {
-          if (F.s[k] == 1)
-            F.out[k][grp] = o[k];
-          else
-            F.ws[k * F.n_groups + grp] = o[k];
         }
       }
     }
