@@ -1160,14 +1160,14 @@ static bool dma_ok(const GemmLaunch& L, int a_t, int b_t, int bm, int bn) {
          (b_t == 0 || g.N % bn == 0);
 }
 
-// A dense product on 256 x 256 tiles.  A forward product whose weight (B,
-// K-contiguous) exceeds 128 MB streams it from HBM: three B stages
-// (bit-identical; the 14B-shaped down projection with its residual, 1.42 ->
-// 1.38 ms in the calibration step).
+// A dense product on 256 x 256 tiles.  An unsplit forward product (both
+// operands K-contiguous) takes three B stages, its weight's copies two k
+// tiles ahead (bit-identical; in the 14B-shaped calibration step down 1.42
+// -> 1.38 ms, q|k|v 0.434 -> 0.409 ms, o 0.308 -> 0.299 ms; no loss on the
+// 1.7B-shaped block's smaller weights).
 template <int A_T, int B_T, typename OutT, typename RT>
 static void launch_dense256(GemmLaunch& L, hipStream_t stream) {
-  const GemmArgs& g = L.g;
-  if (A_T == 0 && B_T == 0 && L.ksplit <= 1 && (double)g.N * (double)g.K * 2.0 > 128.0 * (1 << 20))
+  if (A_T == 0 && B_T == 0 && L.ksplit <= 1)
     launch_dma<256, 256, 4, 4, false, false, OutT, RT, 0, 3>(L, stream);
   else
     launch_dma<256, 256, 4, 4, A_T == 1, B_T == 1, OutT, RT>(L, stream);
@@ -1328,13 +1328,9 @@ catq_status gemm_run_epi(const GemmArgs& a, int a_t, int b_t, hipStream_t stream
     // A [M][K] tokens (K-contiguous), B the fused weight [N][K]
     if (!(shape && a_t == 0 && b_t == 0 && a.M >= 256 && a.N >= 256 && dma_ok(L, 0, 0, 256, 256)))
       return CATQ_ERR_VALUE;
-    // a weight of more than 128 MB streams from HBM: three B stages
-    // (bit-identical; 2.47 -> 2.39 ms on the 14B-shaped gate|up in the
-    // calibration step)
-    if ((double)a.N * (double)a.K * 2.0 > 128.0 * (1 << 20))
-      launch_dma<256, 256, 4, 4, false, false, bf16, bf16, 1, 3>(L, stream);
-    else
-      launch_dma<256, 256, 4, 4, false, false, bf16, bf16, 1>(L, stream);
+    // three B stages, as the plain forward products (bit-identical; 2.47 ->
+    // 2.39 ms on the 14B-shaped gate|up in the calibration step)
+    launch_dma<256, 256, 4, 4, false, false, bf16, bf16, 1, 3>(L, stream);
   } else {
     // dX-shaped: A = dY [M][K] (K-contiguous), B = W_fake [K][N] (K-major)
     if (!(shape && a_t == 0 && b_t == 1 && a.M >= 256 && a.N >= 256 && dma_ok(L, 0, 1, 256, 256)))
