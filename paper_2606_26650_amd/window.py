@@ -114,10 +114,10 @@ class Window:
         """LM+ST of every block -> window forward -> Eq. 7 loss -> backward
         through the blocks in reverse.  Loss stays on the device.
         ``finalize`` (buffers from finalize_buffers) also runs every block's
-        hard ternarisation + packing, on the side stream after LM+ST.
-        ``input_grad`` false skips the gradient of the window input (the
-        first block's dx); the later blocks' input gradients are always formed.
-        ``overlap`` None takes overlap_default."""
+        hard ternarisation + packing after LM+ST (on the side stream with
+        ``overlap``; None takes overlap_default).  ``input_grad`` false skips
+        the gradient of the window input (the first block's dx); the later
+        blocks' input gradients are always formed."""
         if overlap is None:
             overlap = self.overlap_default
         p = self.params(mode, s, s_bwd)
