@@ -831,12 +831,16 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
         if (p + 1 < PARTS) epi3_load(p + 1);
         float sT = 0.f, s1 = 0.f, sW = 0.f, sD = 0.f;
         if (mrow + rr < m_lim && F.mode != CATQ_IDENTITY) {
-          const float mu = gs.mu, inv_a = __builtin_amdgcn_rcpf(gs.alpha_div);
+          const float mu = gs.mu;
+          // z = (w - mu) / alpha * c2s as one FMA per weight
+          const float zk = F.st.c2s * __builtin_amdgcn_rcpf(gs.alpha_div), z0 = -mu * zk;
           const float dz = gs.delta * F.st.c2s;
           const float ed = one_minus_exp_neg(gs.delta * F.st.s4, gs.delta * F.st.s4l);
-          // one pass: 4 weights (rotated into wv[0]) against 4 G values
-          auto pass = [&](int q, auto hard_c) {
-            constexpr bool HARD = decltype(hard_c)::value;
+          // one pass: 4 weights (rotated into wv[0]) against 4 G values;
+          // (HARD, STE: the straight-through estimator, hard mode only) are
+          // launch constants, one loop per combination
+          auto pass = [&](int q, auto hard_c, auto ste_c) {
+            constexpr bool HARD = decltype(hard_c)::value, STE = decltype(ste_c)::value;
             const f32x4 v = *reinterpret_cast<const f32x4*>(st + rr * EP + cq + 4 * q);
             const f32x4 w = widen4(wv[0]);
             // the next pass's weights into wv[0] (registers rotated: no
@@ -849,24 +853,46 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
               const float w4[4] = {w[0], w[1], w[2], w[3]};
               hard_codes_n<4>(w4, mu, hard_thresh(gs.delta, gs.alpha_div), hc);
             }
+            float z[4], E[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-              const float xs = (w[e] - mu) * inv_a;
+              z[e] = fmaf(w[e], zk, z0);
+              E[e] = 1.0f - __builtin_amdgcn_exp2f(-2.0f * fabsf(z[e]));
+            }
+            if constexpr (!STE) {
+              // 1 - 2^(-2y) by its series below y = 0.09 (no cancellation),
+              // only in passes where some lane of the wave has such a y
+              bool small = false;
+#pragma unroll
+              for (int e = 0; e < 4; ++e) small |= fabsf(z[e]) < 0.09016844f;
+              if (__any(small)) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                  const float y = fabsf(z[e]);
+                  E[e] = y < 0.09016844f ? one_minus_exp2_neg2(y, 0.0f) : E[e];
+                }
+              }
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
               float fp = 0.f, fwp = 1.f, fdp = 0.f;
-              if (!F.ste) transition_parts_z(xs, F.st.c2s, dz, ed, fp, fwp, fdp);
+              if constexpr (!STE) transition_parts_zE(z[e], dz, ed, E[e], fp, fwp, fdp);
               sT = fmaf(v[e], HARD ? hc[e] : fp, sT);
               const float gf = v[e] * fwp;
               s1 += gf;
-              sW = fmaf(gf, xs, sW);
+              sW = fmaf(gf, z[e], sW);  // g f_W z: wz rescales per group
               sD = fmaf(v[e], fdp, sD);
             }
           };
-          if (F.mode == CATQ_HARD) {
+          if (F.mode == CATQ_HARD && F.ste) {
 #pragma unroll 1
-            for (int q = 0; q < 4; ++q) pass(q, std::true_type{});
+            for (int q = 0; q < 4; ++q) pass(q, std::true_type{}, std::true_type{});
+          } else if (F.mode == CATQ_HARD) {
+#pragma unroll 1
+            for (int q = 0; q < 4; ++q) pass(q, std::true_type{}, std::false_type{});
           } else {
 #pragma unroll 1
-            for (int q = 0; q < 4; ++q) pass(q, std::false_type{});
+            for (int q = 0; q < 4; ++q) pass(q, std::false_type{}, std::false_type{});
           }
         }
 #pragma unroll
@@ -899,7 +925,7 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
         // the constant factors of f (k2, soft only), f_W and f_Delta (sk4)
         const FacScale k = fac_scale(F.mode, F.ste, F.st);
         const float sT = (a0[0] + a0[4]) * k.f, s1 = (a0[1] + a0[5]) * k.w;
-        const float sW = (a0[2] + a0[6]) * k.w, sD = (a0[3] + a0[7]) * k.d;
+        const float sW = (a0[2] + a0[6]) * k.wz, sD = (a0[3] + a0[7]) * k.d;
         const int64_t grp = fgrp;
         const float alpha0 = gsf[1];
         const GroupScalars gs = group_scalars(gsf[0], alpha0, gsf[2], gsf[3], gsf[4], F.delta0);

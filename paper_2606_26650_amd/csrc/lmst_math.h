@@ -224,16 +224,40 @@ __device__ __forceinline__ void transition_parts_z(float xs, float c2s, float dz
   fdp = copysignf((qa * eb) * om * (rden * rden), -xs);
 }
 
+// The same parts from z itself with E = 1 - 2^(-2|z|) given (the GEMM
+// epilogue forms E for a whole pass of weights, taking the series only where
+// some lane of the wave needs it), 1/(1 + q_a)^2 and 1/(1 + q_b)^2 as
+// (1 + q_b)^2 r^2 and (1 + q_a)^2 r^2 from the one reciprocal r.
+__device__ __forceinline__ void transition_parts_zE(float z, float dz, float ed, float E,
+                                                    float& fp, float& fwp, float& fdp) {
+  const float y = fabsf(z);
+  const float d = y - dz;
+  const float qa = __builtin_amdgcn_exp2f(-fabsf(d));
+  const bool ge = d >= 0.0f;
+  const float eb = ge ? ed : E;
+  const float qb = fmaf(-qa, eb, qa);
+  const float opa = 1.0f + qa, opb = 1.0f + qb;
+  const float rden = __builtin_amdgcn_rcpf(opa * opb);
+  const float r2 = rden * rden;
+  const float num = ge ? E : qa * E;
+  fp = copysignf(num * rden, z);
+  fwp = fmaf(qa, opb * opb, qb * (opa * opa)) * r2;
+  const float om = ge ? E : ed;
+  fdp = copysignf((qa * eb) * om * r2, -z);
+}
+
 // Scales of the per-group sums of transition_parts_z: f is the hard code
-// (HARD, no scale) or k2 fp; f_W is 1 under the straight-through estimator.
+// (HARD, no scale) or k2 fp; f_W is 1 under the straight-through estimator;
+// wz turns a sum of g f_W z (z = xs c2s) into that of g f_W xs.
 struct FacScale {
-  float f, w, d;
+  float f, w, d, wz;
 };
 __device__ __forceinline__ FacScale fac_scale(int mode, int ste, const StConst& c) {
   FacScale k;
   k.f = (mode == CATQ_SOFT) ? c.k2 : 1.0f;
   k.w = ste ? 1.0f : c.sk4;
   k.d = c.sk4;
+  k.wz = k.w / c.c2s;
   return k;
 }
 
