@@ -58,6 +58,7 @@ struct GemmLaunch {
   int64_t kchunk;
   int64_t c_split_stride;
   int32_t tiles_m, tiles_n;
+  int32_t group_m;  // tile rows per band of the tile walk (band_coords)
 };
 
 constexpr int LDS_PAD = 8;
@@ -169,10 +170,11 @@ __device__ __forceinline__ void store_out<bf16>(bf16* p, float v) {
   *p = (bf16)v;
 }
 
-// tile id -> (tile row, tile column), walking bands of 8 tile rows column by
-// column (the A panels of a band stay in L2 while its B panels stream)
-__device__ __forceinline__ void band_coords(int pid, int tiles_m, int tiles_n, int& pm, int& pn) {
-  constexpr int GROUP_M = 8;
+// tile id -> (tile row, tile column), walking bands of GROUP_M tile rows
+// column by column (the A panels of a band stay in L2 while its B panels
+// stream)
+__device__ __forceinline__ void band_coords(int pid, int tiles_m, int tiles_n, int& pm, int& pn,
+                                            int GROUP_M = 8) {
   const int in_group = GROUP_M * tiles_n;
   const int gid = pid / in_group;
   const int first = gid * GROUP_M;
@@ -194,11 +196,11 @@ __device__ __forceinline__ void tile_coords(int pid, int tiles_m, int tiles_n, i
 // with splits an XCD works through one K range (its operand panels are read
 // by that XCD alone) and neighbouring tiles share its L2.
 __device__ __forceinline__ void split_tile_coords(int lin, int tiles_m, int tiles_n, int ksplit,
-                                                  int& pm, int& pn, int& z) {
+                                                  int& pm, int& pn, int& z, int group_m) {
   const int T = tiles_m * tiles_n, num = T * ksplit;
   const int v = (num & 7) == 0 ? (lin & 7) * (num >> 3) + (lin >> 3) : lin;
   z = v / T;
-  band_coords(v - z * T, tiles_m, tiles_n, pm, pn);
+  band_coords(v - z * T, tiles_m, tiles_n, pm, pn, group_m);
 }
 
 template <int BM, int BN, int BK, int WGM, int WGN, int A_T, int B_T, typename OutT, typename RT,
@@ -602,7 +604,7 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
     Bb += (int64_t)e * g.b_gs;
   } else {
     split_tile_coords(blockIdx.x, L.tiles_m, L.tiles_n,
-                      g.group_mode == 2 ? g.n_groups : L.ksplit, pm, pn, z);
+                      g.group_mode == 2 ? g.n_groups : L.ksplit, pm, pn, z, L.group_m);
     m0 = (int64_t)pm * BM;
     if (g.group_mode == 2) {
       // contraction grouped by expert (ragged): rows past the group's end
@@ -1141,6 +1143,12 @@ template <int BM, int BN, int WGM, int WGN, bool AKM, bool BKM, typename OutT, t
           int EPI = 0, int SB = 2>
 static void launch_dma(GemmLaunch& L, hipStream_t stream) {
   const GemmArgs& g = L.g;
+  // Bands of the tile walk: 8 tile rows (of the 32 tiles in flight per XCD,
+  // 8 x 4), but 2 (2 x 16) for the weight-gradient products, both operands
+  // K-major: measured in the 14B-shaped calibration step, their launches
+  // take 4.29 (8 rows), 4.21 (4), 4.16 (2) and 4.18 ms (1) per step, while
+  // the other layouts are best at 8.
+  L.group_m = AKM ? 2 : 8;
   // grouped rows: at most ceil(M/BM) + E m-tiles over all experts together
   L.tiles_m = (int)((g.M + BM - 1) / BM) + (g.group_mode == 1 ? g.n_groups : 0);
   L.tiles_n = (int)((g.N + BN - 1) / BN);
