@@ -340,16 +340,17 @@ def test_streamed_weight_fwd_sampled(catq):
     assert np.all(np.abs(got - ref) <= 2.0 ** -14 * mag + 2.0 ** -20 * np.abs(ref))
 
 
-@pytest.mark.parametrize("out_f32", [False, True])
-def test_partial_last_round_split(catq, out_f32):
+@pytest.mark.parametrize("M,N,out_f32", [(8192, 5120, False), (8192, 5120, True),
+                                         (8092, 5080, True)])   # ragged rows and tail
+def test_partial_last_round_split(catq, M, N, out_f32):
     """8192 x 5120 outputs are 640 tiles of 256 x 256, 2.5 rounds of the 256
     compute units: the columns past the second round run as a 128 x 128
-    launch of their own.  The whole output against float64 (with a residual
-    in the fp32 case), and the split-off columns bit for bit against the
-    same columns from an unsplit launch (the weight's rows 1024.., 512 tiles,
-    whole rounds)."""
+    launch of their own (for 8092 x 5080, with ragged rows and a ragged last
+    tile column).  The whole output against float64 (with a residual in the
+    fp32 case), and the split-off columns bit for bit against the same
+    columns from an unsplit launch (the weight's rows 1024.., whole rounds)."""
     import torch
-    M, N, K = 8192, 5120, 192
+    K = 192
     xb, wb = _xw(13, M, N, K)
     X, W = to_dev_bf16(xb), to_dev_bf16(wb)
     dt = torch.float32 if out_f32 else torch.bfloat16
