@@ -7,18 +7,20 @@
 // {0, 1, 2}; byte b of row n holds elements 4b..4b+3, element 4b+j in bits
 // 2j..2j+1; alpha fp32 [d_out][d_in / g].  Code 3 (invalid) contributes 0.
 //
-// gfx950 design.  One workgroup owns 16 (or 32) output rows and up to 16
-// tokens; its waves split the rows' 128-code chunks round robin and are
-// reduced through LDS in a fixed order (deterministic, no atomics).  Per chunk a lane loads
-// 8 bytes (32 codes) of its row, turns them into four MFMA operands of bf16
-// values 2T in {-2, 0, +2} with two byte-permute table lookups per four
-// codes (the low byte of ±2 and 0 in bf16 is 0, so only the high byte needs
-// a table), and issues four v_mfma_f32_16x16x32_bf16 against the matching
-// 64 contiguous bytes of X.  The operand order is the natural k order, so X
-// is loaded as is.  The chunk's 4 partial outputs per lane are scaled by
-// alpha/2 (the factor 2 of the decode is exact) and accumulated in fp32.
-// The scales of the workgroup's rows are staged in LDS once.
+// gfx950 design.  One workgroup owns R tiles of 16 output rows and up to 16
+// tokens; its waves split the 128-code chunks round robin and are reduced
+// through LDS in a fixed order (deterministic, no atomics).  Per chunk a lane
+// loads 8 bytes (32 codes) of its row in each tile, turns them into four MFMA
+// operands of bf16 values 2T in {-2, 0, +2} with two byte-permute table
+// lookups per four codes (the low byte of +-2 and 0 in bf16 is 0, so only the
+// high byte needs a table), and issues four v_mfma_f32_16x16x32_bf16 per tile
+// against the matching 64 contiguous bytes of X, loaded once for all R tiles.
+// The operand order is the natural k order, so X is loaded as is.  The chunk's
+// 4 partial outputs per lane and tile are scaled by alpha/2 (the factor 2 of
+// the decode is exact) and accumulated in fp32.  The scales of the
+// workgroup's rows are staged in LDS once.
 
+#include <cstdint>
 #include <type_traits>
 
 #include "catq_internal.h"
@@ -89,28 +91,34 @@ constexpr int kMaxChunks = 512;        // d_in <= 65536
 constexpr int kBufferFlags = 0x00020000;  // raw buffer resource word 3 (gfx9 family)
 constexpr int kOutOfRange = 0x40000000;   // offset past every slice this kernel builds
 
-// One workgroup = one tile of 16 output rows x up to 16 tokens; grid
-// (ceil(d_out / 16), ceil(M / 16)).  Its NW waves split the rows' 128-code
-// chunks (wave w: chunks w, w + NW, ...; MAXC at most per batch) and are
-// reduced through LDS in a fixed order.
-//  * Every code load of a batch is issued at once (raw buffer loads over the
-//    tile's rows: wave-uniform base and chunk offset, no address arithmetic
-//    per chunk; rows past d_out get an out-of-range offset and read zeros).
-//  * The tile's scales are staged in LDS ([chunk][row], alpha/2) by a
-//    shift-indexed loop whose loads are all in flight together with the
-//    codes.
-//  * X comes from L2 two chunks ahead with buffer loads whose absent tokens
-//    (15 of 16 lanes at one token) are out of range: no traffic, no branch.
-// Dynamic LDS: n_chunks * 16 floats.
-template <int NW, int MAXC, typename OutT>
+// One workgroup = R tiles of 16 output rows (RT = 16 R rows) x up to 16
+// tokens; grid (ceil(d_out / RT), ceil(M / 16)).  Its NW waves split the
+// 128-code chunks (wave w: chunks w, w + NW, ...) and are reduced through LDS
+// in a fixed order.
+//  * X crosses the vector memory path once per chunk and wave and serves all
+//    R tiles (at one token, 15 of the 16 token lanes read out of range: no
+//    traffic, but the lanes still return data, so that return is shared).
+//  * The codes and X of chunk k + D are issued while chunk k is multiplied:
+//    a ring of D + 1 register slots keeps D chunks of every wave in flight.
+//    Code loads are raw buffer loads over the tile's rows (wave-uniform base
+//    and chunk offset; rows past d_out read zeros).
+//  * The tile's scales ([chunk][row], alpha/2) are loaded first, coalesced
+//    along each row (at most AMAX per thread, all in flight with the first D
+//    chunks), and stored to LDS; the barrier before the products waits for
+//    LDS only, not for the code loads in flight.
+// Dynamic LDS: n_chunks * (RT + 4) floats.
+template <int NW, int R, int D, int AMAX, typename OutT>
 __global__ __launch_bounds__(NW * 64) void ternary_gemv_kernel(TernArgs a) {
+  constexpr int RT = 16 * R;   // rows of the workgroup
+  constexpr int AP = RT + 4;   // pitch of the staged scales (floats; 16-byte rows)
+  constexpr int S = D + 1;     // register slots of the ring
   extern __shared__ __align__(16) float s_alpha[];
-  __shared__ float s_red[NW][16][17];  // [wave][token][row]
+  __shared__ float s_red[NW][16][RT + 1];  // [wave][token][row]
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar branches
   const int q = lane >> 4, c16 = lane & 15;
-  const int64_t n0 = (int64_t)blockIdx.x * 16;
+  const int64_t n0 = (int64_t)blockIdx.x * RT;
   const int64_t m0 = (int64_t)blockIdx.y * 16;
   const int nch = a.n_chunks;
   const int64_t row_bytes = a.d_in >> 2;
@@ -119,94 +127,112 @@ __global__ __launch_bounds__(NW * 64) void ternary_gemv_kernel(TernArgs a) {
   const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<bf16*>(a.X + m0 * a.ldx), 0, (int)(tok_here * a.ldx * 2), kBufferFlags);
   const int xoff = c16 < tok_here ? (int)((c16 * a.ldx + 32 * q) * 2) : kOutOfRange;
-  const int rows_here = (int)min<int64_t>(16, a.d_out - n0);
+  const int rows_here = (int)min<int64_t>(RT, a.d_out - n0);
   const __amdgpu_buffer_rsrc_t pr = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint8_t*>(a.P + n0 * row_bytes), 0, (int)(rows_here * row_bytes), kBufferFlags);
-  const int poff = c16 < rows_here ? (int)(c16 * row_bytes + 8 * q) : kOutOfRange;
-  const int my_chunks = wave < nch ? (nch - wave + NW - 1) / NW : 0;
-  const int last = wave + NW * (my_chunks - 1);
-  const int n_batches = (my_chunks + MAXC - 1) / MAXC;
-
-  uint2 cw[MAXC];
-  auto load_batch = [&](int b) {
-    static_for<0, MAXC>([&](auto I) {
-      const int ch = min(wave + NW * (b * MAXC + I()), last);   // past the last: unused
-      cw[I()] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(pr, poff, ch * 32, 0));
-    });
-  };
-  auto load_x = [&](int ch, u32x4* xv) {
+  int poff[R];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) xv[j] = __builtin_amdgcn_raw_buffer_load_b128(xr, xoff + 16 * j, ch * 256, 0);
-  };
-  if (n_batches > 0) load_batch(0);
-  u32x4 xv[3][4];
-  if (n_batches > 0) {
-    load_x(wave, xv[0]);
-    load_x(min(wave + NW, last), xv[1]);
+  for (int r = 0; r < R; ++r) {
+    const int row = 16 * r + c16;
+    poff[r] = row < rows_here ? (int)(row * row_bytes + 8 * q) : kOutOfRange;
   }
+  const int my = wave < nch ? (nch - wave + NW - 1) / NW : 0;
 
-  // scales: thread handles row tid % 16 and chunks tid / 16 + k (NW * 4),
-  // all loads first, then the stores
-  {
-    constexpr int CPI = NW * 4;               // chunks per pass over the threads
-    constexpr int KA = (kMaxChunks + CPI - 1) / CPI;
-    const int r = tid & 15;
-    const int64_t row = n0 + r;
-    const float* arow = a.A + (row < a.d_out ? row : 0) * (int64_t)(nch >> a.cpg_shift);
-    const bool rok = row < a.d_out;
-    const int npass = (nch + CPI - 1) / CPI;
-    for (int p0 = 0; p0 < npass; p0 += 8) {
-      float v[8];
+  // scales: pair (row, chunk) = idx / nch, idx % nch, consecutive threads on
+  // consecutive chunks of a row; rows past d_out (and pairs past the tile)
+  // read zero through the buffer's bound.  Loaded before the ring's first
+  // chunks and stored after them, so both are in flight together.
+  float av[AMAX];
+  const int ng = nch >> a.cpg_shift;
+  const __amdgpu_buffer_rsrc_t ar = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(a.A + n0 * ng), 0, rows_here * ng * 4, kBufferFlags);
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int ch = (tid >> 4) + CPI * (p0 + u);
-        v[u] = (rok && ch < nch) ? 0.5f * arow[ch >> a.cpg_shift] : 0.f;
-      }
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int ch = (tid >> 4) + CPI * (p0 + u);
-        if (ch < nch) s_alpha[ch * 16 + r] = v[u];
-      }
-    }
-    (void)KA;
+  for (int u = 0; u < AMAX; ++u) {
+    const int idx = tid + NW * 64 * u;
+    const int r = idx / nch, ch = idx - r * nch;
+    av[u] = __builtin_bit_cast(
+        float, __builtin_amdgcn_raw_buffer_load_b32(ar, (r * ng + (ch >> a.cpg_shift)) * 4, 0, 0));
   }
-  __syncthreads();
+  __builtin_amdgcn_sched_barrier(0);   // (the scheduler keeps each phase in program order)
 
-  f32x4 out = {0.f, 0.f, 0.f, 0.f};
-  static_assert(MAXC % 3 == 0, "the three X buffers rotate in step across batches");
-  for (int b = 0; b < n_batches; ++b) {
-    if (b > 0) load_batch(b);
-    static_for<0, MAXC>([&](auto I) {
-      constexpr int i = I();
-      const int k = b * MAXC + i;
-      if (k >= my_chunks) return;                  // wave-uniform
-      const int ch = wave + NW * k;
-      // X two chunks ahead (clamped to the wave's last chunk)
-      load_x(min(ch + 2 * NW, last), xv[(i + 2) % 3]);
-      const u32x4* xa = xv[i % 3];
+  // chunk of the wave's k-th: clamped to its last (the ring's loads past the
+  // end re-read it; a wave without chunks reads chunk 0), never multiplied
+  const int last = my > 0 ? wave + NW * (my - 1) : 0;
+  uint2 cw[S][R];
+  u32x4 xv[S][4];
+  auto issue = [&](int k, auto slot_c) {
+    constexpr int s = decltype(slot_c)::value;
+    const int ch = min(wave + NW * k, last);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      xv[s][j] = __builtin_amdgcn_raw_buffer_load_b128(xr, xoff + 16 * j, ch * 256, 0);
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+      cw[s][r] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(pr, poff[r], ch * 32, 0));
+  };
+  static_for<0, D>([&](auto I) {
+    issue(I(), I);
+    __builtin_amdgcn_sched_barrier(0);   // (same load order as in the ring)
+  });
+
+#pragma unroll
+  for (int u = 0; u < AMAX; ++u) {
+    const int idx = tid + NW * 64 * u;
+    const int r = idx / nch, ch = idx - r * nch;
+    s_alpha[ch * AP + min(r, RT)] = 0.5f * av[u];   // pairs past the tile: the unread pad column
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+
+  f32x4 out[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) out[r] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // chunk k from slot k % S: four products per tile, scaled by the rows'
+  // alpha/2 and accumulated
+  auto compute = [&](int k, auto slot_c) {
+    constexpr int i = decltype(slot_c)::value;
+    const float* al = &s_alpha[(wave + NW * k) * AP + 4 * q];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
       u32x4 w0, w1, w2, w3;
-      decode16(cw[i].x, w0, w1);
-      decode16(cw[i].y, w2, w3);
+      decode16(cw[i][r].x, w0, w1);
+      decode16(cw[i][r].y, w2, w3);
       f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(w0), as_bf16x8(xa[0]), acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(w1), as_bf16x8(xa[1]), acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(w2), as_bf16x8(xa[2]), acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(w3), as_bf16x8(xa[3]), acc, 0, 0, 0);
-      // accumulator: rows 4q..4q+3 of the tile, token c16
-      const f32x4 al = *reinterpret_cast<const f32x4*>(&s_alpha[ch * 16 + 4 * q]);
-      out[0] += al[0] * acc[0];
-      out[1] += al[1] * acc[1];
-      out[2] += al[2] * acc[2];
-      out[3] += al[3] * acc[3];
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(w0), as_bf16x8(xv[i][0]), acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(w1), as_bf16x8(xv[i][1]), acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(w2), as_bf16x8(xv[i][2]), acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(w3), as_bf16x8(xv[i][3]), acc, 0, 0, 0);
+      // accumulator: rows 16 r + 4q .. +3 of the workgroup, token c16
+      const f32x4 sc = *reinterpret_cast<const f32x4*>(al + 16 * r);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) out[r][e] += sc[e] * acc[e];
+    }
+  };
+  // whole rounds of the ring without branches: chunk k + D issued into the
+  // slot chunk k - 1 used, then chunk k multiplied
+  const int full = my / S * S;
+  for (int k0 = 0; k0 < full; k0 += S) {
+    static_for<0, S>([&](auto I) {
+      constexpr int i = I();
+      issue(k0 + i + D, std::integral_constant<int, (i + D) % S>{});
+      __builtin_amdgcn_sched_barrier(0);
+      compute(k0 + i, I);
     });
   }
+  // the last my - full (< S) chunks, already in flight
+  static_for<0, S - 1>([&](auto I) {
+    if (full + I() < my) compute(full + I(), I);
+  });
 
   // fixed-order reduction over the waves
 #pragma unroll
-  for (int r = 0; r < 4; ++r) s_red[wave][c16][4 * q + r] = out[r];
+  for (int r = 0; r < R; ++r)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) s_red[wave][c16][16 * r + 4 * q + e] = out[r][e];
   __syncthreads();
-  for (int i = tid; i < 256; i += NW * 64) {
-    const int tok = i >> 4, r = i & 15;
+  for (int i = tid; i < 16 * RT; i += NW * 64) {
+    const int tok = i / RT, r = i % RT;
     float sum = 0.f;
 #pragma unroll
     for (int w = 0; w < NW; ++w) sum += s_red[w][tok][r];
@@ -215,25 +241,32 @@ __global__ __launch_bounds__(NW * 64) void ternary_gemv_kernel(TernArgs a) {
   }
 }
 
-template <int NW, int MAXC>
+template <int NW, int R, int D, int AMAX>
 catq_status launch_tern(const TernArgs& a, catq_dtype y_dtype, hipStream_t stream) {
-  const dim3 grid((unsigned)((a.d_out + 15) / 16), (unsigned)((a.M + 15) / 16));
-  const size_t lds = (size_t)a.n_chunks * 16 * sizeof(float);
+  constexpr int RT = 16 * R;
+  // every (row, chunk) scale pair of a tile has a thread slot, and the LDS
+  // (scales + reduction) stays within 64 KB
+  CATQ_REQUIRE((int64_t)a.n_chunks * RT <= (int64_t)AMAX * NW * 64 &&
+                   (size_t)a.n_chunks * (RT + 4) * 4 + sizeof(float) * NW * 16 * (RT + 1) <= 65536,
+               CATQ_ERR_SHAPE, "ternary_linear: no launch shape for d_in = %lld",
+               (long long)a.d_in);
+  const dim3 grid((unsigned)((a.d_out + RT - 1) / RT), (unsigned)((a.M + 15) / 16));
+  const size_t lds = (size_t)a.n_chunks * (RT + 4) * sizeof(float);
   const double flops = 2.0 * (double)a.M * (double)a.d_out * (double)a.d_in;
   const double bytes = (double)a.d_out * (double)a.d_in / 4.0 +
                        4.0 * (double)a.d_out * (double)(a.n_chunks >> a.cpg_shift) +
                        2.0 * (double)a.M * (double)a.d_in +
                        (double)a.M * (double)a.d_out * (y_dtype == CATQ_F32 ? 4.0 : 2.0);
   static char tag[64];
-  snprintf(tag, sizeof tag, "ternary_gemv_kernel<%d, %d>", NW, MAXC);
+  snprintf(tag, sizeof tag, "ternary_gemv_kernel<%d, %d, %d>", NW, R, D);
   if (y_dtype == CATQ_F32) {
     CATQ_TRACED(stream, tag, flops, bytes, a.M, a.d_out, a.d_in,
-                hipLaunchKernelGGL((ternary_gemv_kernel<NW, MAXC, float>), grid, dim3(NW * 64),
-                                   lds, stream, a));
+                hipLaunchKernelGGL((ternary_gemv_kernel<NW, R, D, AMAX, float>), grid,
+                                   dim3(NW * 64), lds, stream, a));
   } else {
     CATQ_TRACED(stream, tag, flops, bytes, a.M, a.d_out, a.d_in,
-                hipLaunchKernelGGL((ternary_gemv_kernel<NW, MAXC, bf16>), grid, dim3(NW * 64),
-                                   lds, stream, a));
+                hipLaunchKernelGGL((ternary_gemv_kernel<NW, R, D, AMAX, bf16>), grid,
+                                   dim3(NW * 64), lds, stream, a));
   }
   CATQ_CHECK_LAUNCH("ternary_linear");
   return CATQ_OK;
@@ -281,9 +314,32 @@ extern "C" catq_status catq_ternary_linear(const void* X, int64_t M, int64_t ldx
   a.n_chunks = (int32_t)(d_in / 128);
   a.cpg_shift = __builtin_ctz((unsigned)(g / 128));
   a.Y = Y;
-  // few long waves: all of a wave's chunks (up to 21) in one batch
-  if (a.n_chunks <= 42) return launch_tern<2, 21>(a, y_dtype, stream);
-  if (a.n_chunks <= 84) return launch_tern<4, 21>(a, y_dtype, stream);
-  if (a.n_chunks <= 168) return launch_tern<8, 21>(a, y_dtype, stream);
-  return launch_tern<16, 21>(a, y_dtype, stream);
+  // The product is bound by the decode's vector instructions, so what
+  // matters is the work of the fullest compute unit: the workgroups it gets,
+  // ceil(workgroups / 256), times what one costs, R tiles of 16 rows plus the
+  // X loads that serve all R (worth about 0.3 tile at one to four tokens,
+  // whose other token lanes read nothing, and 1.5 tiles beyond).  Of R = 2..5
+  // the least cost wins, ties to the larger R.  The 34816-row gate|up: R = 3
+  // at one token (726 workgroups, at most 3 per unit; 18.4 us against 22.8
+  // for R = 4), R = 5 at 16 tokens (26.4 against 29.2 for R = 3).  Rows
+  // longer than 64 chunks take eight waves, their scales fewer rows.
+  if (a.n_chunks <= 64) {
+    const int64_t tiles = (d_out + 15) / 16, tok_tiles = (M + 15) / 16;
+    const double x = M > 4 ? 1.5 : 0.3;
+    int best_r = 2;
+    double best = 1e300;
+    for (int r = 2; r <= (a.n_chunks <= 51 ? 5 : 4); ++r) {
+      const int64_t per_cu = ((tiles + r - 1) / r * tok_tiles + 255) / 256;
+      const double cost = (double)per_cu * (r + x);
+      if (cost <= best) best = cost, best_r = r;
+    }
+    switch (best_r) {
+      case 5: return launch_tern<4, 5, 2, 16>(a, y_dtype, stream);
+      case 4: return launch_tern<4, 4, 2, 16>(a, y_dtype, stream);
+      case 3: return launch_tern<4, 3, 2, 16>(a, y_dtype, stream);
+      default: return launch_tern<4, 2, 3, 16>(a, y_dtype, stream);
+    }
+  }
+  if (a.n_chunks <= 256) return launch_tern<8, 2, 3, 16>(a, y_dtype, stream);
+  return launch_tern<8, 1, 3, 16>(a, y_dtype, stream);
 }

@@ -128,6 +128,33 @@ def test_ternary_linear_on_finalized_block(catq):
         np.testing.assert_allclose(ref, x @ hard["W_fake"].T, rtol=1e-12, atol=1e-15)
 
 
+@pytest.mark.parametrize("d_out,d_in,M,nw,r", [
+    (16379, 512, 3, 4, 4),     # 1024 tiles of 16 rows: four per workgroup
+    (20473, 384, 2, 4, 5),     # 1280 tiles: five per workgroup
+    (11000, 640, 1, 4, 3),     # 688 tiles: three per workgroup, the last one short
+    (4100, 768, 16, 4, 2),     # under 256 workgroups: two tiles each
+    (300, 9216, 2, 8, 2)])     # rows of 72 chunks: eight waves
+def test_ternary_linear_launch_shapes(catq, d_out, d_in, M, nw, r):
+    """Every launch shape the dispatch picks (2 to 5 row tiles per workgroup,
+    four or eight waves), each with a ragged last workgroup, against the
+    oracle; the trace names the shape that ran."""
+    import torch
+    packed, alpha, xb = _case(d_out, d_in, M, 128, 11)
+    catq.catq_trace_enable(8)
+    try:
+        y = _run(catq, packed, alpha, xb, 128, torch.float32, ldy_pad=5)
+        tags = [t["tag"] for t in catq.trace_records()]
+    finally:
+        catq.catq_trace_disable()
+    assert tags and tags[-1].startswith(f"ternary_gemv_kernel<{nw}, {r}, "), tags
+    xo = f64(xb)
+    ref = ternary.ternary_linear(xo, packed, alpha, d_in)
+    got = host(y)
+    assert np.isnan(got[:, d_out:]).all()
+    bound = _bound(xo, packed, alpha, d_in, 128, d_in // 128)
+    assert np.all(np.abs(got[:, :d_out] - ref) <= bound), float((np.abs(got[:, :d_out] - ref) / bound).max())
+
+
 @pytest.mark.slow
 @pytest.mark.parametrize("d_out,d_in,M", [(34816, 5120, 1), (5120, 17408, 1), (7168, 5120, 8),
                                           (34816, 5120, 16)])
