@@ -105,10 +105,13 @@ constexpr int kOutOfRange = 0x40000000;   // offset past every slice this kernel
 //  * The tile's scales ([chunk][row], alpha/2) are loaded first, coalesced
 //    along each row (at most AMAX per thread, all in flight with the first D
 //    chunks), and stored to LDS; the barrier before the products waits for
-//    LDS only, not for the code loads in flight.
+//    LDS only, not for the code loads in flight.  With one scale per chunk
+//    and whole quads of chunks per row (VEC), a thread takes four
+//    consecutive scales of a row per 16-byte load (AMAX / 4 loads).
 // Dynamic LDS: n_chunks * (RT + 4) floats.
-template <int NW, int R, int D, int AMAX, typename OutT>
-__global__ __launch_bounds__(NW * 64) void ternary_gemv_kernel(TernArgs a) {
+template <int NW, int R, int D, int AMAX, bool VEC, typename OutT>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4)))
+void ternary_gemv_kernel(TernArgs a) {
   constexpr int RT = 16 * R;   // rows of the workgroup
   constexpr int AP = RT + 4;   // pitch of the staged scales (floats; 16-byte rows)
   constexpr int S = D + 1;     // register slots of the ring
@@ -138,20 +141,28 @@ __global__ __launch_bounds__(NW * 64) void ternary_gemv_kernel(TernArgs a) {
   }
   const int my = wave < nch ? (nch - wave + NW - 1) / NW : 0;
 
-  // scales: pair (row, chunk) = idx / nch, idx % nch, consecutive threads on
-  // consecutive chunks of a row; rows past d_out (and pairs past the tile)
-  // read zero through the buffer's bound.  Loaded before the ring's first
-  // chunks and stored after them, so both are in flight together.
-  float av[AMAX];
+  // scales: pair (row, chunk) = idx / nch, idx % nch (VEC: row and quad of
+  // chunks, idx / (nch/4), idx % (nch/4)), consecutive threads along a row;
+  // rows past d_out (and pairs past the tile) read zero through the buffer's
+  // bound.  Loaded before the ring's first chunks and stored after them, so
+  // both are in flight together.
+  constexpr int NS = VEC ? (AMAX + 3) / 4 : AMAX;   // loads per thread
+  constexpr int T = NW * 64;
   const int ng = nch >> a.cpg_shift;
+  const int per_row = VEC ? nch >> 2 : nch;
   const __amdgpu_buffer_rsrc_t ar = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<float*>(a.A + n0 * ng), 0, rows_here * ng * 4, kBufferFlags);
+  f32x4 av[NS];
 #pragma unroll
-  for (int u = 0; u < AMAX; ++u) {
-    const int idx = tid + NW * 64 * u;
-    const int r = idx / nch, ch = idx - r * nch;
-    av[u] = __builtin_bit_cast(
-        float, __builtin_amdgcn_raw_buffer_load_b32(ar, (r * ng + (ch >> a.cpg_shift)) * 4, 0, 0));
+  for (int u = 0; u < NS; ++u) {
+    const int idx = tid + T * u;
+    if constexpr (VEC) {
+      av[u] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(ar, idx * 16, 0, 0));
+    } else {
+      const int r = idx / per_row, ch = idx - r * per_row;
+      av[u][0] = __builtin_bit_cast(
+          float, __builtin_amdgcn_raw_buffer_load_b32(ar, (r * ng + (ch >> a.cpg_shift)) * 4, 0, 0));
+    }
   }
   __builtin_amdgcn_sched_barrier(0);   // (the scheduler keeps each phase in program order)
 
@@ -176,10 +187,15 @@ __global__ __launch_bounds__(NW * 64) void ternary_gemv_kernel(TernArgs a) {
   });
 
 #pragma unroll
-  for (int u = 0; u < AMAX; ++u) {
-    const int idx = tid + NW * 64 * u;
-    const int r = idx / nch, ch = idx - r * nch;
-    s_alpha[ch * AP + min(r, RT)] = 0.5f * av[u];   // pairs past the tile: the unread pad column
+  for (int u = 0; u < NS; ++u) {   // pairs past the tile: the unread pad column
+    const int idx = tid + T * u;
+    const int r = idx / per_row, c = idx - r * per_row;
+    if constexpr (VEC) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) s_alpha[(4 * c + e) * AP + min(r, RT)] = 0.5f * av[u][e];
+    } else {
+      s_alpha[c * AP + min(r, RT)] = 0.5f * av[u][0];
+    }
   }
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
   __builtin_amdgcn_s_barrier();
@@ -241,8 +257,14 @@ __global__ __launch_bounds__(NW * 64) void ternary_gemv_kernel(TernArgs a) {
   }
 }
 
+template <typename T>
+struct OutTag {
+  using type = T;
+};
+
 template <int NW, int R, int D, int AMAX>
 catq_status launch_tern(const TernArgs& a, catq_dtype y_dtype, hipStream_t stream) {
+  const bool vec = a.cpg_shift == 0 && a.n_chunks % 4 == 0;
   constexpr int RT = 16 * R;
   // every (row, chunk) scale pair of a tile has a thread slot, and the LDS
   // (scales + reduction) stays within 64 KB
@@ -259,14 +281,21 @@ catq_status launch_tern(const TernArgs& a, catq_dtype y_dtype, hipStream_t strea
                        (double)a.M * (double)a.d_out * (y_dtype == CATQ_F32 ? 4.0 : 2.0);
   static char tag[64];
   snprintf(tag, sizeof tag, "ternary_gemv_kernel<%d, %d, %d>", NW, R, D);
+  auto launch = [&](auto vec_c, auto out_c) {
+    constexpr bool V = decltype(vec_c)::value;
+    using OutT = typename decltype(out_c)::type;
+    CATQ_TRACED(stream, tag, flops, bytes, a.M, a.d_out, a.d_in,
+                hipLaunchKernelGGL((ternary_gemv_kernel<NW, R, D, AMAX, V, OutT>), grid,
+                                   dim3(NW * 64), lds, stream, a));
+  };
+  using Vt = std::true_type;
+  using Vf = std::false_type;
   if (y_dtype == CATQ_F32) {
-    CATQ_TRACED(stream, tag, flops, bytes, a.M, a.d_out, a.d_in,
-                hipLaunchKernelGGL((ternary_gemv_kernel<NW, R, D, AMAX, float>), grid,
-                                   dim3(NW * 64), lds, stream, a));
+    if (vec) launch(Vt{}, OutTag<float>{});
+    else launch(Vf{}, OutTag<float>{});
   } else {
-    CATQ_TRACED(stream, tag, flops, bytes, a.M, a.d_out, a.d_in,
-                hipLaunchKernelGGL((ternary_gemv_kernel<NW, R, D, AMAX, bf16>), grid,
-                                   dim3(NW * 64), lds, stream, a));
+    if (vec) launch(Vt{}, OutTag<bf16>{});
+    else launch(Vf{}, OutTag<bf16>{});
   }
   CATQ_CHECK_LAUNCH("ternary_linear");
   return CATQ_OK;
