@@ -197,6 +197,18 @@ __device__ __forceinline__ void dma16_buf(i32x4_rsrc rsrc, uint32_t voff, uint32
                : "memory", "m0");
 #endif
 }
+// The same with the LDS destination as a 32-bit LDS address (uniform), for
+// kernels that form it once from their __shared__ array.
+__device__ __forceinline__ void dma16_lds(i32x4_rsrc rsrc, uint32_t voff, uint32_t soff,
+                                          uint32_t lds_addr) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  const unsigned l = __builtin_amdgcn_readfirstlane(lds_addr);
+  const unsigned so = __builtin_amdgcn_readfirstlane(soff);
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds" ::"s"(l), "v"(voff),
+               "s"(rsrc), "s"(so)
+               : "memory", "m0");
+#endif
+}
 // 4-byte buffer -> LDS copy (lane l landing at lds_base + 4*l) from byte
 // offset voff of the resource; offsets past its size land as zero.
 __device__ __forceinline__ void dma4_buf(i32x4_rsrc rsrc, uint32_t voff, const void* lds_base) {

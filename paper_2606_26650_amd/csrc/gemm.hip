@@ -420,6 +420,8 @@ struct DmaOpNT {
   uint64_t bytes;        // bytes from panel to the end of the matrix
   uint32_t step;         // bytes between instructions i and i+2 (uniform)
   uint32_t voff[2];      // per lane, instructions of parity 0 and 1
+  i32x4_rsrc rs;         // the tile's rows from the first k of its range
+  int64_t k_first;
   __device__ __forceinline__ void init(const bf16* base, int64_t ld, int64_t row0, int64_t rows,
                                        int wave, int lane) {
     panel = reinterpret_cast<const char*>(base + row0 * ld);
@@ -451,13 +453,19 @@ struct DmaOpNT {
       voff[p] = (uint32_t)(mr * ld * 2 + c * 16);
     }
   }
+  // one resource per tile, from the first k of the tile's contraction range
+  // (the k offset of each copy goes in its scalar offset)
+  __device__ __forceinline__ void bind(int64_t kb, int64_t) {
+    const uint64_t b = (uint64_t)kb * 2;
+    rs = buf_rsrc(panel + b, (uint32_t)min(bytes - b, (uint64_t)0xFFFFFFFFu));
+    k_first = kb;
+  }
   // (K-contiguous rows are whole: the contraction extent is a multiple of 64)
-  __device__ __forceinline__ void issue(uint4* lds, int64_t, int64_t k0, int64_t, int wave) const {
-    const uint64_t kb = (uint64_t)k0 * 2;
-    const i32x4_rsrc r = buf_rsrc(panel + kb, (uint32_t)min(bytes - kb, (uint64_t)0xFFFFFFFFu));
+  __device__ __forceinline__ void issue(uint32_t lds, int64_t k0, int wave) const {
+    const uint32_t ko = (uint32_t)(k0 - k_first) * 2;
 #pragma unroll
     for (int i = 0; i < NI; ++i)
-      dma16_buf(r, voff[i & 1], (uint32_t)(i >> 1) * step, &lds[(wave * NI + i) * 64]);
+      dma16_lds(rs, voff[i & 1], ko + (uint32_t)(i >> 1) * step, lds + (wave * NI + i) * 1024);
   }
   // rows row0 .. row0+31 (lane: row row0 + lane%32), k = 16 kk + 8 (lane/32) .. +7
   __device__ __forceinline__ bf16x8 frag(const uint4* lds, int row0, int kk, int lane) const {
@@ -480,6 +488,8 @@ struct DmaOpKM {
   const char* panel;     // byte address of the tile's first column, row 0 (uniform)
   uint32_t ld2;          // row pitch in bytes
   uint32_t voff[P];      // per lane
+  i32x4_rsrc rs;         // rows kb .. ke - 1 of the tile's columns
+  int64_t k_first;
   __device__ __forceinline__ void init(const bf16* base, int64_t ld, int64_t col0, int64_t,
                                        int wave, int lane) {
     panel = reinterpret_cast<const char*>(base + col0);
@@ -491,14 +501,19 @@ struct DmaOpKM {
       voff[p] = (uint32_t)(row * ld * 2 + c * 16);
     }
   }
-  // rows k0 .. min(k0 + 64, kend) - 1 (rows of the slab at or past kend read as zero)
-  __device__ __forceinline__ void issue(uint4* lds, int64_t ld, int64_t k0, int64_t kend,
-                                        int wave) const {
-    const uint32_t rows = (uint32_t)min((int64_t)64, kend - k0);
-    const i32x4_rsrc r = buf_rsrc(panel + (uint64_t)k0 * ld * 2, rows * ld2);
+  // one resource per tile over rows kb .. ke - 1 (rows at or past ke read as
+  // zero; the host keeps (ke - kb + 64) * ld2 below 2^32)
+  __device__ __forceinline__ void bind(int64_t kb, int64_t ke) {
+    rs = buf_rsrc(panel + (uint64_t)kb * ld2, (uint32_t)((uint64_t)(ke - kb) * ld2));
+    k_first = kb;
+  }
+  // rows k0 .. k0 + 63 of the range
+  __device__ __forceinline__ void issue(uint32_t lds, int64_t k0, int wave) const {
+    const uint32_t ko = (uint32_t)(k0 - k_first) * ld2;
 #pragma unroll
     for (int i = 0; i < NI; ++i)
-      dma16_buf(r, voff[i % P], (uint32_t)((i / P) * P * RPI) * ld2, &lds[(wave * NI + i) * 64]);
+      dma16_lds(rs, voff[i % P], ko + (uint32_t)((i / P) * P * RPI) * ld2,
+                lds + (wave * NI + i) * 1024);
   }
   // columns col0 .. col0+31 (lane: column col0 + lane%32), k = 16 kk + 8 (lane/32) .. +7
   __device__ __forceinline__ bf16x8 frag(const uint4* lds, int col0, int kk, int lane) const {
@@ -626,15 +641,24 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
     ob.init_pairs(Bb, g.ldb, n0, g.N / 2, wave, lane);
   else
     ob.init(Bb, g.ldb, n0, g.N, wave, lane);
+  oa.bind(kb, ke);
+  ob.bind(kb, ke);
+  // LDS byte address of the operand stages (uniform): A's two, then B's SB
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint4*)smem;
   bf16x8 fa[2][FM], fb[2][FN];
-  auto ldfrag = [&](int kt, int kk, int slot) {
+  // stages by index: A's is the k tile's parity, B's is carried along (kt % SB)
+  auto ldfrag = [&](int ast, int bst, int kk, int slot) {
 #pragma unroll
-    for (int i = 0; i < FM; ++i) fa[slot][i] = oa.frag(sA(kt & 1), wm * WTM + 32 * i, kk, lane);
+    for (int i = 0; i < FM; ++i) fa[slot][i] = oa.frag(sA(ast), wm * WTM + 32 * i, kk, lane);
 #pragma unroll
-    for (int j = 0; j < FN; ++j) fb[slot][j] = ob.frag(sB(kt % SB), wn * WTN + 32 * j, kk, lane);
+    for (int j = 0; j < FN; ++j) fb[slot][j] = ob.frag(sB(bst), wn * WTN + 32 * j, kk, lane);
   };
-  auto issueA = [&](int kt) { oa.issue(sA(kt & 1), g.lda, kb + (int64_t)kt * 64, ke, wave); };
-  auto issueB = [&](int kt) { ob.issue(sB(kt % SB), g.ldb, kb + (int64_t)kt * 64, ke, wave); };
+  auto issueA = [&](int kt) {
+    oa.issue(lds0 + (uint32_t)(kt & 1) * (BM * 128), kb + (int64_t)kt * 64, wave);
+  };
+  auto issueB = [&](int kt, int bst) {
+    ob.issue(lds0 + 2 * BM * 128 + (uint32_t)bst * (BN * 128), kb + (int64_t)kt * 64, wave);
+  };
   f32x16 acc[FM][FN];
 #pragma unroll
   for (int i = 0; i < FM; ++i)
@@ -668,18 +692,19 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
   // first reads.  MORE is false only for the last tile (no branches inside
   // the steady-state body, so the interleaving spans it whole).
   const int nk = (int)((ke - kb + 63) / 64);
-  auto tile = [&](int kt, auto more_c) {
+  auto tile = [&](int kt, int bst, auto more_c) {
     constexpr bool MORE = decltype(more_c)::value;
+    const int bnext = bst + 1 == SB ? 0 : bst + 1;     // (kt + 1) % SB
     // copies of tile kt+1 (A; and B with two stages) or kt+2 (B, three
     // stages) into the stages tile kt-1 used; B's copies are issued last, so
     // with three stages waiting for all but B's newest finishes tile kt+1
     if (MORE) issueA(kt + 1);
-    if (SB == 2 && MORE) issueB(kt + 1);
+    if (SB == 2 && MORE) issueB(kt + 1, bnext);
     const bool deep = SB == 3 && kt + 2 < nk;
-    if (deep) issueB(kt + 2);
+    if (deep) issueB(kt + 2, bst == 0 ? SB - 1 : bst - 1);   // (kt + 2) % 3
 #pragma unroll
     for (int kk = 0; kk < 3; ++kk) {
-      ldfrag(kt, kk + 1, (kk & 1) ^ 1);
+      ldfrag(kt & 1, bst, kk + 1, (kk & 1) ^ 1);
       mfmas(kk & 1);
       interleave();
     }
@@ -688,7 +713,7 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
     else
       wait_vmem();
     __syncthreads();
-    if (MORE) ldfrag(kt + 1, 0, 0);
+    if (MORE) ldfrag((kt + 1) & 1, bnext, 0, 0);
     mfmas(1);
     if (MORE) interleave();
   };
@@ -709,18 +734,22 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1)
   };
   if (nk > 0) {
     issueA(0);
-    issueB(0);
+    issueB(0, 0);
     if (SB == 3 && nk > 1) {
-      issueB(1);
+      issueB(1, 1);
       wait_vmem_n<OB::NI>();
     } else {
       wait_vmem();
     }
     __syncthreads();
-    ldfrag(0, 0, 0);
-    for (int kt = 0; kt < nk - 1; ++kt) tile(kt, std::true_type{});
+    ldfrag(0, 0, 0, 0);
+    int bst = 0;
+    for (int kt = 0; kt < nk - 1; ++kt) {
+      tile(kt, bst, std::true_type{});
+      bst = bst + 1 == SB ? 0 : bst + 1;
+    }
     if constexpr (EPI == 3) epi3_load(0);
-    tile(nk - 1, std::false_type{});
+    tile(nk - 1, bst, std::false_type{});
   } else if constexpr (EPI == 3) {
     epi3_load(0);
   }
@@ -1190,6 +1219,9 @@ static bool dma_ok(const GemmLaunch& L, int a_t, int b_t, int bm, int bn) {
   return grouping && g.causal == 0 && g.batch == 1 && (g.group_mode == 2 || g.K % 64 == 0) &&
          (L.ksplit <= 1 || L.kchunk % 64 == 0) && g.lda % 8 == 0 && g.ldb % 8 == 0 &&
          g.lda < (1 << 22) && g.ldb < (1 << 22) &&  // 32-bit buffer offsets within a tile
+         // a K-major operand's resource spans its whole contraction range
+         (a_t == 0 || (uint64_t)(g.K + 64) * (uint64_t)g.lda * 2 < (1ull << 32)) &&
+         (b_t == 0 || (uint64_t)(g.K + 64) * (uint64_t)g.ldb * 2 < (1ull << 32)) &&
          aligned16(g.A) && aligned16(g.B) && (a_t == 0 || g.M % bm == 0) &&
          (b_t == 0 || g.N % bn == 0);
 }
