@@ -128,30 +128,32 @@ def test_ternary_linear_on_finalized_block(catq):
         np.testing.assert_allclose(ref, x @ hard["W_fake"].T, rtol=1e-12, atol=1e-15)
 
 
-@pytest.mark.parametrize("d_out,d_in,M,nw,r", [
-    (16379, 512, 3, 4, 4),     # 1024 tiles of 16 rows: four per workgroup
-    (20473, 384, 2, 4, 5),     # 1280 tiles: five per workgroup
-    (11000, 640, 1, 4, 3),     # 688 tiles: three per workgroup, the last one short
-    (4100, 768, 16, 4, 2),     # under 256 workgroups: two tiles each
-    (300, 9216, 2, 8, 2)])     # rows of 72 chunks: eight waves
-def test_ternary_linear_launch_shapes(catq, d_out, d_in, M, nw, r):
-    """Every launch shape the dispatch picks (2 to 5 row tiles per workgroup,
+@pytest.mark.parametrize("d_out,d_in,M,g,nw,r", [
+    (16379, 512, 3, 128, 4, 4),     # 1024 tiles of 16 rows: four per workgroup
+    (20473, 384, 2, 128, 4, 5),     # 1280 tiles: five per workgroup
+    (11000, 640, 1, 128, 4, 3),     # 688 tiles: three per workgroup, the last one short
+    (4100, 768, 16, 128, 4, 2),     # under 256 workgroups: two tiles each
+    (300, 9216, 2, 128, 8, 2),      # rows of 72 chunks: eight waves
+    (40, 65536, 2, 128, 8, 1),      # the longest rows (512 chunks): one tile per workgroup
+    (24, 40960, 3, 256, 8, 1)])     # 320 chunks, two per scale
+def test_ternary_linear_launch_shapes(catq, d_out, d_in, M, g, nw, r):
+    """Every launch shape the dispatch picks (1 to 5 row tiles per workgroup,
     four or eight waves), each with a ragged last workgroup, against the
     oracle; the trace names the shape that ran."""
     import torch
-    packed, alpha, xb = _case(d_out, d_in, M, 128, 11)
+    packed, alpha, xb = _case(d_out, d_in, M, g, 11)
     catq.catq_trace_enable(8)
     try:
-        y = _run(catq, packed, alpha, xb, 128, torch.float32, ldy_pad=5)
+        y = _run(catq, packed, alpha, xb, g, torch.float32, ldy_pad=5)
         tags = [t["tag"] for t in catq.trace_records()]
     finally:
         catq.catq_trace_disable()
     assert tags and tags[-1].startswith(f"ternary_gemv_kernel<{nw}, {r}, "), tags
     xo = f64(xb)
-    ref = ternary.ternary_linear(xo, packed, alpha, d_in)
+    ref = ternary.ternary_linear(xo, packed, alpha, d_in, g)
     got = host(y)
     assert np.isnan(got[:, d_out:]).all()
-    bound = _bound(xo, packed, alpha, d_in, 128, d_in // 128)
+    bound = _bound(xo, packed, alpha, d_in, g, d_in // 128)
     assert np.all(np.abs(got[:, :d_out] - ref) <= bound), float((np.abs(got[:, :d_out] - ref) / bound).max())
 
 
