@@ -13,6 +13,7 @@ Modules
          2-bit packing
   block  dense decoder-block forward/backward and the reconstruction loss
   moe    routed-expert block forward/backward
-  calib  time-state schedule and AdamW on the factors (parity unpinned:
-         the paper prints no trajectory)
+  calib  time-state schedule and AdamW on the factors (the trajectory's
+         parity is unpinned: the paper prints none; AdamW and the learning
+         rate are pinned against torch and closed forms)
 """

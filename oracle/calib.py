@@ -1,8 +1,12 @@
 """One calibration step end to end, the time-state schedule and AdamW, float64.
 
-Parity of the schedule and optimizer against the paper is UNPINNED: the paper
+Parity of the calibration trajectory against the paper is UNPINNED: the paper
 prints no trajectory, only its hyper-parameters (App. B.1: AdamW, lr 1e-3
-decayed linearly to zero, s0 = 30, gamma = 0.8, Delta0 = 0.5).
+decayed linearly to zero, s0 = 30, gamma = 0.8, Delta0 = 0.5).  The optimizer
+and the learning-rate schedule themselves are pinned independently of this
+module (tests/test_oracle_calib.py: torch's float64 AdamW step by step and over
+a trajectory, the closed-form first step, the clamps, and linear_lr at its end
+points and midpoint).
 """
 from __future__ import annotations
 
