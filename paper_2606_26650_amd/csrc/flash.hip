@@ -178,6 +178,34 @@ __device__ __forceinline__ bf16x8 tfrag_row(const uint4* lds, int row, int chunk
   return *reinterpret_cast<const bf16x8*>(&lds[row * (D / 8) + (chunk ^ tswz<D>(row))]);
 }
 
+// Two independent 32-row accumulation chains over the D/16 slices of d:
+// s[c] += (rows 32c + l32 of a swizzled row-major LDS tile) x b[t].  Each
+// fragment is read PF slices ahead of its products, and a scheduling barrier
+// that only vector and scalar ALU work may cross keeps it there: left alone,
+// the scheduler sinks every read next to its product, and each slice then
+// waits out the whole LDS latency.
+template <int D, int PF>
+__device__ __forceinline__ void chains2(const uint4* lds, const bf16x8 (&b)[D / 16], int l32,
+                                        int g, f32x16 (&s)[2]) {
+  constexpr int KS = D / 16, NB = PF + 1;
+  bf16x8 fr[NB][2];
+#pragma unroll
+  for (int t = 0; t < PF; ++t) {
+    fr[t][0] = tfrag_row<D>(lds, l32, 2 * t + g);
+    fr[t][1] = tfrag_row<D>(lds, 32 + l32, 2 * t + g);
+  }
+#pragma unroll
+  for (int t = 0; t < KS; ++t) {
+    if (t + PF < KS) {
+      fr[(t + PF) % NB][0] = tfrag_row<D>(lds, l32, 2 * (t + PF) + g);
+      fr[(t + PF) % NB][1] = tfrag_row<D>(lds, 32 + l32, 2 * (t + PF) + g);
+    }
+    __builtin_amdgcn_sched_barrier(0x0406);
+    s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[t % NB][0], b[t], s[0], 0, 0, 0);
+    s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[t % NB][1], b[t], s[1], 0, 0, 0);
+  }
+}
+
 // Transposed fragment: column col0 + lane%32, rows 16*slice + 4g + 0..3 then
 // 16*slice + 8 + 4g + 0..3 (g = lane/32): the permuted key order of the
 // score accumulators, read with two transpose loads.
@@ -523,25 +551,12 @@ __device__ __forceinline__ void dkdv_waves(const FaArgs& a, uint4* sQ, uint4* sO
       // barriers are kept (both waves of a slab skip alike)
       const bool active = q0 + fa::BK - 1 >= wave_first;
       // S^T[q][key] (dV waves) or dP^T[q][key] (dK waves) for the two 32-query
-      // blocks: two independent accumulation chains, each fragment read one
-      // step ahead of its products
+      // blocks: two independent accumulation chains
       f32x16 s[2];
       s[0] = fa::zero16();
       s[1] = fa::zero16();
       if (active) {
-        const uint4* src = ROLE == 0 ? tQ : tO;
-        bf16x8 fr[2][2];
-        fr[0][0] = fa::tfrag_row<D>(src, l32, g);
-        fr[0][1] = fa::tfrag_row<D>(src, 32 + l32, g);
-#pragma unroll
-        for (int t = 0; t < C::KS; ++t) {
-          if (t + 1 < C::KS) {
-            fr[(t + 1) & 1][0] = fa::tfrag_row<D>(src, l32, 2 * (t + 1) + g);
-            fr[(t + 1) & 1][1] = fa::tfrag_row<D>(src, 32 + l32, 2 * (t + 1) + g);
-          }
-          s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[t & 1][0], rf[t], s[0], 0, 0, 0);
-          s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[t & 1][1], rf[t], s[1], 0, 0, 0);
-        }
+        fa::chains2<D, 2>(ROLE == 0 ? tQ : tO, rf, l32, g, s);
         if constexpr (ROLE == 0) {
           // P, rows = queries of this lane's registers; the causal / length
           // mask only on the 32 x 32 blocks that cross the slab's diagonal or
@@ -631,12 +646,8 @@ __global__ __launch_bounds__(DKDV_NT, 2) void flash_bwd_dkdv_kernel(FaArgs a) {
   __shared__ uint4 sO[2 * TW];  // dO tiles
   __shared__ __attribute__((aligned(16))) float sL[2 * 64], sD[2 * 64];
   __shared__ __attribute__((aligned(16))) float sP[4 * 2 * 16 * 64];  // P handed from dV to dK waves
-  if (__builtin_amdgcn_readfirstlane(threadIdx.x >> 6) < 4) {
-    // the dV waves issue first: their score chains end early and their
-    // exponentials overlap the dK waves' products
-    __builtin_amdgcn_s_setprio(1);
+  if (__builtin_amdgcn_readfirstlane(threadIdx.x >> 6) < 4)
     dkdv_waves<D, 0>(a, sQ, sO, sL, sD, sP);
-  }
   else
     dkdv_waves<D, 1>(a, sQ, sO, sL, sD, sP);
 }
