@@ -66,8 +66,9 @@ def parse():
                        help="run the step on two streams (weight-gradient halves and the "
                             "finalize on a side stream)")
     ap.add_argument("--ternary", type=int, default=0, metavar="M",
-                    help="only time the packed-ternary decode layers of a Qwen3-14B-shaped "
-                         "block at M tokens (deployment on the 2-bit storage)")
+                    help="only time the packed-ternary layers of a Qwen3-14B-shaped block at M "
+                         "tokens (deployment on the 2-bit storage: decode below 64 tokens, "
+                         "prefill from 64)")
     ap.add_argument("--a8", action="store_true",
                     help="the W1.58A8 setting: activations fake-quantized to 8 bits in the step")
     ap.add_argument("--block", default="qwen3-14b",
@@ -214,11 +215,13 @@ def cpu_baseline(cfg, W, xb, row_frac=1, n_samples=None):
 def ternary_bench(args):
     """Deployment side: the four linears of a Qwen3-14B-shaped block (q|k|v
     7168x5120, o 5120x5120, gate|up 34816x5120, down 5120x17408) as packed
-    ternary weights, applied to M tokens (decode).  Random codes and scales
-    (the product's cost does not depend on their values); inputs resident in
-    HBM.  Reports HBM bytes moved per second (2-bit codes + fp32 scales + X +
-    Y, each once) against the 8 TB/s peak, with torch's bf16 dense product
-    on the same shapes (hipBLASLt) as context."""
+    ternary weights, applied to M tokens.  Random codes and scales (the
+    product's cost does not depend on their values); inputs resident in HBM.
+    At decode sizes (M < 64) it reports HBM bytes moved per second (2-bit
+    codes + fp32 scales + X + Y, each once) against the 8 TB/s peak; at
+    prefill sizes, where the tiled kernel runs, the matrix-core rate
+    (2 M N K flops) against the 2.5 PFLOP/s bf16 peak.  torch's bf16 dense
+    product on the same shapes (hipBLASLt) is timed as context."""
     import numpy as np
     import torch
 
@@ -257,11 +260,14 @@ def ternary_bench(args):
     cq.catq_trace_disable()
     per = {}
     for r, (name, n, k, *_rest) in zip(recs, [l for _ in range(args.steps) for l in layers]):
-        a = per.setdefault(name, {"ms": 0.0, "bytes": r["bytes"], "tag": r["tag"]})
+        a = per.setdefault(name, {"ms": 0.0, "bytes": r["bytes"], "flops": r["flops"],
+                                  "tag": r["tag"]})
         a["ms"] += r["ms"] / args.steps
     tot_bytes = sum(v["bytes"] for v in per.values())
+    tot_flops = sum(v["flops"] for v in per.values())
     tot_ms = sum(v["ms"] for v in per.values())
     big = per["gu"]
+    tiled = big["tag"].startswith("ternary_gemm")
     # context: bf16 dense weights through torch (hipBLASLt), same shapes
     dense = [(torch.randn(n, k, device="cuda", generator=g).to(torch.bfloat16), x)
              for (_, n, k, _, _, x, _) in layers]
@@ -275,10 +281,24 @@ def ternary_bench(args):
             torch.nn.functional.linear(x, w)
     torch.cuda.synchronize()
     dense_ms = 1000.0 * (time.perf_counter() - d0) / args.steps
+    if tiled:
+        ach = big["flops"] / (big["ms"] * 1e-3) / 1e12
+        roof = {"bound": "mfma", "kernel": big["tag"] + " (gate|up 34816x5120)", "achieved": ach,
+                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": ach / PEAK_BF16_TFLOPS,
+                "avg_launch_us": 1000.0 * big["ms"], "flops_per_launch": big["flops"],
+                "traffic": None}
+    else:
+        ach = big["bytes"] / (big["ms"] * 1e-3) / 1e9
+        roof = {"bound": "hbm", "kernel": big["tag"] + " (gate|up 34816x5120)", "achieved": ach,
+                "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": ach / PEAK_HBM_GBS,
+                "avg_launch_us": 1000.0 * big["ms"], "bytes_per_launch": big["bytes"],
+                "traffic": None}
     out = {
-        "metric": "packed-ternary decode: HBM GB/s of the 2-bit linear layers",
-        "value": tot_bytes / (tot_ms * 1e-3) / 1e9,
-        "unit": "GB/s",
+        "metric": ("packed-ternary prefill: matrix-core TFLOP/s of the 2-bit linear layers" if tiled
+                   else "packed-ternary decode: HBM GB/s of the 2-bit linear layers"),
+        "value": (tot_flops / (tot_ms * 1e-3) / 1e12 if tiled
+                  else tot_bytes / (tot_ms * 1e-3) / 1e9),
+        "unit": "TFLOP/s" if tiled else "GB/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": 1000.0 * elapsed / args.steps,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
@@ -286,13 +306,9 @@ def ternary_bench(args):
         "config": {"workload": f"qwen3-14b-shaped block linears (q|k|v, o, gate|up, down) as "
                                f"2-bit ternary + fp32 group scales, {M} token(s)",
                    "tokens": M, "weights": sum(n * k for _, n, k in shapes), "group_size": 128},
-        "roofline": {"bound": "hbm", "kernel": big["tag"] + " (gate|up 34816x5120)",
-                     "achieved": big["bytes"] / (big["ms"] * 1e-3) / 1e9, "peak": PEAK_HBM_GBS,
-                     "unit": "GB/s",
-                     "frac": big["bytes"] / (big["ms"] * 1e-3) / 1e9 / PEAK_HBM_GBS,
-                     "avg_launch_us": 1000.0 * big["ms"], "bytes_per_launch": big["bytes"],
-                     "traffic": None},
-        "per_layer": {k: {"us": 1000.0 * v["ms"], "GB/s": v["bytes"] / (v["ms"] * 1e-3) / 1e9}
+        "roofline": roof,
+        "per_layer": {k: {"us": 1000.0 * v["ms"], "GB/s": v["bytes"] / (v["ms"] * 1e-3) / 1e9,
+                          "TFLOP/s": v["flops"] / (v["ms"] * 1e-3) / 1e12, "kernel": v["tag"]}
                       for k, v in per.items()},
         "bf16_dense_torch_ms_per_step": dense_ms,
         "kernel_ms_per_step": tot_ms,

@@ -257,6 +257,184 @@ void ternary_gemv_kernel(TernArgs a) {
   }
 }
 
+// Prefill-sized M: one workgroup = a tile of 128 weight rows x 128 tokens on
+// four waves (2 x 2, each 64 rows x 64 tokens), so a row's codes are decoded
+// once per 128 tokens instead of once per 16.  Per 128-code chunk:
+//  * the tile's X chunk (128 tokens x 128 k, bf16) arrives by direct copies
+//    into a double-buffered LDS tile [token][16 slots of 8 k], slot s of
+//    token t holding global slot s ^ (t & 15) (conflict-free fragment reads);
+//  * a lane loads 32 bytes of codes of each of its two weight rows (one per
+//    32-row block) and turns the half it needs of each word pair into two
+//    MFMA operands (decode16 after one byte permute), in the natural k
+//    order that the X fragments (16 bytes of a token row) share;
+//  * eight k-steps of four v_mfma_f32_32x32x16_bf16 form the chunk's partial
+//    products, which are scaled by the rows' alpha/2 (staged in LDS per
+//    chunk) and accumulated in fp32, as in the decode kernel.
+// The next chunk's copies, codes and scales are issued before the current
+// chunk is multiplied.  Rows past d_out read zero codes and tokens past M
+// zero X; neither is stored.  X offsets are 32-bit: 128 * ldx * 2 < 2^32.
+constexpr int kGT = 128;
+
+template <typename OutT>
+__global__ __launch_bounds__(256, 2) void ternary_gemm_kernel(TernArgs a) {
+  __shared__ __align__(16) uint4 s_x[2][kGT * 16];  // [buffer][token * 16 + slot]
+  __shared__ __align__(16) float s_al[2][kGT];      // [buffer][row]: alpha/2 of one chunk
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wr = wave & 1, wc = wave >> 1;  // 64-row and 64-token half of the tile
+  const int h = lane >> 5, l32 = lane & 31;
+  const int64_t n0 = (int64_t)blockIdx.x * kGT, m0 = (int64_t)blockIdx.y * kGT;
+  const int nch = a.n_chunks;
+  const int64_t row_bytes = a.d_in >> 2;
+  const int tok_here = (int)min<int64_t>(kGT, a.M - m0);
+  const int rows_here = (int)min<int64_t>(kGT, a.d_out - n0);
+  const int ng = nch >> a.cpg_shift;
+
+  // X copies: wave w fills tokens 32 w .. 32 w + 31, four per instruction;
+  // the lane's part of the offset repeats every four instructions (the
+  // swizzle key is t & 15), the rest is uniform
+  const i32x4_rsrc xr = buf_rsrc(a.X + m0 * a.ldx, (uint32_t)(tok_here * a.ldx * 2));
+  uint32_t xl[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int tq = lane >> 4, slot = lane & 15;
+    xl[j] = (uint32_t)(tq * a.ldx * 2) + (uint32_t)((slot ^ ((4 * j + tq) & 15)) * 16);
+  }
+  const uint32_t xlds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint4*)&s_x[0][0];
+  const uint32_t xrow = (uint32_t)(a.ldx * 2);
+  // codes of the lane's rows 64 wr + 32 rb + l32
+  const __amdgpu_buffer_rsrc_t pr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(a.P + n0 * row_bytes), 0, (int)(rows_here * row_bytes), kBufferFlags);
+  uint32_t poff[2];
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb) poff[rb] = (uint32_t)((64 * wr + 32 * rb + l32) * row_bytes);
+  // scales: thread t < 128 takes row t of the tile
+  const __amdgpu_buffer_rsrc_t ar = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(a.A + n0 * ng), 0, rows_here * ng * 4, kBufferFlags);
+  const uint32_t aoff = (uint32_t)(min(tid, kGT - 1) * ng * 4);
+
+  auto issue_x = [&](int c, int buf) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      dma16_lds(xr, xl[i & 3], (uint32_t)c * 256u + (uint32_t)(32 * wave + 4 * i) * xrow,
+                xlds0 + (uint32_t)(buf * kGT * 16 + (32 * wave + 4 * i) * 16) * 16u);
+  };
+  u32x4 cw[2][2], cn[2][2];  // codes of this chunk and of the next: [row block][16-byte half]
+  auto load_codes = [&](int c, u32x4 (&dst)[2][2]) {
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        dst[rb][j] = __builtin_amdgcn_raw_buffer_load_b128(pr, (int)(poff[rb] + 16 * j), c * 32, 0);
+  };
+  auto load_alpha = [&](int c) {
+    return __builtin_bit_cast(
+        float, __builtin_amdgcn_raw_buffer_load_b32(ar, (int)(aoff + (uint32_t)(c >> a.cpg_shift) * 4u),
+                                                    0, 0));
+  };
+  // vmcnt(0) as an s_waitcnt the compiler sees: the copies above are inline
+  // assembly it does not count, so its own waits for the codes must know
+  // that everything issued before has landed
+  auto wait_all_vmem = [] { __builtin_amdgcn_s_waitcnt(0x0F70); };
+
+  issue_x(0, 0);
+  load_codes(0, cw);
+  float av = load_alpha(0);
+  wait_all_vmem();
+  if (tid < kGT) s_al[0][tid] = 0.5f * av;
+  __syncthreads();
+
+  f32x16 out[2][2];
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) out[rb][cb][r] = 0.f;
+  const uint32_t sel = h ? 0x07060302u : 0x05040100u;  // the lane's 16-bit half of two words
+  int tr[2];
+#pragma unroll
+  for (int cb = 0; cb < 2; ++cb) tr[cb] = 64 * wc + 32 * cb + l32;
+
+  for (int c = 0; c < nch; ++c) {
+    const int buf = c & 1;
+    if (c + 1 < nch) {
+      issue_x(c + 1, buf ^ 1);
+      load_codes(c + 1, cn);
+      av = load_alpha(c + 1);
+    }
+    const uint4* xt = s_x[buf];
+    f32x16 acc[2][2];
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      bf16x8 A[2][2];  // [row block][k step of the pair]
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb) {
+        const u32x4& q = cw[rb][p >> 1];
+        const uint32_t t = __builtin_amdgcn_perm(q[(2 * p + 1) & 3], q[(2 * p) & 3], sel);
+        u32x4 lo, hi;
+        decode16(t, lo, hi);
+        A[rb][0] = as_bf16x8(lo);
+        A[rb][1] = as_bf16x8(hi);
+      }
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const int st = 2 * p + e;
+        bf16x8 B[2];
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb)
+          B[cb] = __builtin_bit_cast(bf16x8, xt[tr[cb] * 16 + ((2 * st + h) ^ (tr[cb] & 15))]);
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+          for (int cb = 0; cb < 2; ++cb)
+            acc[rb][cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                A[rb][e], B[cb], st == 0 ? f32x16{} : acc[rb][cb], 0, 0, 0);
+      }
+    }
+    // out += (alpha/2 of the accumulator's rows) * acc; register r holds row
+    // 8 (r / 4) + 4 h + r % 4 of its 32-row block
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+      for (int qd = 0; qd < 4; ++qd) {
+        const f32x4 sc =
+            *reinterpret_cast<const f32x4*>(&s_al[buf][64 * wr + 32 * rb + 8 * qd + 4 * h]);
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            out[rb][cb][4 * qd + e] = fmaf(sc[e], acc[rb][cb][4 * qd + e], out[rb][cb][4 * qd + e]);
+      }
+    // the next chunk's copies, codes and scale have landed; this chunk's
+    // buffers are free once every wave has passed the barrier
+    wait_all_vmem();
+    if (c + 1 < nch) {
+      if (tid < kGT) s_al[buf ^ 1][tid] = 0.5f * av;
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) cw[rb][j] = cn[rb][j];
+    }
+    __syncthreads();
+  }
+
+  // Y[token][row]: lane column = token 64 wc + 32 cb + l32, register r = row
+#pragma unroll
+  for (int cb = 0; cb < 2; ++cb) {
+    const int tok = tr[cb];
+    if (tok >= tok_here) continue;
+    OutT* yrow = reinterpret_cast<OutT*>(a.Y) + (m0 + tok) * a.ldy + n0;
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = 64 * wr + 32 * rb + 8 * (r >> 2) + 4 * h + (r & 3);
+        if (row < rows_here) store1<OutT>(yrow + row, out[rb][cb][r]);
+      }
+  }
+}
+
 template <typename T>
 struct OutTag {
   using type = T;
@@ -297,6 +475,26 @@ catq_status launch_tern(const TernArgs& a, catq_dtype y_dtype, hipStream_t strea
     if (vec) launch(Vt{}, OutTag<bf16>{});
     else launch(Vf{}, OutTag<bf16>{});
   }
+  CATQ_CHECK_LAUNCH("ternary_linear");
+  return CATQ_OK;
+}
+
+// tokens from which the tiled kernel takes over
+constexpr int64_t kGemmMinM = 64;
+
+catq_status launch_tern_gemm(const TernArgs& a, catq_dtype y_dtype, hipStream_t stream) {
+  const dim3 grid((unsigned)((a.d_out + kGT - 1) / kGT), (unsigned)((a.M + kGT - 1) / kGT));
+  const double flops = 2.0 * (double)a.M * (double)a.d_out * (double)a.d_in;
+  const double bytes = (double)grid.y * ((double)a.d_out * (double)a.d_in / 4.0 +
+                                         4.0 * (double)a.d_out * (double)(a.n_chunks >> a.cpg_shift)) +
+                       2.0 * (double)a.M * (double)a.d_in +
+                       (double)a.M * (double)a.d_out * (y_dtype == CATQ_F32 ? 4.0 : 2.0);
+  if (y_dtype == CATQ_F32)
+    CATQ_TRACED(stream, "ternary_gemm_kernel<128, 128>", flops, bytes, a.M, a.d_out, a.d_in,
+                hipLaunchKernelGGL(ternary_gemm_kernel<float>, grid, dim3(256), 0, stream, a));
+  else
+    CATQ_TRACED(stream, "ternary_gemm_kernel<128, 128>", flops, bytes, a.M, a.d_out, a.d_in,
+                hipLaunchKernelGGL(ternary_gemm_kernel<bf16>, grid, dim3(256), 0, stream, a));
   CATQ_CHECK_LAUNCH("ternary_linear");
   return CATQ_OK;
 }
@@ -343,6 +541,9 @@ extern "C" catq_status catq_ternary_linear(const void* X, int64_t M, int64_t ldx
   a.n_chunks = (int32_t)(d_in / 128);
   a.cpg_shift = __builtin_ctz((unsigned)(g / 128));
   a.Y = Y;
+  // From kGemmMinM tokens on, 128 x 128 tiles decode each code once per 128
+  // tokens (their X offsets need 128 * ldx * 2 < 2^32).
+  if (M >= kGemmMinM && ldx <= (1 << 23)) return launch_tern_gemm(a, y_dtype, stream);
   // The product is bound by the decode's vector instructions, so what
   // matters is the work of the fullest compute unit: the workgroups it gets,
   // ceil(workgroups / 256), times what one costs, R tiles of 16 rows plus the

@@ -3,10 +3,11 @@ storage) against the oracle's product of the decoded weights.
 
 Bound (fp32 output): every product x * 2T is exact in fp32 and the kernel
 sums them in fp32 (128 per chunk inside the matrix core), scales each chunk
-once by alpha/2 and adds the chunks and the waves' partials: at most
-128 + 1 + n_chunks + 16 roundings on any path, so |y - ref| <=
-(145 + n_chunks) * 2^-24 * sum_k |x_k alpha_k T_k|.  bf16 output adds one
-rounding to 8 significant bits, at most 2^-8 |y|."""
+once by alpha/2 and adds the chunks and (decode-sized M) the waves'
+partials: at most 128 + 1 + n_chunks + 16 roundings on any path, so
+|y - ref| <= (145 + n_chunks) * 2^-24 * sum_k |x_k alpha_k T_k|.  The tiled
+kernel for prefill-sized M has no wave partials, so the same bound holds.
+bf16 output adds one rounding to 8 significant bits, at most 2^-8 |y|."""
 import numpy as np
 import pytest
 
@@ -157,13 +158,70 @@ def test_ternary_linear_launch_shapes(catq, d_out, d_in, M, g, nw, r):
     assert np.all(np.abs(got[:, :d_out] - ref) <= bound), float((np.abs(got[:, :d_out] - ref) / bound).max())
 
 
+def _traced_run(catq, packed, alpha, xb, g, y_dtype, **pad):
+    catq.catq_trace_enable(8)
+    try:
+        y = _run(catq, packed, alpha, xb, g, y_dtype, **pad)
+        tags = [t["tag"] for t in catq.trace_records()]
+    finally:
+        catq.catq_trace_disable()
+    return y, tags
+
+
+@pytest.mark.parametrize("d_out,d_in,M,g", [
+    (130, 256, 64, 128),       # the fewest tokens the tiled kernel takes; ragged rows
+    (200, 384, 150, 128),      # ragged rows and tokens (two token tiles)
+    (257, 1024, 300, 256),     # two chunks per scale, three token tiles
+    (64, 2048, 129, 512),      # four chunks per scale, one token into a second tile
+    (384, 65536, 70, 128)])    # the longest rows: 512 chunks
+def test_ternary_linear_tiled_parity(catq, d_out, d_in, M, g):
+    """Prefill-sized M: the kernel of 128-row x 128-token tiles (named by the
+    trace), with padded X and Y rows, against the oracle."""
+    import torch
+    packed, alpha, xb = _case(d_out, d_in, M, g, 12)
+    y, tags = _traced_run(catq, packed, alpha, xb, g, torch.float32, ldx_pad=8, ldy_pad=3)
+    assert tags and tags[-1].startswith("ternary_gemm_kernel<128, 128>"), tags
+    xo = f64(xb)
+    ref = ternary.ternary_linear(xo, packed, alpha, d_in, g)
+    got = host(y)
+    assert np.isnan(got[:, d_out:]).all()
+    bound = _bound(xo, packed, alpha, d_in, g, d_in // 128)
+    err = np.abs(got[:, :d_out] - ref)
+    assert np.all(err <= bound), float((err / bound).max())
+
+
+def test_ternary_linear_tiled_bf16_output_and_determinism(catq):
+    import torch
+    packed, alpha, xb = _case(300, 1536, 200, 128, 13)
+    y, tags = _traced_run(catq, packed, alpha, xb, 128, torch.bfloat16)
+    assert tags[-1].startswith("ternary_gemm_kernel<128, 128>"), tags
+    xo = f64(xb)
+    ref = ternary.ternary_linear(xo, packed, alpha, 1536)
+    bound = _bound(xo, packed, alpha, 1536, 128, 12) * (1 + 2.0 ** -8) + 2.0 ** -8 * np.abs(ref)
+    assert np.all(np.abs(host(y) - ref) <= bound)
+    y2 = _run(catq, packed, alpha, xb, 128, torch.bfloat16)
+    assert torch.equal(y, y2)
+
+
+def test_ternary_linear_tiled_invalid_codes(catq):
+    import torch
+    packed, alpha, xb = _case(160, 512, 96, 128, 14)
+    packed[129] = 0xFF                               # a row of invalid codes -> 0
+    y, _ = _traced_run(catq, packed, alpha, xb, 128, torch.float32)
+    assert not torch.any(y[:, 129])
+    ref = ternary.ternary_linear(f64(xb), packed, alpha, 512)
+    assert np.all(np.abs(host(y) - ref) <= _bound(f64(xb), packed, alpha, 512, 128, 4))
+
+
 @pytest.mark.slow
 @pytest.mark.parametrize("d_out,d_in,M", [(34816, 5120, 1), (5120, 17408, 1), (7168, 5120, 8),
-                                          (34816, 5120, 16)])
+                                          (34816, 5120, 16), (34816, 5120, 512),
+                                          (5120, 17408, 300)])
 def test_ternary_linear_full_size_sampled(catq, d_out, d_in, M):
-    """Qwen3-14B-shaped layers (gate|up, down, q|k|v) at decode sizes, in the
-    launch configuration the benchmark times: sampled output rows against
-    the oracle (computed for those rows only)."""
+    """Qwen3-14B-shaped layers (gate|up, down, q|k|v) at decode sizes and at
+    prefill sizes (the tiled kernel), in the launch configurations the
+    benchmark times: sampled output rows against the oracle (computed for
+    those rows only)."""
     import torch
     rng = np.random.default_rng([9, d_out, d_in, M])
     packed = rng.integers(0, 256, (d_out, d_in // 4), dtype=np.uint8)   # code 3 -> 0 included
