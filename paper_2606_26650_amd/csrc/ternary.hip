@@ -479,8 +479,23 @@ catq_status launch_tern(const TernArgs& a, catq_dtype y_dtype, hipStream_t strea
   return CATQ_OK;
 }
 
-// tokens from which the tiled kernel takes over
-constexpr int64_t kGemmMinM = 64;
+// Which kernel: below 32 tokens always the decode kernel.  From there a
+// cost model fitted to both kernels on MI355X picks the cheaper:
+//  * tiled: every workgroup runs all n_chunks chunks at ~1.45 us each, one
+//    round per 256 workgroups (fewer than 256 still take a whole round);
+//  * decode: ~7.5e-15 s per weight and token (rows over 64 chunks, whose
+//    workgroups take eight waves, ~11e-15 s).
+// 14B-shaped layers at 64 / 128 / 256 / 512 tokens: gate|up tiled from 64,
+// q|k|v and down from 256, o from 512; at 256 tokens o measured 52.6 us
+// decode against 67.3 tiled, down 265 against 195.
+bool use_tiled(const TernArgs& a) {
+  if (a.M < 32 || a.ldx > (1 << 23)) return false;
+  const double wgs = (double)((a.d_out + kGT - 1) / kGT) * (double)((a.M + kGT - 1) / kGT);
+  const double tiled_us = a.n_chunks * 1.45 * (wgs > 256.0 ? wgs / 256.0 : 1.0);
+  const double decode_us =
+      (double)a.M * (double)a.d_out * (double)a.d_in * (a.n_chunks > 64 ? 11e-9 : 7.5e-9);
+  return tiled_us < decode_us;
+}
 
 catq_status launch_tern_gemm(const TernArgs& a, catq_dtype y_dtype, hipStream_t stream) {
   const dim3 grid((unsigned)((a.d_out + kGT - 1) / kGT), (unsigned)((a.M + kGT - 1) / kGT));
@@ -541,9 +556,9 @@ extern "C" catq_status catq_ternary_linear(const void* X, int64_t M, int64_t ldx
   a.n_chunks = (int32_t)(d_in / 128);
   a.cpg_shift = __builtin_ctz((unsigned)(g / 128));
   a.Y = Y;
-  // From kGemmMinM tokens on, 128 x 128 tiles decode each code once per 128
-  // tokens (their X offsets need 128 * ldx * 2 < 2^32).
-  if (M >= kGemmMinM && ldx <= (1 << 23)) return launch_tern_gemm(a, y_dtype, stream);
+  // Prefill-sized M: 128 x 128 tiles decode each code once per 128 tokens
+  // (their X offsets need 128 * ldx * 2 < 2^32).
+  if (use_tiled(a)) return launch_tern_gemm(a, y_dtype, stream);
   // The product is bound by the decode's vector instructions, so what
   // matters is the work of the fullest compute unit: the workgroups it gets,
   // ceil(workgroups / 256), times what one costs, R tiles of 16 rows plus the

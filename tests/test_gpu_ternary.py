@@ -168,49 +168,76 @@ def _traced_run(catq, packed, alpha, xb, g, y_dtype, **pad):
     return y, tags
 
 
+def _tile_rows(d_out, rng, n=48):
+    """Sampled output rows: both ends of every 128-row tile near the first,
+    the last rows, and random ones."""
+    edges = [r for t in range(0, d_out, 128)[:4] for r in (t, t + 127)] + [d_out - 2, d_out - 1]
+    return np.unique(np.clip(np.concatenate([edges, rng.choice(d_out, n, replace=False)]),
+                             0, d_out - 1))
+
+
+# shapes on which the dispatch picks the tiled kernel (its cost model needs
+# about 1.5e6 output rows x tokens at rows of up to 64 chunks)
 @pytest.mark.parametrize("d_out,d_in,M,g", [
-    (130, 256, 64, 128),       # the fewest tokens the tiled kernel takes; ragged rows
-    (200, 384, 150, 128),      # ragged rows and tokens (two token tiles)
-    (257, 1024, 300, 256),     # two chunks per scale, three token tiles
-    (64, 2048, 129, 512),      # four chunks per scale, one token into a second tile
-    (384, 65536, 70, 128)])    # the longest rows: 512 chunks
+    (4100, 384, 400, 128),     # ragged row and token tiles
+    (2000, 1024, 900, 256),    # two chunks per scale, eight token tiles (the last ragged)
+    (1600, 2048, 1000, 512),   # four chunks per scale
+    (640, 65536, 1700, 128)])  # the longest rows (512 chunks), 14 token tiles
 def test_ternary_linear_tiled_parity(catq, d_out, d_in, M, g):
     """Prefill-sized M: the kernel of 128-row x 128-token tiles (named by the
-    trace), with padded X and Y rows, against the oracle."""
+    trace), with padded X and Y rows, against the oracle on sampled rows."""
     import torch
     packed, alpha, xb = _case(d_out, d_in, M, g, 12)
     y, tags = _traced_run(catq, packed, alpha, xb, g, torch.float32, ldx_pad=8, ldy_pad=3)
     assert tags and tags[-1].startswith("ternary_gemm_kernel<128, 128>"), tags
-    xo = f64(xb)
-    ref = ternary.ternary_linear(xo, packed, alpha, d_in, g)
     got = host(y)
-    assert np.isnan(got[:, d_out:]).all()
-    bound = _bound(xo, packed, alpha, d_in, g, d_in // 128)
-    err = np.abs(got[:, :d_out] - ref)
+    assert np.isnan(got[:, d_out:]).all() and not np.isnan(got[:, :d_out]).any()
+    rows = _tile_rows(d_out, np.random.default_rng([d_out, M]))
+    xo = f64(xb)
+    ref = ternary.ternary_linear(xo, packed[rows], alpha[rows], d_in, g)
+    bound = _bound(xo, packed[rows], alpha[rows], d_in, g, d_in // 128)
+    err = np.abs(got[:, rows] - ref)
     assert np.all(err <= bound), float((err / bound).max())
 
 
 def test_ternary_linear_tiled_bf16_output_and_determinism(catq):
     import torch
-    packed, alpha, xb = _case(300, 1536, 200, 128, 13)
+    packed, alpha, xb = _case(4100, 384, 400, 128, 13)
     y, tags = _traced_run(catq, packed, alpha, xb, 128, torch.bfloat16)
     assert tags[-1].startswith("ternary_gemm_kernel<128, 128>"), tags
+    rows = _tile_rows(4100, np.random.default_rng(13))
     xo = f64(xb)
-    ref = ternary.ternary_linear(xo, packed, alpha, 1536)
-    bound = _bound(xo, packed, alpha, 1536, 128, 12) * (1 + 2.0 ** -8) + 2.0 ** -8 * np.abs(ref)
-    assert np.all(np.abs(host(y) - ref) <= bound)
+    ref = ternary.ternary_linear(xo, packed[rows], alpha[rows], 384)
+    bound = (_bound(xo, packed[rows], alpha[rows], 384, 128, 3) * (1 + 2.0 ** -8)
+             + 2.0 ** -8 * np.abs(ref))
+    assert np.all(np.abs(host(y)[:, rows] - ref) <= bound)
     y2 = _run(catq, packed, alpha, xb, 128, torch.bfloat16)
     assert torch.equal(y, y2)
 
 
 def test_ternary_linear_tiled_invalid_codes(catq):
     import torch
-    packed, alpha, xb = _case(160, 512, 96, 128, 14)
+    packed, alpha, xb = _case(4100, 512, 400, 128, 14)
     packed[129] = 0xFF                               # a row of invalid codes -> 0
-    y, _ = _traced_run(catq, packed, alpha, xb, 128, torch.float32)
+    y, tags = _traced_run(catq, packed, alpha, xb, 128, torch.float32)
+    assert tags[-1].startswith("ternary_gemm_kernel<128, 128>"), tags
     assert not torch.any(y[:, 129])
-    ref = ternary.ternary_linear(f64(xb), packed, alpha, 512)
-    assert np.all(np.abs(host(y) - ref) <= _bound(f64(xb), packed, alpha, 512, 128, 4))
+    rows = np.array([0, 128, 129, 130, 4099])
+    ref = ternary.ternary_linear(f64(xb), packed[rows], alpha[rows], 512)
+    assert np.all(np.abs(host(y)[:, rows] - ref) <= _bound(f64(xb), packed[rows], alpha[rows],
+                                                           512, 128, 4))
+
+
+def test_ternary_linear_kernel_choice(catq):
+    """Decode sizes stay on the decode kernel; the 14B-shaped gate|up takes
+    the tiled one from 64 tokens."""
+    import torch
+    for d_out, d_in, M, tiled in ((48, 384, 40, False), (34816, 5120, 16, False),
+                                  (34816, 5120, 64, True)):
+        packed, alpha, xb = _case(d_out, d_in, M, 128, 15)
+        _, tags = _traced_run(catq, packed, alpha, xb, 128, torch.float32)
+        assert tags[-1].startswith("ternary_gemm_kernel" if tiled else "ternary_gemv_kernel"), \
+            (d_out, d_in, M, tags)
 
 
 @pytest.mark.slow
