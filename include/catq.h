@@ -283,7 +283,7 @@ catq_status catq_ternarize_pack(const void* W, catq_dtype w_dtype, int64_t d_out
  * M = 0 is a no-op.  Accumulation in fp32 in a fixed order (bitwise
  * deterministic for a given shape).  Decode-sized M re-reads the codes per
  * 16 tokens; from 32 tokens on, where it is estimated cheaper, a kernel of
- * 128-row x 128-token tiles decodes each code once per 128 tokens (same
+ * 128-row x 64- or 128-token tiles decodes each code once per tile (same
  * per-chunk fp32 scaling, so the same error bound).  X and alpha 16-byte
  * aligned, packed 8-byte, Y 4-byte. */
 catq_status catq_ternary_linear(const void* X, int64_t M, int64_t ldx, const uint8_t* packed,

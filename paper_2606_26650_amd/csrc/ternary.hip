@@ -20,6 +20,7 @@
 // the decode is exact) and accumulated in fp32.  The scales of the
 // workgroup's rows are staged in LDS once.
 
+#include <cmath>
 #include <cstdint>
 #include <type_traits>
 
@@ -257,10 +258,12 @@ void ternary_gemv_kernel(TernArgs a) {
   }
 }
 
-// Prefill-sized M: one workgroup = a tile of 128 weight rows x 128 tokens on
-// four waves (2 x 2, each 64 rows x 64 tokens), so a row's codes are decoded
-// once per 128 tokens instead of once per 16.  Per 128-code chunk:
-//  * the tile's X chunk (128 tokens x 128 k, bf16) arrives by direct copies
+// Prefill-sized M: one workgroup = a tile of 128 weight rows x TT tokens
+// (TT = 128 or 64) on four waves (2 x 2, each 64 rows x TT/2 tokens), so a
+// row's codes are decoded once per TT tokens instead of once per 16.  The
+// 64-token tiles need fewer registers (three workgroups per compute unit
+// instead of two) and give more workgroups on few rows.  Per 128-code chunk:
+//  * the tile's X chunk (TT tokens x 128 k, bf16) arrives by direct copies
 //    into a double-buffered LDS tile [token][16 slots of 8 k], slot s of
 //    token t holding global slot s ^ (t & 15) (conflict-free fragment reads);
 //  * a lane loads 32 bytes of codes of each of its two weight rows (one per
@@ -275,22 +278,24 @@ void ternary_gemv_kernel(TernArgs a) {
 // zero X; neither is stored.  X offsets are 32-bit: 128 * ldx * 2 < 2^32.
 constexpr int kGT = 128;
 
-template <typename OutT>
-__global__ __launch_bounds__(256, 2) void ternary_gemm_kernel(TernArgs a) {
-  __shared__ __align__(16) uint4 s_x[2][kGT * 16];  // [buffer][token * 16 + slot]
+template <int TT, typename OutT>
+__global__ __launch_bounds__(256, TT == 128 ? 2 : 3) void ternary_gemm_kernel(TernArgs a) {
+  constexpr int CB = TT / 64;    // 32-token blocks per wave
+  constexpr int NI = TT / 16;    // copy instructions per wave and chunk
+  __shared__ __align__(16) uint4 s_x[2][TT * 16];   // [buffer][token * 16 + slot]
   __shared__ __align__(16) float s_al[2][kGT];      // [buffer][row]: alpha/2 of one chunk
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wr = wave & 1, wc = wave >> 1;  // 64-row and 64-token half of the tile
+  const int wr = wave & 1, wc = wave >> 1;  // 64-row and TT/2-token half of the tile
   const int h = lane >> 5, l32 = lane & 31;
-  const int64_t n0 = (int64_t)blockIdx.x * kGT, m0 = (int64_t)blockIdx.y * kGT;
+  const int64_t n0 = (int64_t)blockIdx.x * kGT, m0 = (int64_t)blockIdx.y * TT;
   const int nch = a.n_chunks;
   const int64_t row_bytes = a.d_in >> 2;
-  const int tok_here = (int)min<int64_t>(kGT, a.M - m0);
+  const int tok_here = (int)min<int64_t>(TT, a.M - m0);
   const int rows_here = (int)min<int64_t>(kGT, a.d_out - n0);
   const int ng = nch >> a.cpg_shift;
 
-  // X copies: wave w fills tokens 32 w .. 32 w + 31, four per instruction;
+  // X copies: wave w fills tokens TT/4 w .. TT/4 (w + 1) - 1, four per instruction;
   // the lane's part of the offset repeats every four instructions (the
   // swizzle key is t & 15), the rest is uniform
   const i32x4_rsrc xr = buf_rsrc(a.X + m0 * a.ldx, (uint32_t)(tok_here * a.ldx * 2));
@@ -315,9 +320,9 @@ __global__ __launch_bounds__(256, 2) void ternary_gemm_kernel(TernArgs a) {
 
   auto issue_x = [&](int c, int buf) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
-      dma16_lds(xr, xl[i & 3], (uint32_t)c * 256u + (uint32_t)(32 * wave + 4 * i) * xrow,
-                xlds0 + (uint32_t)(buf * kGT * 16 + (32 * wave + 4 * i) * 16) * 16u);
+    for (int i = 0; i < NI; ++i)
+      dma16_lds(xr, xl[i & 3], (uint32_t)c * 256u + (uint32_t)(TT / 4 * wave + 4 * i) * xrow,
+                xlds0 + (uint32_t)(buf * TT * 16 + (TT / 4 * wave + 4 * i) * 16) * 16u);
   };
   u32x4 cw[2][2], cn[2][2];  // codes of this chunk and of the next: [row block][16-byte half]
   auto load_codes = [&](int c, u32x4 (&dst)[2][2]) {
@@ -344,17 +349,17 @@ __global__ __launch_bounds__(256, 2) void ternary_gemm_kernel(TernArgs a) {
   if (tid < kGT) s_al[0][tid] = 0.5f * av;
   __syncthreads();
 
-  f32x16 out[2][2];
+  f32x16 out[2][CB];
 #pragma unroll
   for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
-    for (int cb = 0; cb < 2; ++cb)
+    for (int cb = 0; cb < CB; ++cb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) out[rb][cb][r] = 0.f;
   const uint32_t sel = h ? 0x07060302u : 0x05040100u;  // the lane's 16-bit half of two words
-  int tr[2];
+  int tr[CB];
 #pragma unroll
-  for (int cb = 0; cb < 2; ++cb) tr[cb] = 64 * wc + 32 * cb + l32;
+  for (int cb = 0; cb < CB; ++cb) tr[cb] = TT / 2 * wc + 32 * cb + l32;
 
   for (int c = 0; c < nch; ++c) {
     const int buf = c & 1;
@@ -364,7 +369,7 @@ __global__ __launch_bounds__(256, 2) void ternary_gemm_kernel(TernArgs a) {
       av = load_alpha(c + 1);
     }
     const uint4* xt = s_x[buf];
-    f32x16 acc[2][2];
+    f32x16 acc[2][CB];
 #pragma unroll
     for (int p = 0; p < 4; ++p) {
       bf16x8 A[2][2];  // [row block][k step of the pair]
@@ -380,14 +385,14 @@ __global__ __launch_bounds__(256, 2) void ternary_gemm_kernel(TernArgs a) {
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
         const int st = 2 * p + e;
-        bf16x8 B[2];
+        bf16x8 B[CB];
 #pragma unroll
-        for (int cb = 0; cb < 2; ++cb)
+        for (int cb = 0; cb < CB; ++cb)
           B[cb] = __builtin_bit_cast(bf16x8, xt[tr[cb] * 16 + ((2 * st + h) ^ (tr[cb] & 15))]);
 #pragma unroll
         for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
-          for (int cb = 0; cb < 2; ++cb)
+          for (int cb = 0; cb < CB; ++cb)
             acc[rb][cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
                 A[rb][e], B[cb], st == 0 ? f32x16{} : acc[rb][cb], 0, 0, 0);
       }
@@ -401,7 +406,7 @@ __global__ __launch_bounds__(256, 2) void ternary_gemm_kernel(TernArgs a) {
         const f32x4 sc =
             *reinterpret_cast<const f32x4*>(&s_al[buf][64 * wr + 32 * rb + 8 * qd + 4 * h]);
 #pragma unroll
-        for (int cb = 0; cb < 2; ++cb)
+        for (int cb = 0; cb < CB; ++cb)
 #pragma unroll
           for (int e = 0; e < 4; ++e)
             out[rb][cb][4 * qd + e] = fmaf(sc[e], acc[rb][cb][4 * qd + e], out[rb][cb][4 * qd + e]);
@@ -419,9 +424,9 @@ __global__ __launch_bounds__(256, 2) void ternary_gemm_kernel(TernArgs a) {
     __syncthreads();
   }
 
-  // Y[token][row]: lane column = token 64 wc + 32 cb + l32, register r = row
+  // Y[token][row]: lane column = token TT/2 wc + 32 cb + l32, register r = row
 #pragma unroll
-  for (int cb = 0; cb < 2; ++cb) {
+  for (int cb = 0; cb < CB; ++cb) {
     const int tok = tr[cb];
     if (tok >= tok_here) continue;
     OutT* yrow = reinterpret_cast<OutT*>(a.Y) + (m0 + tok) * a.ldy + n0;
@@ -480,36 +485,48 @@ catq_status launch_tern(const TernArgs& a, catq_dtype y_dtype, hipStream_t strea
 }
 
 // Which kernel: below 32 tokens always the decode kernel.  From there a
-// cost model fitted to both kernels on MI355X picks the cheaper:
-//  * tiled: every workgroup runs all n_chunks chunks at ~1.45 us each, one
-//    round per 256 workgroups (fewer than 256 still take a whole round);
+// cost model fitted to the kernels on MI355X picks the cheapest:
+//  * tiled, TT tokens per tile: n_chunks x max(the chunk latency of a lone
+//    workgroup, the workgroups on the fullest compute unit x what a unit
+//    takes per workgroup and chunk); 1.45 / 1.23 us for 128-token tiles,
+//    1.33 / 0.82 us for 64-token tiles;
 //  * decode: ~7.5e-15 s per weight and token (rows over 64 chunks, whose
 //    workgroups take eight waves, ~11e-15 s).
-// 14B-shaped layers at 64 / 128 / 256 / 512 tokens: gate|up tiled from 64,
-// q|k|v and down from 256, o from 512; at 256 tokens o measured 52.6 us
-// decode against 67.3 tiled, down 265 against 195.
-bool use_tiled(const TernArgs& a) {
-  if (a.M < 32 || a.ldx > (1 << 23)) return false;
-  const double wgs = (double)((a.d_out + kGT - 1) / kGT) * (double)((a.M + kGT - 1) / kGT);
-  const double tiled_us = a.n_chunks * 1.45 * (wgs > 256.0 ? wgs / 256.0 : 1.0);
-  const double decode_us =
+// 14B-shaped layers: gate|up tiled from 64 tokens, q|k|v and down from 256,
+// o from 512; 64-token tiles for q|k|v and down at 256 tokens (53 against
+// 66 us, 152 against 189) and gate|up at 64 (66 against 81), 128-token tiles
+// from 512 (down 195 against 205, gate|up at 2048 839 against 1118 us).
+// Returns 0 (decode), 64 or 128.
+int pick_kernel(const TernArgs& a) {
+  if (a.M < 32 || a.ldx > (1 << 23)) return 0;
+  const double rows = (double)((a.d_out + kGT - 1) / kGT);
+  auto tiled = [&](int tt, double lat, double thr) {
+    const double wgs = rows * (double)((a.M + tt - 1) / tt);
+    const double per = std::ceil(wgs / 256.0) * thr;
+    return a.n_chunks * (per > lat ? per : lat);
+  };
+  const double t128 = tiled(128, 1.45, 1.23), t64 = tiled(64, 1.33, 0.82);
+  const double decode =
       (double)a.M * (double)a.d_out * (double)a.d_in * (a.n_chunks > 64 ? 11e-9 : 7.5e-9);
-  return tiled_us < decode_us;
+  if (decode <= t128 && decode <= t64) return 0;
+  return t64 < t128 ? 64 : 128;
 }
 
+template <int TT>
 catq_status launch_tern_gemm(const TernArgs& a, catq_dtype y_dtype, hipStream_t stream) {
-  const dim3 grid((unsigned)((a.d_out + kGT - 1) / kGT), (unsigned)((a.M + kGT - 1) / kGT));
+  const dim3 grid((unsigned)((a.d_out + kGT - 1) / kGT), (unsigned)((a.M + TT - 1) / TT));
   const double flops = 2.0 * (double)a.M * (double)a.d_out * (double)a.d_in;
   const double bytes = (double)grid.y * ((double)a.d_out * (double)a.d_in / 4.0 +
                                          4.0 * (double)a.d_out * (double)(a.n_chunks >> a.cpg_shift)) +
                        2.0 * (double)a.M * (double)a.d_in +
                        (double)a.M * (double)a.d_out * (y_dtype == CATQ_F32 ? 4.0 : 2.0);
+  const char* tag = TT == 128 ? "ternary_gemm_kernel<128, 128>" : "ternary_gemm_kernel<128, 64>";
   if (y_dtype == CATQ_F32)
-    CATQ_TRACED(stream, "ternary_gemm_kernel<128, 128>", flops, bytes, a.M, a.d_out, a.d_in,
-                hipLaunchKernelGGL(ternary_gemm_kernel<float>, grid, dim3(256), 0, stream, a));
+    CATQ_TRACED(stream, tag, flops, bytes, a.M, a.d_out, a.d_in,
+                hipLaunchKernelGGL((ternary_gemm_kernel<TT, float>), grid, dim3(256), 0, stream, a));
   else
-    CATQ_TRACED(stream, "ternary_gemm_kernel<128, 128>", flops, bytes, a.M, a.d_out, a.d_in,
-                hipLaunchKernelGGL(ternary_gemm_kernel<bf16>, grid, dim3(256), 0, stream, a));
+    CATQ_TRACED(stream, tag, flops, bytes, a.M, a.d_out, a.d_in,
+                hipLaunchKernelGGL((ternary_gemm_kernel<TT, bf16>), grid, dim3(256), 0, stream, a));
   CATQ_CHECK_LAUNCH("ternary_linear");
   return CATQ_OK;
 }
@@ -556,9 +573,13 @@ extern "C" catq_status catq_ternary_linear(const void* X, int64_t M, int64_t ldx
   a.n_chunks = (int32_t)(d_in / 128);
   a.cpg_shift = __builtin_ctz((unsigned)(g / 128));
   a.Y = Y;
-  // Prefill-sized M: 128 x 128 tiles decode each code once per 128 tokens
-  // (their X offsets need 128 * ldx * 2 < 2^32).
-  if (use_tiled(a)) return launch_tern_gemm(a, y_dtype, stream);
+  // Prefill-sized M: tiles of 128 rows x 64 or 128 tokens decode each code
+  // once per tile (their X offsets need 128 * ldx * 2 < 2^32).
+  switch (pick_kernel(a)) {
+    case 128: return launch_tern_gemm<128>(a, y_dtype, stream);
+    case 64: return launch_tern_gemm<64>(a, y_dtype, stream);
+    default: break;
+  }
   // The product is bound by the decode's vector instructions, so what
   // matters is the work of the fullest compute unit: the workgroups it gets,
   // ceil(workgroups / 256), times what one costs, R tiles of 16 rows plus the

@@ -176,20 +176,23 @@ def _tile_rows(d_out, rng, n=48):
                              0, d_out - 1))
 
 
-# shapes on which the dispatch picks the tiled kernel (its cost model needs
-# about 1.5e6 output rows x tokens at rows of up to 64 chunks)
-@pytest.mark.parametrize("d_out,d_in,M,g", [
-    (4100, 384, 400, 128),     # ragged row and token tiles
-    (2000, 1024, 900, 256),    # two chunks per scale, eight token tiles (the last ragged)
-    (1600, 2048, 1000, 512),   # four chunks per scale
-    (640, 65536, 1700, 128)])  # the longest rows (512 chunks), 14 token tiles
-def test_ternary_linear_tiled_parity(catq, d_out, d_in, M, g):
-    """Prefill-sized M: the kernel of 128-row x 128-token tiles (named by the
-    trace), with padded X and Y rows, against the oracle on sampled rows."""
+# shapes on which the dispatch picks a tiled kernel (its cost model needs
+# about 1.5e6 output rows x tokens at rows of up to 64 chunks), with the
+# tokens per tile it picks
+@pytest.mark.parametrize("d_out,d_in,M,g,tt", [
+    (4100, 384, 400, 128, 64),      # ragged row and token tiles
+    (2000, 1024, 900, 256, 64),     # two chunks per scale, the last token tile ragged
+    (1600, 2048, 1000, 512, 64),    # four chunks per scale
+    (640, 65536, 1700, 128, 64),    # the longest rows (512 chunks)
+    (12800, 384, 1100, 128, 128)])  # 100 row tiles x 9 token tiles of 128, the last ragged
+def test_ternary_linear_tiled_parity(catq, d_out, d_in, M, g, tt):
+    """Prefill-sized M: the kernels of 128-row x 64- or 128-token tiles (named
+    by the trace), with padded X and Y rows, against the oracle on sampled
+    rows."""
     import torch
     packed, alpha, xb = _case(d_out, d_in, M, g, 12)
     y, tags = _traced_run(catq, packed, alpha, xb, g, torch.float32, ldx_pad=8, ldy_pad=3)
-    assert tags and tags[-1].startswith("ternary_gemm_kernel<128, 128>"), tags
+    assert tags and tags[-1] == f"ternary_gemm_kernel<128, {tt}>", tags
     got = host(y)
     assert np.isnan(got[:, d_out:]).all() and not np.isnan(got[:, :d_out]).any()
     rows = _tile_rows(d_out, np.random.default_rng([d_out, M]))
@@ -204,7 +207,7 @@ def test_ternary_linear_tiled_bf16_output_and_determinism(catq):
     import torch
     packed, alpha, xb = _case(4100, 384, 400, 128, 13)
     y, tags = _traced_run(catq, packed, alpha, xb, 128, torch.bfloat16)
-    assert tags[-1].startswith("ternary_gemm_kernel<128, 128>"), tags
+    assert tags[-1].startswith("ternary_gemm_kernel<128, "), tags
     rows = _tile_rows(4100, np.random.default_rng(13))
     xo = f64(xb)
     ref = ternary.ternary_linear(xo, packed[rows], alpha[rows], 384)
@@ -220,7 +223,7 @@ def test_ternary_linear_tiled_invalid_codes(catq):
     packed, alpha, xb = _case(4100, 512, 400, 128, 14)
     packed[129] = 0xFF                               # a row of invalid codes -> 0
     y, tags = _traced_run(catq, packed, alpha, xb, 128, torch.float32)
-    assert tags[-1].startswith("ternary_gemm_kernel<128, 128>"), tags
+    assert tags[-1].startswith("ternary_gemm_kernel<128, "), tags
     assert not torch.any(y[:, 129])
     rows = np.array([0, 128, 129, 130, 4099])
     ref = ternary.ternary_linear(f64(xb), packed[rows], alpha[rows], 512)
@@ -230,14 +233,15 @@ def test_ternary_linear_tiled_invalid_codes(catq):
 
 def test_ternary_linear_kernel_choice(catq):
     """Decode sizes stay on the decode kernel; the 14B-shaped gate|up takes
-    the tiled one from 64 tokens."""
+    64-token tiles at 64 tokens and 128-token tiles at 512."""
     import torch
-    for d_out, d_in, M, tiled in ((48, 384, 40, False), (34816, 5120, 16, False),
-                                  (34816, 5120, 64, True)):
+    for d_out, d_in, M, kern in ((48, 384, 40, "ternary_gemv_kernel<"),
+                                 (34816, 5120, 16, "ternary_gemv_kernel<"),
+                                 (34816, 5120, 64, "ternary_gemm_kernel<128, 64>"),
+                                 (34816, 5120, 512, "ternary_gemm_kernel<128, 128>")):
         packed, alpha, xb = _case(d_out, d_in, M, 128, 15)
         _, tags = _traced_run(catq, packed, alpha, xb, 128, torch.float32)
-        assert tags[-1].startswith("ternary_gemm_kernel" if tiled else "ternary_gemv_kernel"), \
-            (d_out, d_in, M, tags)
+        assert tags[-1].startswith(kern), (d_out, d_in, M, tags)
 
 
 @pytest.mark.slow
