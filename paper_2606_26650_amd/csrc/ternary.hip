@@ -19,6 +19,10 @@
 // 4 partial outputs per lane and tile are scaled by alpha/2 (the factor 2 of
 // the decode is exact) and accumulated in fp32.  The scales of the
 // workgroup's rows are staged in LDS once.
+//
+// Prefill-sized M takes a second kernel (ternary_gemm_kernel below) whose
+// workgroups tile 128 rows x 64 or 128 tokens, so each code is decoded once
+// per tile; the host picks the kernel by a fitted cost model.
 
 #include <cmath>
 #include <cstdint>
