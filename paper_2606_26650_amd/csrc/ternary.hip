@@ -584,8 +584,7 @@ extern "C" catq_status catq_ternary_linear(const void* X, int64_t M, int64_t ldx
     case 64: return launch_tern_gemm<64>(a, y_dtype, stream);
     default: break;
   }
-  // The product is bound by the decode's vector instructions, so what
-  // matters is the work of the fullest compute unit: the workgroups it gets,
+  // What matters is the work of the fullest compute unit: the workgroups it gets,
   // ceil(workgroups / 256), times what one costs, R tiles of 16 rows plus the
   // X loads that serve all R (worth about 0.3 tile at one to four tokens,
   // whose other token lanes read nothing, and 1.5 tiles beyond).  Of R = 2..5
