@@ -231,6 +231,30 @@ def test_ternary_linear_tiled_invalid_codes(catq):
                                                            512, 128, 4))
 
 
+@pytest.mark.parametrize("d_out,d_in,M,kern", [(48, 384, 5, "ternary_gemv_kernel<"),
+                                                (4100, 384, 400, "ternary_gemm_kernel<")])
+def test_ternary_linear_nan_stays_in_its_token(catq, d_out, d_in, M, kern):
+    """A NaN in one token's input makes every output of that token NaN (the
+    products take it through x * 0 as well) and leaves the other tokens
+    finite and at parity, in both kernels."""
+    import torch
+    packed, alpha, xb = _case(d_out, d_in, M, 128, 16)
+    xb = xb.copy()
+    bad = M // 2
+    xb[bad, d_in // 3] = 0x7FC0                      # bf16 quiet NaN
+    y, tags = _traced_run(catq, packed, alpha, xb, 128, torch.float32)
+    assert tags[-1].startswith(kern), tags
+    got = host(y)
+    assert np.isnan(got[bad]).all()
+    others = np.delete(np.arange(M), bad)
+    assert np.isfinite(got[others]).all()
+    rows = np.array([0, d_out // 2, d_out - 1])
+    xo = f64(xb[others])
+    ref = ternary.ternary_linear(xo, packed[rows], alpha[rows], d_in)
+    assert np.all(np.abs(got[np.ix_(others, rows)] - ref)
+                  <= _bound(xo, packed[rows], alpha[rows], d_in, 128, d_in // 128))
+
+
 def test_ternary_linear_kernel_choice(catq):
     """Decode sizes stay on the decode kernel; the 14B-shaped gate|up takes
     64-token tiles at 64 tokens and 128-token tiles at 512."""
