@@ -24,6 +24,7 @@
 // workgroups tile 128 rows x 64 or 128 tokens, so each code is decoded once
 // per tile; the host picks the kernel by a fitted cost model.
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <type_traits>
@@ -114,14 +115,15 @@ constexpr int kOutOfRange = 0x40000000;   // offset past every slice this kernel
 //    and whole quads of chunks per row (VEC), a thread takes four
 //    consecutive scales of a row per 16-byte load (AMAX / 4 loads).
 // Dynamic LDS: n_chunks * (RT + 4) floats.
-template <int NW, int R, int D, int AMAX, bool VEC, typename OutT>
+template <int NW, int R, int D, int AMAX, bool VEC, bool XL, typename OutT>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4)))
 void ternary_gemv_kernel(TernArgs a) {
   constexpr int RT = 16 * R;   // rows of the workgroup
   constexpr int AP = RT + 4;   // pitch of the staged scales (floats; 16-byte rows)
   constexpr int S = D + 1;     // register slots of the ring
   extern __shared__ __align__(16) float s_alpha[];
-  __shared__ float s_red[NW][16][RT + 1];  // [wave][token][row]
+  // [wave][token][row] partial outputs; with X in LDS they reuse its space
+  __shared__ float s_red_own[XL ? 1 : NW][16][RT + 1];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar branches
@@ -135,6 +137,25 @@ void ternary_gemv_kernel(TernArgs a) {
   const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<bf16*>(a.X + m0 * a.ldx), 0, (int)(tok_here * a.ldx * 2), kBufferFlags);
   const int xoff = c16 < tok_here ? (int)((c16 * a.ldx + 32 * q) * 2) : kOutOfRange;
+  // XL (at most four tokens): the workgroup's X rows are copied once into LDS
+  // past the scales ([token][d_in] bf16, 16-byte slots, padded to whole
+  // copies), before the scales are loaded, so that the wait for the scales
+  // covers the copies; the ring then carries codes only, and the products
+  // read X from LDS.  (Per chunk and wave, X loads cost as much as the codes
+  // at one token, where 15 of 16 token lanes read nothing.)
+  uint4* s_x = reinterpret_cast<uint4*>(s_alpha + a.n_chunks * AP);
+  float (*s_red)[16][RT + 1] =
+      XL ? reinterpret_cast<float (*)[16][RT + 1]>(s_x) : s_red_own;
+  if constexpr (XL) {
+    const i32x4_rsrc xb = buf_rsrc(a.X + m0 * a.ldx, (uint32_t)(tok_here * a.ldx * 2));
+    const int row_slots = a.n_chunks * 16, slots = tok_here * row_slots;
+    for (int i = wave; i * 64 < slots; i += NW) {
+      const int sl = i * 64 + lane, t = sl / row_slots;
+      const uint32_t off =
+          sl < slots ? (uint32_t)(t * a.ldx * 2 + (sl - t * row_slots) * 16) : (uint32_t)kOutOfRange;
+      dma16_buf(xb, off, 0u, s_x + i * 64);
+    }
+  }
   const int rows_here = (int)min<int64_t>(RT, a.d_out - n0);
   const __amdgpu_buffer_rsrc_t pr = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint8_t*>(a.P + n0 * row_bytes), 0, (int)(rows_here * row_bytes), kBufferFlags);
@@ -175,13 +196,15 @@ void ternary_gemv_kernel(TernArgs a) {
   // end re-read it; a wave without chunks reads chunk 0), never multiplied
   const int last = my > 0 ? wave + NW * (my - 1) : 0;
   uint2 cw[S][R];
-  u32x4 xv[S][4];
+  [[maybe_unused]] u32x4 xv[S][4];
   auto issue = [&](int k, auto slot_c) {
     constexpr int s = decltype(slot_c)::value;
     const int ch = min(wave + NW * k, last);
+    if constexpr (!XL) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      xv[s][j] = __builtin_amdgcn_raw_buffer_load_b128(xr, xoff + 16 * j, ch * 256, 0);
+      for (int j = 0; j < 4; ++j)
+        xv[s][j] = __builtin_amdgcn_raw_buffer_load_b128(xr, xoff + 16 * j, ch * 256, 0);
+    }
 #pragma unroll
     for (int r = 0; r < R; ++r)
       cw[s][r] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(pr, poff[r], ch * 32, 0));
@@ -214,16 +237,25 @@ void ternary_gemv_kernel(TernArgs a) {
   auto compute = [&](int k, auto slot_c) {
     constexpr int i = decltype(slot_c)::value;
     const float* al = &s_alpha[(wave + NW * k) * AP + 4 * q];
+    u32x4 xf[4];   // X of the chunk: lane (q, c16) holds token c16, k 32 q .. 32 q + 31
+    if constexpr (XL) {
+      const uint4* xp = s_x + min(c16, tok_here - 1) * (nch * 16) + (wave + NW * k) * 16 + 4 * q;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) xf[j] = __builtin_bit_cast(u32x4, xp[j]);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) xf[j] = xv[i][j];
+    }
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       u32x4 w0, w1, w2, w3;
       decode16(cw[i][r].x, w0, w1);
       decode16(cw[i][r].y, w2, w3);
       f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(w0), as_bf16x8(xv[i][0]), acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(w1), as_bf16x8(xv[i][1]), acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(w2), as_bf16x8(xv[i][2]), acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(w3), as_bf16x8(xv[i][3]), acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(w0), as_bf16x8(xf[0]), acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(w1), as_bf16x8(xf[1]), acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(w2), as_bf16x8(xf[2]), acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(w3), as_bf16x8(xf[3]), acc, 0, 0, 0);
       // accumulator: rows 16 r + 4q .. +3 of the workgroup, token c16
       const f32x4 sc = *reinterpret_cast<const f32x4*>(al + 16 * r);
 #pragma unroll
@@ -246,7 +278,9 @@ void ternary_gemv_kernel(TernArgs a) {
     if (full + I() < my) compute(full + I(), I);
   });
 
-  // fixed-order reduction over the waves
+  // fixed-order reduction over the waves (with X in LDS, once every wave has
+  // finished reading it)
+  if constexpr (XL) __syncthreads();
 #pragma unroll
   for (int r = 0; r < R; ++r)
 #pragma unroll
@@ -460,29 +494,42 @@ catq_status launch_tern(const TernArgs& a, catq_dtype y_dtype, hipStream_t strea
                CATQ_ERR_SHAPE, "ternary_linear: no launch shape for d_in = %lld",
                (long long)a.d_in);
   const dim3 grid((unsigned)((a.d_out + RT - 1) / RT), (unsigned)((a.M + 15) / 16));
-  const size_t lds = (size_t)a.n_chunks * (RT + 4) * sizeof(float);
+  const size_t lds_scales = (size_t)a.n_chunks * (RT + 4) * sizeof(float);
+  // X in LDS for at most four tokens, where it fits beside the scales: whole
+  // copies of 64 slots of 16 bytes
+  // (the reduction's partial outputs then reuse the X space)
+  const size_t red = sizeof(float) * NW * 16 * (RT + 1);
+  const size_t lds_x = a.M <= 4 ? (size_t)((a.M * a.n_chunks * 16 + 63) / 64) * 64 * 16 : 0;
+  const bool xl = lds_x > 0 && lds_scales + std::max(lds_x, red) <= 65536;
+  const size_t lds = lds_scales + (xl ? std::max(lds_x, red) : 0);
   const double flops = 2.0 * (double)a.M * (double)a.d_out * (double)a.d_in;
   const double bytes = (double)a.d_out * (double)a.d_in / 4.0 +
                        4.0 * (double)a.d_out * (double)(a.n_chunks >> a.cpg_shift) +
                        2.0 * (double)a.M * (double)a.d_in +
                        (double)a.M * (double)a.d_out * (y_dtype == CATQ_F32 ? 4.0 : 2.0);
   static char tag[64];
-  snprintf(tag, sizeof tag, "ternary_gemv_kernel<%d, %d, %d>", NW, R, D);
-  auto launch = [&](auto vec_c, auto out_c) {
-    constexpr bool V = decltype(vec_c)::value;
+  snprintf(tag, sizeof tag, "ternary_gemv_kernel<%d, %d, %d%s>", NW, R, D, xl ? ", x in lds" : "");
+  auto launch = [&](auto vec_c, auto xl_c, auto out_c) {
+    constexpr bool V = decltype(vec_c)::value, X = decltype(xl_c)::value;
     using OutT = typename decltype(out_c)::type;
     CATQ_TRACED(stream, tag, flops, bytes, a.M, a.d_out, a.d_in,
-                hipLaunchKernelGGL((ternary_gemv_kernel<NW, R, D, AMAX, V, OutT>), grid,
+                hipLaunchKernelGGL((ternary_gemv_kernel<NW, R, D, AMAX, V, X, OutT>), grid,
                                    dim3(NW * 64), lds, stream, a));
   };
-  using Vt = std::true_type;
-  using Vf = std::false_type;
-  if (y_dtype == CATQ_F32) {
-    if (vec) launch(Vt{}, OutTag<float>{});
-    else launch(Vf{}, OutTag<float>{});
+  auto with_out = [&](auto vec_c, auto xl_c) {
+    if (y_dtype == CATQ_F32)
+      launch(vec_c, xl_c, OutTag<float>{});
+    else
+      launch(vec_c, xl_c, OutTag<bf16>{});
+  };
+  using Tt = std::true_type;
+  using Tf = std::false_type;
+  if (vec) {
+    if (xl) with_out(Tt{}, Tt{});
+    else with_out(Tt{}, Tf{});
   } else {
-    if (vec) launch(Vt{}, OutTag<bf16>{});
-    else launch(Vf{}, OutTag<bf16>{});
+    if (xl) with_out(Tf{}, Tt{});
+    else with_out(Tf{}, Tf{});
   }
   CATQ_CHECK_LAUNCH("ternary_linear");
   return CATQ_OK;
