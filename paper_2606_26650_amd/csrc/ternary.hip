@@ -103,7 +103,8 @@ constexpr int kOutOfRange = 0x40000000;   // offset past every slice this kernel
 // in a fixed order.
 //  * X crosses the vector memory path once per chunk and wave and serves all
 //    R tiles (at one token, 15 of the 16 token lanes read out of range: no
-//    traffic, but the lanes still return data, so that return is shared).
+//    traffic, but the lanes still return data, so that return is shared);
+//    with up to four tokens (XL) it is instead copied into LDS once.
 //  * The codes and X of chunk k + D are issued while chunk k is multiplied:
 //    a ring of D + 1 register slots keeps D chunks of every wave in flight.
 //    Code loads are raw buffer loads over the tile's rows (wave-uniform base
